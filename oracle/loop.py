@@ -1,0 +1,107 @@
+"""Anchor-cache inference, Algorithm 1 (oracle; test infrastructure only).
+
+For i = T .. 1: c_i = S(z_i); if (T - i) mod K == 0 the anchor is refreshed,
+h_cache = A(c_i); h~_i = Phi(c_i, h_cache); x^_i = D(h~_i); z_{i-1} ~ P(z_i, x^_i, i).
+
+The sampler P reveals n_i = floor(M0 i / T) - floor(M0 (i-1) / T) masked positions
+at step i, so that exactly floor(M0 (i-1)/T) stay masked afterwards: the integer
+form of the linear schedule alpha_t = 1 - t on the grid t(i) = i/T (Sec. 2.1), with
+alpha_0 = 1 making the last step reveal everything.
+
+Single-canvas mode (block_len == gen_len): the prompt and the canvas form one
+bidirectional sequence.  Block mode (block_len < gen_len): the prompt is block 0,
+run once as a fresh pass whose per-layer K, V become the context; each block of
+``block_len`` positions is then denoised for T steps attending to the context and
+to itself, and once finished is appended to the context by another fresh pass
+(bidirectional within a block, causal across blocks).  The refresh counter
+restarts at each block.  Each reverse step has id block*T + (T - i).
+
+``net`` provides shared / anchor_cache / fuse / denoise / head / fresh_kv on one
+row (``oracle.network.Network``); ``counts`` records layer calls in the units of
+the paper's compute count (one call per layer per step for the batch).
+"""
+import numpy as np
+
+from . import sampler as smp
+
+
+def unmask_count(M0, i, T):
+    return (M0 * i) // T - (M0 * (i - 1)) // T
+
+
+def is_refresh(i, T, K):
+    return (T - i) % K == 0
+
+
+class Counts:
+    def __init__(self):
+        self.anchor_refreshes = 0
+        self.layer_calls = 0
+        self.steps = 0
+
+
+def generate(net, prompt, gen_len, T, K, block_len, seed, temperature, mask_id,
+             counts=None, trace=None, sample_fn=None):
+    """Run Algorithm 1 on every row of ``prompt`` [B, P]; returns tokens [B, P+gen_len].
+
+    ``trace`` (list) receives per-step dicts (i, step_id, refresh, canvas before the
+    step) for tests; ``sample_fn`` replaces the reverse step (used by counting tests).
+    """
+    cfg = net.cfg
+    prompt = np.asarray(prompt, dtype=np.int64)
+    B, P = prompt.shape
+    if gen_len % block_len != 0 or T < 1 or K < 1:
+        raise ValueError("invalid generation arguments")
+    Ls, La, Ld = cfg["n_shared"], cfg["n_anchor"], cfg["n_denoise"]
+    inv_temp = np.float32(1.0 / float(temperature))
+    seq = np.concatenate([prompt, np.full((B, gen_len), mask_id, dtype=np.int64)], axis=1)
+    single = block_len == gen_len
+    if single:
+        windows = [(0, P, P + gen_len)]
+        ctx = [None] * B
+    else:
+        windows = [(P + j * block_len, P + j * block_len, P + (j + 1) * block_len)
+                   for j in range(gen_len // block_len)]
+        ctx = [net.fresh_kv(seq[b, :P], np.arange(P)) if P > 0 else None for b in range(B)]
+        if counts is not None and P > 0:
+            counts.layer_calls += Ls + La + Ld
+    sample = sample_fn or smp.reverse_step
+    for j, (w0, c0, w1) in enumerate(windows):
+        pos = np.arange(w0, w1)
+        M0 = int((seq[0, c0:w1] == mask_id).sum())
+        caches = [None] * B
+        for i in range(T, 0, -1):
+            step_id = j * T + (T - i)
+            n = unmask_count(M0, i, T)
+            refresh = is_refresh(i, T, K)
+            if trace is not None:
+                trace.append(dict(block=j, i=i, step_id=step_id, refresh=refresh, n=n,
+                                  canvas=seq[:, w0:w1].copy()))
+            if counts is not None:
+                counts.steps += 1
+                counts.layer_calls += Ls + Ld + (La if refresh else 0)
+                counts.anchor_refreshes += int(refresh)
+            for b in range(B):
+                c = net.shared(seq[b, w0:w1], pos, ctx[b])
+                if refresh:
+                    caches[b] = net.anchor_cache(c, pos, ctx[b])
+                ht = net.fuse(c, caches[b])
+                xf = net.denoise(ht, pos, ctx[b])
+                logits = net.head(xf[c0 - w0:]).astype(np.float32)
+                nxt, _, _ = sample(logits, seq[b, c0:w1], mask_id, n, c0, b, step_id,
+                                   seed, inv_temp)
+                seq[b, c0:w1] = nxt
+        if not single:
+            for b in range(B):
+                kv = net.fresh_kv(seq[b, w0:w1], pos, ctx[b])
+                ctx[b] = kv if ctx[b] is None else {
+                    li: (np.concatenate([ctx[b][li][0], kv[li][0]]),
+                         np.concatenate([ctx[b][li][1], kv[li][1]])) for li in kv}
+            if counts is not None:
+                counts.layer_calls += Ls + La + Ld
+    return seq
+
+
+def layer_call_count(T, K, L_shared, L_anchor, L_denoise):
+    """Closed form of eq. anchor-cache-compute: T (L_S + L_D) + ceil(T/K) L_A."""
+    return T * (L_shared + L_denoise) + -(-T // K) * L_anchor

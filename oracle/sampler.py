@@ -1,0 +1,170 @@
+"""Masked-diffusion reverse step with confidence-ranked unmasking (oracle).
+
+Semantics (App. B.1.1, MDLM posterior with zero-masking and carry-over, sigma_t = 0):
+a position that is already decoded keeps its token; a masked position may only
+become a real token (the head has no column for the mask id).  Which masked
+positions are revealed at step i follows the linear schedule: n_i positions, the
+ones whose sampled token is most confident.
+
+Sampling contract, identical on CPU and GPU so that token choices and unmask
+order can be compared bit for bit.  Every decision is taken in IEEE float32 with
+individually rounded +, -, *, / (no fused multiply-add):
+
+* uniform u for (row b, absolute position l, vocab entry v, step id) is word
+  (v mod 4) of Philox4x32-10 (Salmon et al., SC'11) at counter
+  (v div 4, l, b, step_id) with key (seed low 32 bits, seed high 32 bits), mapped
+  to u = (2*(x >> 9) + 1) * 2^-24, which lies in [2^-24, 1 - 2^-24];
+* Gumbel noise G = -log(-log u); the token is argmax_v (l_v * inv_temp + G_v) with
+  ties broken towards the smaller v (Gumbel-max sampling from softmax(l/temp));
+* confidence = log-softmax of the chosen token at temperature temp, with the
+  normaliser summed exactly in 64-bit fixed point:
+  S = sum_v rint(exp(l'_v - m) * 2^40), conf = (l'_x - m) - log(float(S) * 2^-40),
+  where l' = l * inv_temp and m = max l' (terms with l'_v - m < -30 are 0);
+* ranking key: confidence descending, then position ascending.
+
+``log32`` and ``exp32`` are this module's own float32 logarithm and exponential:
+exponent/mantissa split with the mantissa in [sqrt(1/2), sqrt(2)] and the series
+log m = 2 atanh(s), s = (m-1)/(m+1); exponential by Cody-Waite reduction with
+ln2 split into a 15-bit head and a tail, and the degree-7 Taylor polynomial.
+"""
+import numpy as np
+
+U32 = np.uint32
+F32 = np.float32
+
+# Philox4x32 round multipliers and Weyl key increments (Salmon et al., SC'11).
+PHILOX_M0, PHILOX_M1 = 0xD2511F53, 0xCD9E8D57
+PHILOX_W0, PHILOX_W1 = 0x9E3779B9, 0xBB67AE85
+
+
+def philox4x32_10(c0, c1, c2, c3, k0, k1):
+    """Ten Philox4x32 rounds; all arguments uint32 (broadcastable arrays)."""
+    c = [np.asarray(x, dtype=np.uint64) for x in (c0, c1, c2, c3)]
+    k0 = np.uint64(k0) if np.isscalar(k0) else np.asarray(k0, dtype=np.uint64)
+    k1 = np.uint64(k1) if np.isscalar(k1) else np.asarray(k1, dtype=np.uint64)
+    mask = np.uint64(0xFFFFFFFF)
+    for rnd in range(10):
+        if rnd > 0:
+            k0 = (k0 + np.uint64(PHILOX_W0)) & mask
+            k1 = (k1 + np.uint64(PHILOX_W1)) & mask
+        p0 = np.uint64(PHILOX_M0) * c[0]
+        p1 = np.uint64(PHILOX_M1) * c[2]
+        hi0, lo0 = p0 >> np.uint64(32), p0 & mask
+        hi1, lo1 = p1 >> np.uint64(32), p1 & mask
+        c = [hi1 ^ c[1] ^ k0, lo1, hi0 ^ c[3] ^ k1, lo0]
+    return [x.astype(U32) for x in c]
+
+
+def bits_to_uniform(x):
+    """u = (2*(x >> 9) + 1) * 2^-24 (exact in float32; never 0 or 1)."""
+    k = (np.asarray(x, dtype=U32) >> U32(9)).astype(np.int64) * 2 + 1
+    return k.astype(F32) * F32(2.0 ** -24)
+
+
+# float32 constants, given by their bit patterns.
+def _f(bits):
+    return np.array([bits], dtype=U32).view(F32)[0]
+
+
+LN2_HI = _f(0x3F317200)      # 0.693145751953125 (15 significant bits)
+LN2_LO = _f(0x35BFBE8E)      # ln 2 - LN2_HI
+INV_LN2 = _f(0x3FB8AA3B)     # 1/ln 2
+SQRT2_BITS = 0x3FB504F3      # float32 nearest sqrt(2)
+# log: s * (2 + 2/3 z + 2/5 z^2 + 2/7 z^3 + 2/9 z^4 + 2/11 z^5), z = s^2
+LOG_C = [_f(0x3E3A2E8C), _f(0x3E638E39), _f(0x3E924925), _f(0x3ECCCCCD), _f(0x3F2AAAAB)]
+# exp: 1 + r + r^2/2 + ... + r^7/7!
+EXP_C = [_f(0x39500D01), _f(0x3AB60B61), _f(0x3C088889), _f(0x3D2AAAAB), _f(0x3E2AAAAB)]
+EXP_CUTOFF = F32(-30.0)
+
+
+def log32(x):
+    """Natural log of positive normal float32 values, in float32 arithmetic."""
+    x = np.asarray(x, dtype=F32)
+    bits = x.view(U32)
+    e = (bits >> U32(23)).astype(np.int32) - 127
+    mb = (bits & U32(0x007FFFFF)) | U32(0x3F800000)
+    big = mb > U32(SQRT2_BITS)
+    mb = np.where(big, mb - U32(0x00800000), mb).astype(U32)
+    e = e + big.astype(np.int32)
+    m = mb.view(F32)
+    f = m - F32(1.0)
+    s = f / (F32(2.0) + f)
+    z = s * s
+    p = LOG_C[0]
+    for c in LOG_C[1:]:
+        p = p * z + c
+    p = p * z + F32(2.0)
+    t = s * p
+    ef = e.astype(F32)
+    return (ef * LN2_HI + (ef * LN2_LO + t)).astype(F32)
+
+
+def exp32(y):
+    """exp(y) for float32 y <= 0, in float32 arithmetic; 0 below -30."""
+    y = np.asarray(y, dtype=F32)
+    yc = np.maximum(y, EXP_CUTOFF)
+    k = np.rint(yc * INV_LN2).astype(F32)
+    r = (yc - k * LN2_HI) - k * LN2_LO
+    p = EXP_C[0]
+    for c in EXP_C[1:]:
+        p = p * r + c
+    p = p * r + F32(0.5)
+    p = p * r + F32(1.0)
+    p = p * r + F32(1.0)
+    scale = ((k.astype(np.int32) + 127).astype(U32) << U32(23)).view(F32)
+    return np.where(y < EXP_CUTOFF, F32(0.0), p * scale).astype(F32)
+
+
+def uniforms(V, pos, row, step_id, seed):
+    """u[v] for one (row, position, step): Philox words laid out over the vocabulary."""
+    n_ctr = (V + 3) // 4
+    c0 = np.arange(n_ctr, dtype=U32)
+    w = philox4x32_10(c0, U32(pos), U32(row), U32(step_id),
+                      U32(seed & 0xFFFFFFFF), U32((seed >> 32) & 0xFFFFFFFF))
+    words = np.stack(w, axis=1).reshape(-1)[:V]
+    return bits_to_uniform(words)
+
+
+def sample_position(logits_row, inv_temp, pos, row, step_id, seed):
+    """(token, confidence) for one masked position; logits_row is float32 [V]."""
+    lg = np.asarray(logits_row, dtype=F32)
+    V = lg.shape[0]
+    lp = lg * F32(inv_temp)
+    u = uniforms(V, pos, row, step_id, seed)
+    gumbel = -log32(-log32(u))
+    score = lp + gumbel
+    tok = int(np.argmax(score))            # first maximum: smallest v on ties
+    m = lp.max()
+    e = exp32(lp - m)
+    S = int(np.sum(np.rint(e * F32(2.0 ** 40)).astype(np.int64)))
+    norm = F32(np.int64(S).astype(F32)) * F32(2.0 ** -40)
+    conf = F32(lp[tok] - m) - log32(np.array([norm], dtype=F32))[0]
+    return tok, F32(conf)
+
+
+def rank_order(conf, candidates):
+    """Candidate positions ordered by (confidence desc, position asc)."""
+    cand = np.flatnonzero(candidates)
+    order = np.lexsort((cand, -conf[cand].astype(np.float64)))
+    return cand[order]
+
+
+def reverse_step(logits, canvas, mask_id, n_unmask, pos0, row, step_id, seed, inv_temp):
+    """One reverse step for one row of the active canvas.
+
+    logits [Lc, V] float32 (all canvas positions), canvas [Lc] ints, pos0 = absolute
+    position of canvas entry 0.  Returns (next canvas, choice, conf); choice/conf
+    are -1 / -inf at positions that are not masked.
+    """
+    canvas = np.asarray(canvas)
+    Lc = canvas.shape[0]
+    masked = canvas == mask_id
+    choice = np.full(Lc, -1, dtype=np.int64)
+    conf = np.full(Lc, -np.inf, dtype=F32)
+    for j in np.flatnonzero(masked):
+        choice[j], conf[j] = sample_position(logits[j], inv_temp, pos0 + j, row, step_id, seed)
+    n = min(int(n_unmask), int(masked.sum()))
+    sel = rank_order(conf, masked)[:n]
+    nxt = canvas.copy()
+    nxt[sel] = choice[sel]
+    return nxt, choice, conf
