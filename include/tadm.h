@@ -1,0 +1,193 @@
+/*
+ * tadm.h -- C ABI of the MI355X (gfx950) implementation of the reverse-diffusion
+ * step of Time-Anchored Diffusion Models (TADM).
+ *
+ * The method (Sec. 3.1, eq. DenoiserOp): a shared network S maps the current
+ * canvas z_t to c_t = S(z_t); an expensive anchor network A produces
+ * h_t' = A(S(z_t')) only at refresh steps and the result is cached; every reverse
+ * step runs the fusion module h~ = Phi(c_t, h_t'), the lightweight denoiser D and
+ * the vocabulary head, then the masked-diffusion reverse step.  Anchor-cache
+ * inference (Algorithm 1) refreshes the cache at reverse step i iff
+ * (T - i) mod K == 0.
+ *
+ * Conventions shared by every call:
+ *  - Array arguments named *_dev are device pointers (HIP device memory of the
+ *    model's device).  Token ids are int32, hidden states and logits float32.
+ *  - The mask token id is cfg.vocab; real token ids are in [0, cfg.vocab).
+ *  - All work is enqueued on the model's stream (tadm_set_stream); calls return
+ *    without synchronising unless stated.  Inputs must stay valid until the
+ *    enqueued work completes.  Outputs are caller-allocated.
+ *  - Arguments are validated on the host before anything is enqueued; an invalid
+ *    argument returns TADM_ERR_INVALID and has no side effects.  A cache or
+ *    context built for another model or shape returns TADM_ERR_STATE.  HIP
+ *    failures return TADM_ERR_DEVICE.  tadm_last_error() then describes the
+ *    failure.  No call aborts the process.
+ *  - Objects (model, cache, context) are opaque, created and destroyed by the
+ *    caller.  A cache or context must be destroyed before its model.
+ */
+#ifndef TADM_H
+#define TADM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TADM_OK = 0,
+  TADM_ERR_INVALID = 1,      /* bad argument (shape, range, null pointer)          */
+  TADM_ERR_OOM = 2,          /* device allocation failed                           */
+  TADM_ERR_DEVICE = 3,       /* HIP runtime error                                  */
+  TADM_ERR_STATE = 4,        /* object mismatch, weights missing, wrong model      */
+  TADM_ERR_UNSUPPORTED = 5   /* valid request this build does not implement        */
+} tadm_status;
+
+enum { TADM_DTYPE_F32 = 0, TADM_DTYPE_BF16 = 1 };
+enum { TADM_FFN_GELU = 0, TADM_FFN_SWIGLU = 1, TADM_FFN_GEGLU = 2 };
+/* Fusion Phi: gated residual MLP (App. C.2) or paired attention (App. C.1). */
+enum { TADM_FUSION_GATED_MLP = 0, TADM_FUSION_PAIRED = 1 };
+
+/* Model shape.  Layers are numbered shared [0, n_shared), anchor, then denoiser.
+ * dtype is the storage/operand type of weights and GEMM/attention operands; the
+ * residual stream, norm statistics, softmax, logits and the sampler are float32.
+ * max_batch x max_seq bounds every call (positions include any context). */
+typedef struct {
+  int32_t vocab, d_model, n_heads, n_kv_heads, head_dim, d_ffn, ffn_kind;
+  int32_t n_shared, n_anchor, n_denoise, fusion_kind, fusion_rank, paired_heads;
+  int32_t dtype, max_batch, max_seq;
+  float rms_eps;     /* RMSNorm epsilon of the transformer layers / paired scales */
+  float ln_eps;      /* LayerNorm epsilon of the gated-MLP fusion                  */
+  float rope_theta;  /* rotary base                                               */
+} tadm_config;
+
+typedef struct tadm_model tadm_model;
+typedef struct tadm_cache tadm_cache;
+typedef struct tadm_context tadm_context;
+
+/* Arguments of one reverse step (Sec. 2.1 time grid t(i) = i/T). */
+typedef struct {
+  int32_t i, T;        /* reverse step i in [1, T]                                   */
+  int32_t n_unmask;    /* masked positions revealed per row (clamped per row)        */
+  uint32_t step_id;    /* Philox counter word: block * T + (T - i) in tadm_generate  */
+  uint64_t seed;       /* Philox key                                                 */
+  float inv_temp;      /* 1 / temperature, > 0                                       */
+} tadm_step_args;
+
+/* ---------------------------------------------------------------- model ---- */
+/* Number of weight tensors of a configuration, and the shape of tensor `index`
+ * (matrices [rows = out features, cols = in features]; vectors cols = 0).
+ * Order: embed [V+1, d], final_norm [d], w_out [V, d], the fusion tensors, then
+ * per layer attn_norm, wq, wk, wv, wo, ffn_norm, (w_gate,) w_up, w_down. */
+int32_t tadm_weight_count(const tadm_config* cfg);
+tadm_status tadm_weight_info(const tadm_config* cfg, int32_t index, int64_t* rows, int64_t* cols);
+
+/* Creates a model on the current HIP device and allocates its weight arena. */
+tadm_status tadm_model_create(const tadm_config* cfg, tadm_model** out);
+/* Copies weight `index` (elements of cfg.dtype, row-major, `bytes` long) from
+ * host (src_on_device = 0) or device memory into the model's own layout.
+ * Synchronous.  Every tensor must be loaded before a compute call. */
+tadm_status tadm_model_load_weight(tadm_model* m, int32_t index, const void* src, size_t bytes,
+                                   int32_t src_on_device);
+tadm_status tadm_model_destroy(tadm_model* m);
+/* Stream for all later work of this model (a hipStream_t; NULL = default stream). */
+tadm_status tadm_set_stream(tadm_model* m, void* hip_stream);
+
+/* ---------------------------------------------------------------- cache ---- */
+/* Anchor cache for B rows x L positions (Algorithm 1's h^cache plus refresh index).
+ * Fields: TADM_CACHE_H   anchor output h' = A(c')            float32 [B, L, d]
+ *         TADM_CACHE_C   shared state c' at the refresh      float32 [B, L, d]
+ *         TADM_CACHE_A   LN_a(h') (gated-MLP fusion input)   dtype   [B, L, d] */
+enum { TADM_CACHE_H = 0, TADM_CACHE_C = 1, TADM_CACHE_A = 2 };
+tadm_status tadm_cache_create(tadm_model* m, int32_t B, int32_t L, tadm_cache** out);
+tadm_status tadm_cache_destroy(tadm_cache* c);
+/* Enqueues a copy of one field into dst_dev (bytes must equal the field size). */
+tadm_status tadm_cache_read(const tadm_cache* c, int32_t field, void* dst_dev, size_t bytes);
+/* Reverse step index i of the last refresh (0 = never refreshed). */
+int32_t tadm_cache_refresh_step(const tadm_cache* c);
+
+/* -------------------------------------------------------------- context ---- */
+/* Block diffusion: per-layer K, V of the prompt and finished blocks, attended by
+ * later blocks (bidirectional within a block, causal across blocks). */
+tadm_status tadm_context_create(tadm_model* m, int32_t B, int32_t max_ctx, tadm_context** out);
+/* Fresh pass (a refresh step: S, A, Phi with the fresh anchor, D) over n clean
+ * tokens per row [B, n] at positions [len, len + n); appends every layer's K, V. */
+tadm_status tadm_context_append(tadm_model* m, tadm_context* ctx, const int32_t* tokens_dev,
+                                int32_t B, int32_t n);
+int32_t tadm_context_length(const tadm_context* ctx);
+tadm_status tadm_context_reset(tadm_context* ctx);
+tadm_status tadm_context_destroy(tadm_context* ctx);
+
+/* ------------------------------------------------------------ the step ---- */
+/* Anchor refresh (Alg. 1): c = S(canvas), h = A(c), written to `cache`.
+ * canvas_dev [B, L] is the window at positions [ctx_len, ctx_len + L) (ctx may be
+ * NULL: positions [0, L)).  (i, T) is recorded as the refresh step. */
+tadm_status tadm_anchor_forward(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev,
+                                int32_t B, int32_t L, int32_t i, int32_t T, tadm_cache* cache);
+
+/* One reverse step on a stale (or fresh) cache (Sec. 3.1, eq. DenoiserOp;
+ * MDLM posterior with carry-over, App. B.1.1):
+ * c = S(canvas), h~ = Phi(c, cache), x = D(h~), logits = head(x) for the canvas
+ * columns [canvas_off, L), then tadm_sample.  logits_dev (float32
+ * [B, L - canvas_off, V]) may be NULL; next_canvas_dev [B, L] receives the canvas
+ * after the step.  The cache is read only. */
+tadm_status tadm_denoise_step(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev,
+                              int32_t B, int32_t L, int32_t canvas_off, const tadm_cache* cache,
+                              const tadm_step_args* args, float* logits_dev,
+                              int32_t* next_canvas_dev);
+
+/* Masked-diffusion reverse step from given logits [B, L - canvas_off, V]
+ * (MDLM zero-masking and carry-over, App. B.1.1, with sigma_t = 0).
+ * For every masked position (absolute position pos0 + column): Gumbel-max token
+ * from softmax(logits * inv_temp) with Philox4x32-10 noise, and its confidence
+ * (log-probability at that temperature, normaliser summed in 2^-40 fixed point).
+ * Per row, the n_unmask masked positions of highest (confidence, then lowest
+ * position) take their token; every other entry of canvas_dev is copied.
+ * choice_dev / conf_dev ([B, L - canvas_off], nullable) receive the sampled token
+ * and confidence (-1 / -inf where not masked). */
+tadm_status tadm_sample(tadm_model* m, const float* logits_dev, const int32_t* canvas_dev,
+                        int32_t B, int32_t L, int32_t canvas_off, int32_t pos0,
+                        const tadm_step_args* args, int32_t* next_canvas_dev,
+                        int32_t* choice_dev, float* conf_dev);
+
+/* Whole generation (Algorithm 1 with the linear unmask schedule
+ * n_i = floor(M0 i / T) - floor(M0 (i-1) / T)).  prompt_dev [B, P]; tokens_dev
+ * [B, P + gen_len] receives prompt and generated tokens.  block_len == gen_len:
+ * one bidirectional canvas; block_len < gen_len (must divide gen_len): block
+ * diffusion with a context KV.  Returns after enqueueing. */
+tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, int32_t P,
+                          int32_t gen_len, int32_t T, int32_t K, int32_t block_len, uint64_t seed,
+                          float temperature, int32_t* tokens_dev);
+
+/* Pure host helper: n_i of the linear schedule. */
+int32_t tadm_unmask_count(int32_t M0, int32_t i, int32_t T);
+
+/* -------------------------------------------------------- observability ---- */
+/* Copies (float32) a buffer of the last step into dst_dev:
+ *   TADM_TAP_EMBED  c = S(z)          [B, L, d]
+ *   TADM_TAP_FUSED  h~ = Phi(c, h')   [B, L, d]
+ *   TADM_TAP_FINAL  final-normed D output of the canvas columns [B, L - off, d] */
+enum { TADM_TAP_EMBED = 0, TADM_TAP_FUSED = 1, TADM_TAP_FINAL = 2 };
+/* Keep a copy of h~ for TADM_TAP_FUSED (one extra [B, L, d] copy per step; off by default). */
+tadm_status tadm_debug_taps(tadm_model* m, int32_t enable);
+tadm_status tadm_debug_read(tadm_model* m, int32_t tap, float* dst_dev, size_t bytes);
+
+/* Per-stage timing with HIP events recorded on the model stream around each
+ * stage; read synchronises the stream.  Stage ids: */
+enum {
+  TADM_STAGE_EMBED = 0, TADM_STAGE_ANCHOR = 1, TADM_STAGE_FUSION = 2, TADM_STAGE_DENOISE = 3,
+  TADM_STAGE_HEAD = 4, TADM_STAGE_SAMPLE = 5, TADM_STAGE_SELECT = 6, TADM_STAGE_CONTEXT = 7,
+  TADM_STAGE_COUNT = 8
+};
+tadm_status tadm_profile_enable(tadm_model* m, int32_t enable);
+tadm_status tadm_profile_read(tadm_model* m, int32_t stage, double* total_ms, int64_t* count);
+tadm_status tadm_profile_reset(tadm_model* m);
+
+/* Message of the last failure on the calling thread ("" if none). */
+const char* tadm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TADM_H */

@@ -1,0 +1,283 @@
+// Rotary embedding + head split, and bidirectional softmax attention.
+//
+// bf16 attention: one workgroup = 64 queries of one (row, head); 4 wave64s with
+// 16 queries each.  K (64 keys x dh) and V^T (dh x 64 keys) tiles are staged in LDS,
+// double-buffered.  Scores are computed transposed, S^T = K Q^T with
+// v_mfma_f32_16x16x32_bf16, so that each lane owns one query: the online-softmax
+// statistics live in the lane and the probabilities feed the O^T = V^T P^T MFMA
+// directly from registers (the k index of that product walks keys in the order the
+// score accumulators hold them, and V^T is read in the same order).
+#include "common.h"
+#include "kernels.h"
+
+namespace tadm {
+namespace {
+
+// grid: x = B * ceil(L/64) token tiles, y = H + 2*Hkv head slots.
+template <class T>
+__global__ __launch_bounds__(256) void rope_split_kernel(const T* qkv, int B, int L, int H, int Hkv,
+                                                         int dh, int pos0, const float* cos_t,
+                                                         const float* sin_t, T* Q, T* K, T* Vt,
+                                                         int kv_cap, int kv_off) {
+  __shared__ float tile[64][129];
+  const int ntile = (L + 63) / 64;
+  const int b = blockIdx.x / ntile, l0 = (blockIdx.x % ntile) * 64;
+  const int slot = blockIdx.y;
+  const int width = (H + 2 * Hkv) * dh;
+  const int half = dh / 2;
+  if (slot < H + Hkv) {
+    const bool isq = slot < H;
+    const int hh = isq ? slot : slot - H;
+    for (int idx = threadIdx.x; idx < 64 * half; idx += 256) {
+      const int l = l0 + idx / half, j = idx % half;
+      if (l >= L) continue;
+      const T* src = qkv + ((size_t)b * L + l) * width + slot * dh;
+      const float x1 = f32_of(src[j]), x2 = f32_of(src[j + half]);
+      const int pos = pos0 + l;
+      const float c = cos_t[(size_t)pos * half + j], s = sin_t[(size_t)pos * half + j];
+      T* dst = isq ? Q + (((size_t)b * H + hh) * L + l) * dh
+                   : K + (((size_t)b * Hkv + hh) * kv_cap + kv_off + l) * dh;
+      dst[j] = from_f32<T>(x1 * c - x2 * s);
+      dst[j + half] = from_f32<T>(x2 * c + x1 * s);
+    }
+  } else {
+    const int hh = slot - H - Hkv;
+    for (int idx = threadIdx.x; idx < 64 * dh; idx += 256) {
+      const int l = idx / dh, d = idx % dh;
+      if (l0 + l < L) tile[l][d] = f32_of(qkv[((size_t)b * L + l0 + l) * width + slot * dh + d]);
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 64 * dh; idx += 256) {
+      const int d = idx / 64, l = idx % 64;
+      if (l0 + l < L)
+        Vt[(((size_t)b * Hkv + hh) * dh + d) * kv_cap + kv_off + l0 + l] = from_f32<T>(tile[l][d]);
+    }
+  }
+}
+
+template <int DH>
+__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const bf16* K,
+                                                           const bf16* Vt, bf16* O, int H, int Hkv,
+                                                           int Lq, int Lk, int kv_cap,
+                                                           float scale_log2) {
+  constexpr int KT = 64;
+  constexpr int KS = DH + 8;  // K tile row stride (elements)
+  constexpr int VS = KT + 8;  // V^T tile row stride
+  constexpr int NC = DH / 32; // 16-byte chunks per thread per tile (K and V each)
+  __shared__ __attribute__((aligned(16))) bf16 sK[2][KT * KS];
+  __shared__ __attribute__((aligned(16))) bf16 sV[2][DH * VS];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, grp = lane >> 4;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int hk = (h * Hkv) / H;
+  const bf16* Kb = K + ((size_t)b * Hkv + hk) * kv_cap * DH;
+  const bf16* Vb = Vt + ((size_t)b * Hkv + hk) * DH * kv_cap;
+  const int q = blockIdx.x * 64 + wave * 16 + (lane & 15);
+  const bf16* Qr = Q + (((size_t)b * H + h) * Lq + min(q, Lq - 1)) * DH;
+
+  bf16x8 qf[DH / 32];
+#pragma unroll
+  for (int kc = 0; kc < DH / 32; ++kc) qf[kc] = *reinterpret_cast<const bf16x8*>(Qr + 32 * kc + 8 * grp);
+
+  uint4 rk[NC], rv[NC];
+  auto gload = [&](int t) {
+    const int k0 = t * KT;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int c = tid + 256 * i, key = c / (DH / 8), ch = c % (DH / 8);
+      rk[i] = *reinterpret_cast<const uint4*>(Kb + (size_t)min(k0 + key, Lk - 1) * DH + ch * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int c = tid + 256 * i, row = c >> 3, ch = c & 7;
+      const int key0 = k0 + ch * 8;  // < kv_cap (a multiple of 64): in bounds
+      uint4 v = *reinterpret_cast<const uint4*>(Vb + (size_t)row * kv_cap + key0);
+      if (key0 + 8 > Lk) {  // zero keys past the end so that p = 0 meets finite values
+        bf16x8 w = *reinterpret_cast<bf16x8*>(&v);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (key0 + e >= Lk) w[e] = (bf16)0.f;
+        v = *reinterpret_cast<uint4*>(&w);
+      }
+      rv[i] = v;
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int c = tid + 256 * i, key = c / (DH / 8), ch = c % (DH / 8);
+      *reinterpret_cast<uint4*>(&sK[buf][key * KS + ch * 8]) = rk[i];
+    }
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int c = tid + 256 * i, row = c >> 3, ch = c & 7;
+      *reinterpret_cast<uint4*>(&sV[buf][row * VS + ch * 8]) = rv[i];
+    }
+  };
+
+  f32x4 o[DH / 16];
+#pragma unroll
+  for (int d = 0; d < DH / 16; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int nt = (Lk + KT - 1) / KT;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nt) gload(t + 1);
+    f32x4 s[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      s[ks] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kc = 0; kc < DH / 32; ++kc) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
+            &sK[buf][(ks * 16 + (lane & 15)) * KS + 32 * kc + 8 * grp]);
+        s[ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kc], s[ks], 0, 0, 0);
+      }
+    }
+    // s[ks][j] = score(query lane&15, key t*64 + ks*16 + 4*grp + j)
+    float mt = -INFINITY;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int key = t * KT + ks * 16 + 4 * grp + j;
+        const float v = key < Lk ? s[ks][j] * scale_log2 : -INFINITY;
+        s[ks][j] = v;
+        mt = fmaxf(mt, v);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
+    float ps = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float p = exp2f(s[ks][j] - m_new);
+        s[ks][j] = p;
+        ps += p;
+      }
+    l_run = l_run * alpha + ps;
+    m_run = m_new;
+#pragma unroll
+    for (int d = 0; d < DH / 16; ++d) o[d] *= alpha;
+#pragma unroll
+    for (int kc2 = 0; kc2 < 2; ++kc2) {
+      bf16x8 pf;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        pf[j] = (bf16)s[2 * kc2][j];
+        pf[4 + j] = (bf16)s[2 * kc2 + 1][j];
+      }
+#pragma unroll
+      for (int d = 0; d < DH / 16; ++d) {
+        const bf16* vr = &sV[buf][(d * 16 + (lane & 15)) * VS + 32 * kc2 + 4 * grp];
+        const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(vr);
+        const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(vr + 16);
+        bf16x8 vf;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) { vf[j] = v0[j]; vf[4 + j] = v1[j]; }
+        o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[d], 0, 0, 0);
+      }
+    }
+    if (t + 1 < nt) sstore(buf ^ 1);
+    __syncthreads();
+  }
+  float l_tot = l_run + __shfl_xor(l_run, 16, 64);
+  l_tot += __shfl_xor(l_tot, 32, 64);
+  const float inv = 1.f / l_tot;
+  if (q < Lq) {
+    bf16* orow = O + ((size_t)b * Lq + q) * H * DH + h * DH;
+#pragma unroll
+    for (int d = 0; d < DH / 16; ++d)
+      store4(orow + d * 16 + 4 * grp, o[d][0] * inv, o[d][1] * inv, o[d][2] * inv, o[d][3] * inv);
+  }
+}
+
+// float32 attention for small fp32 models: one wave per query, scores in LDS.
+__global__ __launch_bounds__(256) void attn_f32_kernel(const float* Q, const float* K, const float* Vt,
+                                                       float* O, int H, int Hkv, int Lq, int Lk,
+                                                       int kv_cap, int dh, float scale) {
+  extern __shared__ float sp[];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int q = blockIdx.x * 4 + wave, h = blockIdx.y, b = blockIdx.z;
+  const int hk = (h * Hkv) / H;
+  const int qc = min(q, Lq - 1);
+  float* p = sp + wave * Lk;
+  const float* qr = Q + (((size_t)b * H + h) * Lq + qc) * dh;
+  const float* Kb = K + ((size_t)b * Hkv + hk) * kv_cap * dh;
+  const float* Vb = Vt + ((size_t)b * Hkv + hk) * dh * kv_cap;
+  float mx = -INFINITY;
+  for (int k = lane; k < Lk; k += 64) {
+    float acc = 0.f;
+    for (int d = 0; d < dh; ++d) acc += qr[d] * Kb[(size_t)k * dh + d];
+    p[k] = acc * scale;
+    mx = fmaxf(mx, acc * scale);
+  }
+  mx = wave_max(mx);
+  float sum = 0.f;
+  for (int k = lane; k < Lk; k += 64) {
+    const float e = __expf(p[k] - mx);
+    p[k] = e;
+    sum += e;
+  }
+  sum = wave_sum(sum);
+  __syncthreads();
+  if (q < Lq)
+    for (int d = lane; d < dh; d += 64) {
+      float acc = 0.f;
+      for (int k = 0; k < Lk; ++k) acc += p[k] * Vb[(size_t)d * kv_cap + k];
+      O[((size_t)b * Lq + q) * H * dh + h * dh + d] = acc / sum;
+    }
+}
+
+}  // namespace
+
+hipError_t rope_split(DType dt, const void* qkv, int B, int L, int H, int Hkv, int dh, int pos0,
+                      const float* cos_t, const float* sin_t, void* Q, void* K, void* Vt, int kv_cap,
+                      int kv_off, hipStream_t s) {
+  if (B * L == 0) return hipSuccess;
+  const dim3 grid(B * ((L + 63) / 64), H + 2 * Hkv);
+  if (dt == BF16)
+    hipLaunchKernelGGL(rope_split_kernel<bf16>, grid, dim3(256), 0, s, static_cast<const bf16*>(qkv), B,
+                       L, H, Hkv, dh, pos0, cos_t, sin_t, static_cast<bf16*>(Q), static_cast<bf16*>(K),
+                       static_cast<bf16*>(Vt), kv_cap, kv_off);
+  else
+    hipLaunchKernelGGL(rope_split_kernel<float>, grid, dim3(256), 0, s, static_cast<const float*>(qkv),
+                       B, L, H, Hkv, dh, pos0, cos_t, sin_t, static_cast<float*>(Q),
+                       static_cast<float*>(K), static_cast<float*>(Vt), kv_cap, kv_off);
+  return hipGetLastError();
+}
+
+hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, void* O, int B, int H,
+                     int Hkv, int Lq, int Lk, int kv_cap, int dh, hipStream_t s) {
+  if (B * Lq == 0) return hipSuccess;
+  if (dt == BF16) {
+    const dim3 grid((Lq + 63) / 64, H, B);
+    const float sl2 = 1.4426950408889634f / sqrtf((float)dh);
+    if (dh == 64)
+      hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
+                         static_cast<const bf16*>(K), static_cast<const bf16*>(Vt), static_cast<bf16*>(O),
+                         H, Hkv, Lq, Lk, kv_cap, sl2);
+    else if (dh == 128)
+      hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
+                         static_cast<const bf16*>(K), static_cast<const bf16*>(Vt), static_cast<bf16*>(O),
+                         H, Hkv, Lq, Lk, kv_cap, sl2);
+    else
+      return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
+  const dim3 grid((Lq + 3) / 4, H, B);
+  hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(256), 4 * Lk * sizeof(float), s,
+                     static_cast<const float*>(Q), static_cast<const float*>(K),
+                     static_cast<const float*>(Vt), static_cast<float*>(O), H, Hkv, Lq, Lk, kv_cap, dh,
+                     1.f / sqrtf((float)dh));
+  return hipGetLastError();
+}
+
+}  // namespace tadm

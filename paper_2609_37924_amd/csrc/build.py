@@ -1,0 +1,65 @@
+"""Builds libtadm.so (gfx950) from the HIP sources next to this file.
+
+Usage: python build.py [--jobs N].  Each source compiles to an object with hipcc
+(-O3, --offload-arch=gfx950, packed-fp32 instructions disabled); the sampler is
+compiled without floating-point contraction so that its float32 arithmetic is
+exactly the documented sequence of rounded operations.
+"""
+import os
+import subprocess
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+PKG = os.path.dirname(HERE)
+ROOT = os.path.dirname(PKG)
+SOURCES = ["runtime.hip", "gemm.hip", "attention.hip", "norm.hip", "sampler.hip"]
+EXTRA = {"sampler.hip": ["-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt"]}
+OUT = os.path.join(PKG, "libtadm.so")
+
+
+def hipcc():
+    for c in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc"):
+        if c and os.path.exists(c):
+            return c
+    return "hipcc"
+
+
+def flags():
+    return ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result",
+            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            "-I", os.path.join(ROOT, "include"), "-I", HERE]
+
+
+def compile_one(src, objdir):
+    obj = os.path.join(objdir, src.replace(".hip", ".o"))
+    cmd = [hipcc(), "-c", os.path.join(HERE, src), "-o", obj] + flags() + EXTRA.get(src, [])
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    errs = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
+                     if "packed-fp32-ops" not in l and l.strip())
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {src}:\n{errs}")
+    return obj, errs
+
+
+def build(jobs=8, verbose=False):
+    objdir = os.path.join(ROOT, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    with ThreadPoolExecutor(max_workers=jobs) as ex:
+        results = list(ex.map(lambda s: compile_one(s, objdir), SOURCES))
+    if verbose:
+        for _, e in results:
+            if e:
+                print(e)
+    tmp = OUT + ".tmp"
+    cmd = [hipcc(), "-shared", "-o", tmp, "--offload-arch=gfx950"] + [o for o, _ in results]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("link failed:\n" + r.stderr)
+    os.replace(tmp, OUT)
+    return OUT
+
+
+if __name__ == "__main__":
+    jobs = int(sys.argv[sys.argv.index("--jobs") + 1]) if "--jobs" in sys.argv else 8
+    print(build(jobs, verbose=True))

@@ -1,0 +1,96 @@
+// Host-side launchers of the TADM kernels.  All enqueue on the given stream and
+// return the launch status; shapes are validated by the caller (runtime.cpp).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tadm {
+
+enum DType { F32 = 0, BF16 = 1 };
+
+// C[m, n] = sum_k A[m, k] * W[n, k].  A is [M, K] row-major, split along K:
+// columns [0, K1) come from A1 (row stride lda1), [K1, K) from A2 (lda2).
+// W is [N, K] row-major (row n = weights of output feature n).
+struct GemmProblem {
+  int M, N, K;
+  const void* A1; int lda1; int K1;
+  const void* A2; int lda2;
+  const void* W;  int ldw;
+};
+
+enum EpiKind {
+  EPI_STORE = 0,      // out(T)[m, n] = acc
+  EPI_STORE_F32,      // out(float)[m, n] = acc
+  EPI_RESID,          // resid(float)[m, n] += acc
+  EPI_GELU,           // out(T)[m, n] = gelu(acc)
+  EPI_GLU_SILU,       // out(T)[m, f] = silu(gate) * up   (16-row interleaved weights)
+  EPI_GLU_GELU,       // out(T)[m, f] = gelu(gate) * up
+  EPI_FUSION1,        // n < split: out(T)[m, n] = gelu(acc + bias[n]);  else out2(float)[m, n-split] = sigmoid(acc + bias[n])
+  EPI_FUSION2,        // resid(float)[m, n] = aux[m, n] + gate[m, n] * (acc + bias[n])
+};
+
+struct EpiParams {
+  void* out = nullptr;  int ldo = 0;
+  float* resid = nullptr; int ldr = 0;
+  const float* bias = nullptr;
+  const float* aux = nullptr; int ld_aux = 0;
+  const float* gate = nullptr; int ldg = 0;
+  float* out2 = nullptr; int ldo2 = 0;
+  int split = 0;
+};
+
+hipError_t gemm(DType dt, const GemmProblem& p, EpiKind epi, const EpiParams& e, hipStream_t s);
+
+// ---- norms / embedding / elementwise (norm.hip)
+// out[t, :] = embed[tok[t], :] as float32; `embed` has table_rows rows of length d
+// (ids outside [0, table_rows) are clamped so that the gather stays in bounds).
+hipError_t embed_gather(DType dt, const int32_t* tok, int n_tok, const void* embed, int table_rows,
+                        int d, float* out, hipStream_t s);
+// y(T) = x / sqrt(mean(x^2) + eps) * g over rows of length d.  Row r of the
+// output is taken from input row map(r) = (r / rows_per_b) * in_stride_b + in_off + r % rows_per_b
+// (a gather of the canvas columns); pass rows_per_b = n_rows, in_stride_b = 0, in_off = 0 for identity.
+hipError_t rms_norm(DType dt, const float* x, const float* g, float eps, int n_rows, int d,
+                    int rows_per_b, int in_stride_b, int in_off, void* y, hipStream_t s);
+// LayerNorm with affine; output as T (y_t) or float (y_f), whichever is non-null.
+hipError_t layer_norm(DType dt, const float* x, const float* w, const float* b, float eps,
+                      int n_rows, int d, void* y_t, float* y_f, hipStream_t s);
+hipError_t copy_f32(const float* src, float* dst, size_t n, hipStream_t s);
+hipError_t to_f32(DType dt, const void* src, float* dst, size_t n, hipStream_t s);
+// out[r, f] = act(pre[r, gate_row(f)]) * pre[r, up_row(f)] for the fp32 GLU path.
+hipError_t glu_f32(const float* pre, int n_rows, int F, int silu, float* out, hipStream_t s);
+
+// ---- rotary + head split (attention.hip)
+// qkv(T) [B*L, (H + 2*Hkv)*dh] -> Q(T) [B, H, L, dh] (rotated), K(T) rows
+// [b, hk, off + l, :] of a [B, Hkv, kv_cap, dh] buffer (rotated), Vt(T) [b, hk, :, off + l]
+// of a [B, Hkv, dh, kv_cap] buffer.  Positions pos0 + l; cos/sin tables [max_pos, dh/2].
+hipError_t rope_split(DType dt, const void* qkv, int B, int L, int H, int Hkv, int dh, int pos0,
+                      const float* cos_t, const float* sin_t, void* Q, void* K, void* Vt,
+                      int kv_cap, int kv_off, hipStream_t s);
+// O(T) [B*Lq, H*dh] = softmax(Q K^T / sqrt(dh)) V over keys [0, Lk) of the K/Vt buffers.
+hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, void* O, int B, int H,
+                     int Hkv, int Lq, int Lk, int kv_cap, int dh, hipStream_t s);
+
+// ---- sampler (sampler.hip)
+// For every masked canvas position: Gumbel-max token and fixed-point confidence.
+hipError_t sample_tokens(const float* logits, const int32_t* canvas, int B, int L, int canvas_off,
+                         int V, int mask_id, int pos0, uint32_t step_id, uint64_t seed,
+                         float inv_temp, int32_t* choice, float* conf, hipStream_t s);
+// Per row: reveal the n_unmask most confident masked positions; copy the rest.
+hipError_t select_unmask(const int32_t* canvas, const int32_t* choice, const float* conf, int B,
+                         int L, int canvas_off, int mask_id, int n_unmask, int32_t* next,
+                         hipStream_t s);
+
+}  // namespace tadm
+
+namespace tadm {
+// ---- weight placement and small copies (norm.hip)
+// dst row map(r) <- src row r (cols elements) for r < rows.  map(r) = row_off + r,
+// or, for glu_half >= 0, row_off + 32*(r/16) + 16*glu_half + r%16 (gate/up interleave
+// in 16-row blocks).  Elements keep the model type (dst_f32 = 0) or become float32.
+hipError_t scatter_rows(DType dt, const void* src, long rows, int cols, void* dst, int dst_f32,
+                        long row_off, int glu_half, hipStream_t s);
+// canvas rows: dst[b, :] = concat(prompt[b, :P], mask_id * gen)
+hipError_t init_canvas(const int32_t* prompt, int B, int P, int gen, int mask_id, int32_t* dst,
+                       hipStream_t s);
+hipError_t fill_i32(int32_t* dst, size_t n, int32_t v, hipStream_t s);
+}  // namespace tadm

@@ -1,0 +1,998 @@
+// Runtime of the TADM reverse-diffusion step: model weights in HBM, anchor cache,
+// block-diffusion context KV, step orchestration on one HIP stream, C ABI.
+//
+// Every step is a fixed sequence of kernel launches whose sizes are known on the
+// host (the unmask count of the linear schedule is a host integer), so a whole
+// generation is enqueued without any device-to-host synchronisation.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/tadm.h"
+#include "kernels.h"
+
+using namespace tadm;
+
+// ------------------------------------------------------------------ errors ----
+static thread_local std::string g_err;
+
+static tadm_status fail(tadm_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define HIPCHK(expr)                                                                          \
+  do {                                                                                        \
+    hipError_t e_ = (expr);                                                                   \
+    if (e_ != hipSuccess)                                                                     \
+      return fail(e_ == hipErrorOutOfMemory ? TADM_ERR_OOM : TADM_ERR_DEVICE, "%s: %s (%s:%d)", \
+                  #expr, hipGetErrorString(e_), __FILE__, __LINE__);                          \
+  } while (0)
+
+#define TRY(expr)                      \
+  do {                                 \
+    tadm_status s_ = (expr);           \
+    if (s_ != TADM_OK) return s_;      \
+  } while (0)
+
+static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+static int round64(int x) { return (x + 63) / 64 * 64; }
+
+// ----------------------------------------------------------- weight specs ----
+namespace {
+
+enum Place { P_COPY, P_ROWS, P_GLU, P_VEC };
+
+struct Spec {
+  std::string name;
+  long rows, cols;  // cols == 0: vector of `rows` elements
+  // destination
+  int target;       // index into Model::tensors
+  Place place;
+  long row_off;
+  int glu_half;
+};
+
+struct Tensor {
+  long rows, cols;  // stored shape
+  bool f32;         // stored as float32 (norm gains, biases) or model dtype
+  size_t off;       // byte offset in the arena
+};
+
+struct LayerIdx {
+  int attn_norm, wqkv, wo, ffn_norm, wup, wdown;
+};
+
+struct Layout {
+  std::vector<Spec> specs;
+  std::vector<Tensor> tensors;
+  int embed, final_norm, w_out;
+  int ln_s_w, ln_s_b, ln_a_w, ln_a_b, w1g, b1g, w2, b2, ln_o_w, ln_o_b;  // gated MLP
+  std::vector<LayerIdx> layers;
+  size_t bytes;
+};
+
+int add_tensor(Layout& L, long rows, long cols, bool f32) {
+  L.tensors.push_back(Tensor{rows, cols, f32, 0});
+  return (int)L.tensors.size() - 1;
+}
+
+void add_spec(Layout& L, const std::string& n, long rows, long cols, int target, Place p,
+              long row_off = 0, int glu_half = -1) {
+  L.specs.push_back(Spec{n, rows, cols, target, p, row_off, glu_half});
+}
+
+Layout make_layout(const tadm_config& c) {
+  Layout L{};
+  const long d = c.d_model, V = c.vocab, H = c.n_heads, Hk = c.n_kv_heads, dh = c.head_dim,
+             F = c.d_ffn;
+  L.embed = add_tensor(L, V + 1, d, false);
+  L.final_norm = add_tensor(L, d, 1, true);
+  L.w_out = add_tensor(L, V, d, false);
+  add_spec(L, "embed", V + 1, d, L.embed, P_COPY);
+  add_spec(L, "final_norm", d, 0, L.final_norm, P_VEC);
+  add_spec(L, "w_out", V, d, L.w_out, P_COPY);
+  if (c.fusion_kind == TADM_FUSION_GATED_MLP) {
+    L.ln_s_w = add_tensor(L, d, 1, true);
+    L.ln_s_b = add_tensor(L, d, 1, true);
+    L.ln_a_w = add_tensor(L, d, 1, true);
+    L.ln_a_b = add_tensor(L, d, 1, true);
+    L.w1g = add_tensor(L, 5 * d, 2 * d, false);  // rows [0,4d) = W1, [4d,5d) = W_g
+    L.b1g = add_tensor(L, 5 * d, 1, true);
+    L.w2 = add_tensor(L, d, 4 * d, false);
+    L.b2 = add_tensor(L, d, 1, true);
+    L.ln_o_w = add_tensor(L, d, 1, true);
+    L.ln_o_b = add_tensor(L, d, 1, true);
+    add_spec(L, "fusion.ln_s_w", d, 0, L.ln_s_w, P_VEC);
+    add_spec(L, "fusion.ln_s_b", d, 0, L.ln_s_b, P_VEC);
+    add_spec(L, "fusion.ln_a_w", d, 0, L.ln_a_w, P_VEC);
+    add_spec(L, "fusion.ln_a_b", d, 0, L.ln_a_b, P_VEC);
+    add_spec(L, "fusion.w1", 4 * d, 2 * d, L.w1g, P_ROWS, 0);
+    add_spec(L, "fusion.b1", 4 * d, 0, L.b1g, P_VEC, 0);
+    add_spec(L, "fusion.wg", d, 2 * d, L.w1g, P_ROWS, 4 * d);
+    add_spec(L, "fusion.bg", d, 0, L.b1g, P_VEC, 4 * d);
+    add_spec(L, "fusion.w2", d, 4 * d, L.w2, P_COPY);
+    add_spec(L, "fusion.b2", d, 0, L.b2, P_VEC);
+    add_spec(L, "fusion.ln_o_w", d, 0, L.ln_o_w, P_VEC);
+    add_spec(L, "fusion.ln_o_b", d, 0, L.ln_o_b, P_VEC);
+  }
+  const int nl = c.n_shared + c.n_anchor + c.n_denoise;
+  const bool glu = c.ffn_kind != TADM_FFN_GELU;
+  for (int li = 0; li < nl; ++li) {
+    const std::string p = "layer" + std::to_string(li) + ".";
+    LayerIdx x;
+    x.attn_norm = add_tensor(L, d, 1, true);
+    x.wqkv = add_tensor(L, (H + 2 * Hk) * dh, d, false);
+    x.wo = add_tensor(L, d, H * dh, false);
+    x.ffn_norm = add_tensor(L, d, 1, true);
+    x.wup = add_tensor(L, glu ? 2 * F : F, d, false);
+    x.wdown = add_tensor(L, d, F, false);
+    L.layers.push_back(x);
+    add_spec(L, p + "attn_norm", d, 0, x.attn_norm, P_VEC);
+    add_spec(L, p + "wq", H * dh, d, x.wqkv, P_ROWS, 0);
+    add_spec(L, p + "wk", Hk * dh, d, x.wqkv, P_ROWS, H * dh);
+    add_spec(L, p + "wv", Hk * dh, d, x.wqkv, P_ROWS, (H + Hk) * dh);
+    add_spec(L, p + "wo", d, H * dh, x.wo, P_COPY);
+    add_spec(L, p + "ffn_norm", d, 0, x.ffn_norm, P_VEC);
+    if (glu) {
+      add_spec(L, p + "w_gate", F, d, x.wup, P_GLU, 0, 0);
+      add_spec(L, p + "w_up", F, d, x.wup, P_GLU, 0, 1);
+    } else {
+      add_spec(L, p + "w_up", F, d, x.wup, P_COPY);
+    }
+    add_spec(L, p + "w_down", d, F, x.wdown, P_COPY);
+  }
+  return L;
+}
+
+tadm_status finish_layout(Layout& L, size_t esz) {
+  size_t off = 0;
+  for (auto& t : L.tensors) {
+    t.off = off;
+    off = align256(off + (size_t)t.rows * (size_t)t.cols * (t.f32 ? 4 : esz));
+  }
+  L.bytes = off;
+  return TADM_OK;
+}
+
+bool valid_config(const tadm_config* c, std::string& why) {
+  if (!c) { why = "null config"; return false; }
+  if (c->dtype != TADM_DTYPE_F32 && c->dtype != TADM_DTYPE_BF16) { why = "dtype"; return false; }
+  if (c->vocab < 1 || c->d_model < 4 || c->n_heads < 1 || c->n_kv_heads < 1 || c->head_dim < 2 ||
+      c->d_ffn < 16 || c->max_batch < 1 || c->max_seq < 1) { why = "non-positive size"; return false; }
+  if (c->n_shared < 0 || c->n_anchor < 0 || c->n_denoise < 0) { why = "layer counts"; return false; }
+  if (c->n_heads % c->n_kv_heads) { why = "n_heads must be a multiple of n_kv_heads"; return false; }
+  if (c->head_dim % 2) { why = "odd head_dim"; return false; }
+  if (c->ffn_kind < 0 || c->ffn_kind > 2) { why = "ffn_kind"; return false; }
+  if (c->fusion_kind < 0 || c->fusion_kind > 1) { why = "fusion_kind"; return false; }
+  if (c->d_ffn % 16) { why = "d_ffn must be a multiple of 16"; return false; }
+  if (c->d_model % 4 || (c->n_heads * c->head_dim) % 4) { why = "widths must be multiples of 4"; return false; }
+  if (!(c->rms_eps > 0) || !(c->ln_eps > 0) || !(c->rope_theta > 0)) { why = "eps/theta"; return false; }
+  return true;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ objects ---
+struct Workspace {
+  int n_tok = 0, n_canvas = 0;  // capacity in tokens / canvas rows
+  float *x = nullptr, *c = nullptr, *ht = nullptr, *fus_g = nullptr, *conf = nullptr;
+  void *xn = nullptr, *qkv = nullptr, *q = nullptr, *k = nullptr, *vt = nullptr, *ao = nullptr,
+       *ffn = nullptr, *fus_h = nullptr;
+  float* ffn_pre = nullptr;  // fp32 GLU pre-activations
+  int32_t* choice = nullptr;
+  float* logits = nullptr;
+  size_t logits_cap = 0;
+  int kv_cap = 0;
+  std::vector<void*> allocs;
+};
+
+struct ProfRec {
+  int stage;
+  hipEvent_t a, b;
+};
+
+struct tadm_model {
+  tadm_config cfg;
+  DType dt;
+  size_t esz;
+  int device;
+  hipStream_t stream = nullptr;
+  Layout lay;
+  char* arena = nullptr;
+  std::vector<char> loaded;
+  float *rope_cos = nullptr, *rope_sin = nullptr;
+  Workspace ws;
+  bool taps = false;
+  // objects reused across calls so that a generation allocates nothing after warm-up
+  tadm_cache* scratch = nullptr;   // anchor state of context appends (capacity max_batch x max_seq)
+  tadm_cache* gcache = nullptr;    // anchor cache of tadm_generate
+  tadm_context* gctx = nullptr;    // context of block-mode tadm_generate
+  int32_t* gwin = nullptr;         // active block of block-mode tadm_generate
+  int tap_B = 0, tap_L = 0, tap_Lc = 0;
+  // profiling
+  bool prof = false;
+  std::vector<ProfRec> recs;
+  std::vector<hipEvent_t> pool;
+  int cur_stage = -1;
+  hipEvent_t cur_ev = nullptr;
+
+  void* W(int t) const { return arena + lay.tensors[t].off; }
+  float* Wf(int t) const { return reinterpret_cast<float*>(arena + lay.tensors[t].off); }
+  int n_layers() const { return cfg.n_shared + cfg.n_anchor + cfg.n_denoise; }
+};
+
+struct tadm_cache {
+  tadm_model* model;
+  int B, L;
+  float *h = nullptr, *c = nullptr;
+  void* a = nullptr;
+  int refresh_i = 0;
+};
+
+struct tadm_context {
+  tadm_model* model;
+  int B, cap, len = 0;
+  std::vector<void*> k, vt;  // per layer [B, Hkv, cap, dh] / [B, Hkv, dh, cap]
+};
+
+// ---------------------------------------------------------------- profiling ---
+static tadm_status prof_begin(tadm_model* m, int stage) {
+  if (!m->prof) return TADM_OK;
+  hipEvent_t e;
+  if (m->pool.empty()) {
+    HIPCHK(hipEventCreate(&e));
+  } else {
+    e = m->pool.back();
+    m->pool.pop_back();
+  }
+  HIPCHK(hipEventRecord(e, m->stream));
+  m->cur_stage = stage;
+  m->cur_ev = e;
+  return TADM_OK;
+}
+
+static tadm_status prof_end(tadm_model* m) {
+  if (!m->prof || m->cur_stage < 0) return TADM_OK;
+  hipEvent_t e;
+  if (m->pool.empty()) {
+    HIPCHK(hipEventCreate(&e));
+  } else {
+    e = m->pool.back();
+    m->pool.pop_back();
+  }
+  HIPCHK(hipEventRecord(e, m->stream));
+  m->recs.push_back(ProfRec{m->cur_stage, m->cur_ev, e});
+  m->cur_stage = -1;
+  return TADM_OK;
+}
+
+// ---------------------------------------------------------------- workspace ---
+static tadm_status ws_alloc(tadm_model* m, void** p, size_t bytes) {
+  HIPCHK(hipMalloc(p, std::max<size_t>(bytes, 256)));
+  m->ws.allocs.push_back(*p);
+  return TADM_OK;
+}
+
+static tadm_status ensure_workspace(tadm_model* m) {
+  Workspace& w = m->ws;
+  if (w.n_tok) return TADM_OK;
+  const tadm_config& c = m->cfg;
+  const size_t N = (size_t)c.max_batch * c.max_seq, d = c.d_model, es = m->esz;
+  const size_t H = c.n_heads, Hk = c.n_kv_heads, dh = c.head_dim, F = c.d_ffn;
+  w.kv_cap = round64(c.max_seq);
+  TRY(ws_alloc(m, (void**)&w.x, N * d * 4));
+  TRY(ws_alloc(m, (void**)&w.c, N * d * 4));
+  TRY(ws_alloc(m, (void**)&w.ht, N * d * 4));
+  TRY(ws_alloc(m, &w.xn, N * d * es));
+  TRY(ws_alloc(m, &w.qkv, N * (H + 2 * Hk) * dh * es));
+  TRY(ws_alloc(m, &w.q, N * H * dh * es));
+  TRY(ws_alloc(m, &w.k, (size_t)c.max_batch * Hk * w.kv_cap * dh * es));
+  TRY(ws_alloc(m, &w.vt, (size_t)c.max_batch * Hk * w.kv_cap * dh * es));
+  TRY(ws_alloc(m, &w.ao, N * H * dh * es));
+  TRY(ws_alloc(m, &w.ffn, N * F * es));
+  if (m->dt == F32 && c.ffn_kind != TADM_FFN_GELU) TRY(ws_alloc(m, (void**)&w.ffn_pre, N * 2 * F * 4));
+  if (c.fusion_kind == TADM_FUSION_GATED_MLP) {
+    TRY(ws_alloc(m, &w.fus_h, N * 4 * d * es));
+    TRY(ws_alloc(m, (void**)&w.fus_g, N * d * 4));
+  }
+  TRY(ws_alloc(m, (void**)&w.choice, N * 4));
+  TRY(ws_alloc(m, (void**)&w.conf, N * 4));
+  w.n_tok = (int)N;
+  w.n_canvas = (int)N;
+  return TADM_OK;
+}
+
+static tadm_status ensure_logits(tadm_model* m, size_t n) {
+  Workspace& w = m->ws;
+  if (w.logits_cap >= n) return TADM_OK;
+  if (w.logits) HIPCHK(hipFree(w.logits));
+  w.logits = nullptr;
+  HIPCHK(hipMalloc((void**)&w.logits, n * 4));
+  w.logits_cap = n;
+  return TADM_OK;
+}
+
+// --------------------------------------------------------------- the layers ---
+struct KVTarget {
+  void *k, *vt;
+  int cap, off;
+};
+
+static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int pos0, KVTarget kv) {
+  const tadm_config& c = m->cfg;
+  const LayerIdx& w = m->lay.layers[li];
+  Workspace& s = m->ws;
+  const int N = B * L, d = c.d_model, H = c.n_heads, Hk = c.n_kv_heads, dh = c.head_dim,
+            F = c.d_ffn;
+  const hipStream_t st = m->stream;
+  HIPCHK(rms_norm(m->dt, x, m->Wf(w.attn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
+  {
+    GemmProblem p{N, (H + 2 * Hk) * dh, d, s.xn, d, d, nullptr, 0, m->W(w.wqkv), d};
+    EpiParams e;
+    e.out = s.qkv;
+    e.ldo = (H + 2 * Hk) * dh;
+    HIPCHK(gemm(m->dt, p, EPI_STORE, e, st));
+  }
+  HIPCHK(rope_split(m->dt, s.qkv, B, L, H, Hk, dh, pos0, m->rope_cos, m->rope_sin, s.q, kv.k, kv.vt,
+                    kv.cap, kv.off, st));
+  HIPCHK(attention(m->dt, s.q, kv.k, kv.vt, s.ao, B, H, Hk, L, kv.off + L, kv.cap, dh, st));
+  {
+    GemmProblem p{N, d, H * dh, s.ao, H * dh, H * dh, nullptr, 0, m->W(w.wo), H * dh};
+    EpiParams e;
+    e.resid = x;
+    e.ldr = d;
+    HIPCHK(gemm(m->dt, p, EPI_RESID, e, st));
+  }
+  HIPCHK(rms_norm(m->dt, x, m->Wf(w.ffn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
+  if (c.ffn_kind == TADM_FFN_GELU) {
+    GemmProblem p{N, F, d, s.xn, d, d, nullptr, 0, m->W(w.wup), d};
+    EpiParams e;
+    e.out = s.ffn;
+    e.ldo = F;
+    HIPCHK(gemm(m->dt, p, EPI_GELU, e, st));
+  } else if (m->dt == BF16) {
+    GemmProblem p{N, 2 * F, d, s.xn, d, d, nullptr, 0, m->W(w.wup), d};
+    EpiParams e;
+    e.out = s.ffn;
+    e.ldo = F;
+    HIPCHK(gemm(m->dt, p, c.ffn_kind == TADM_FFN_SWIGLU ? EPI_GLU_SILU : EPI_GLU_GELU, e, st));
+  } else {
+    GemmProblem p{N, 2 * F, d, s.xn, d, d, nullptr, 0, m->W(w.wup), d};
+    EpiParams e;
+    e.out = s.ffn_pre;
+    e.ldo = 2 * F;
+    HIPCHK(gemm(m->dt, p, EPI_STORE_F32, e, st));
+    HIPCHK(glu_f32(s.ffn_pre, N, F, c.ffn_kind == TADM_FFN_SWIGLU, (float*)s.ffn, st));
+  }
+  {
+    GemmProblem p{N, d, F, s.ffn, F, F, nullptr, 0, m->W(w.wdown), F};
+    EpiParams e;
+    e.resid = x;
+    e.ldr = d;
+    HIPCHK(gemm(m->dt, p, EPI_RESID, e, st));
+  }
+  return TADM_OK;
+}
+
+static KVTarget kv_target(tadm_model* m, const tadm_context* ctx, int li) {
+  if (ctx) return KVTarget{ctx->k[li], ctx->vt[li], ctx->cap, ctx->len};
+  return KVTarget{m->ws.k, m->ws.vt, m->ws.kv_cap, 0};
+}
+
+static tadm_status run_part(tadm_model* m, int first, int count, float* x, int B, int L, int pos0,
+                            const tadm_context* ctx) {
+  for (int li = first; li < first + count; ++li) TRY(run_layer(m, li, x, B, L, pos0, kv_target(m, ctx, li)));
+  return TADM_OK;
+}
+
+// c = S(z): embedding gather then the shared layers (in place on `c`).
+static tadm_status shared_net(tadm_model* m, const tadm_context* ctx, const int32_t* z, int B, int L,
+                              float* c) {
+  const int pos0 = ctx ? ctx->len : 0;
+  HIPCHK(embed_gather(m->dt, z, B * L, m->W(m->lay.embed), m->cfg.vocab + 1, m->cfg.d_model, c,
+                      m->stream));
+  return run_part(m, 0, m->cfg.n_shared, c, B, L, pos0, ctx);
+}
+
+// anchor refresh: h = A(c) into the cache, with the fusion's anchor-side input.
+static tadm_status anchor_net(tadm_model* m, const tadm_context* ctx, int B, int L, const float* c,
+                              tadm_cache* cache) {
+  const tadm_config& cf = m->cfg;
+  const size_t n = (size_t)B * L * cf.d_model;
+  HIPCHK(copy_f32(c, cache->c, n, m->stream));
+  HIPCHK(copy_f32(c, cache->h, n, m->stream));
+  TRY(run_part(m, cf.n_shared, cf.n_anchor, cache->h, B, L, ctx ? ctx->len : 0, ctx));
+  if (cf.fusion_kind == TADM_FUSION_GATED_MLP)
+    HIPCHK(layer_norm(m->dt, cache->h, m->Wf(m->lay.ln_a_w), m->Wf(m->lay.ln_a_b), cf.ln_eps, B * L,
+                      cf.d_model, cache->a, nullptr, m->stream));
+  return TADM_OK;
+}
+
+// h~ = Phi(c, cache) into ws.x (gated residual MLP).
+static tadm_status fusion(tadm_model* m, int B, int L, const float* c, const tadm_cache* cache) {
+  const tadm_config& cf = m->cfg;
+  Workspace& s = m->ws;
+  const int N = B * L, d = cf.d_model;
+  const Layout& Y = m->lay;
+  const hipStream_t st = m->stream;
+  HIPCHK(layer_norm(m->dt, c, m->Wf(Y.ln_s_w), m->Wf(Y.ln_s_b), cf.ln_eps, N, d, s.xn, nullptr, st));
+  {
+    GemmProblem p{N, 5 * d, 2 * d, s.xn, d, d, cache->a, d, m->W(Y.w1g), 2 * d};
+    EpiParams e;
+    e.out = s.fus_h;
+    e.ldo = 4 * d;
+    e.bias = m->Wf(Y.b1g);
+    e.out2 = s.fus_g;
+    e.ldo2 = d;
+    e.split = 4 * d;
+    HIPCHK(gemm(m->dt, p, EPI_FUSION1, e, st));
+  }
+  {
+    GemmProblem p{N, d, 4 * d, s.fus_h, 4 * d, 4 * d, nullptr, 0, m->W(Y.w2), 4 * d};
+    EpiParams e;
+    e.resid = s.x;
+    e.ldr = d;
+    e.bias = m->Wf(Y.b2);
+    e.aux = cache->h;
+    e.ld_aux = d;
+    e.gate = s.fus_g;
+    e.ldg = d;
+    HIPCHK(gemm(m->dt, p, EPI_FUSION2, e, st));
+  }
+  HIPCHK(layer_norm(m->dt, s.x, m->Wf(Y.ln_o_w), m->Wf(Y.ln_o_b), cf.ln_eps, N, d, nullptr, s.x, st));
+  return TADM_OK;
+}
+
+// ------------------------------------------------------------- validation -----
+static tadm_status check_model(const tadm_model* m) {
+  if (!m) return fail(TADM_ERR_INVALID, "null model");
+  for (size_t i = 0; i < m->loaded.size(); ++i)
+    if (!m->loaded[i]) return fail(TADM_ERR_STATE, "weight %zu (%s) not loaded", i, m->lay.specs[i].name.c_str());
+  return TADM_OK;
+}
+
+static tadm_status check_window(const tadm_model* m, const tadm_context* ctx, int B, int L) {
+  if (B < 1 || B > m->cfg.max_batch) return fail(TADM_ERR_INVALID, "B=%d outside [1, %d]", B, m->cfg.max_batch);
+  const int pos0 = ctx ? ctx->len : 0;
+  if (L < 1 || pos0 + L > m->cfg.max_seq)
+    return fail(TADM_ERR_INVALID, "positions [%d, %d) exceed max_seq %d", pos0, pos0 + L, m->cfg.max_seq);
+  if (ctx) {
+    if (ctx->model != m) return fail(TADM_ERR_STATE, "context belongs to another model");
+    if (ctx->B != B) return fail(TADM_ERR_STATE, "context has B=%d, call has B=%d", ctx->B, B);
+    if (ctx->len + L > ctx->cap) return fail(TADM_ERR_INVALID, "context capacity %d too small", ctx->cap);
+  }
+  if (m->dt == F32 && ctx == nullptr && L > 4096) return fail(TADM_ERR_UNSUPPORTED, "fp32 attention limited to 4096 keys");
+  return TADM_OK;
+}
+
+static tadm_status check_args(const tadm_step_args* a, int Lc) {
+  if (!a) return fail(TADM_ERR_INVALID, "null step args");
+  if (a->T < 1 || a->i < 1 || a->i > a->T) return fail(TADM_ERR_INVALID, "step i=%d T=%d", a->i, a->T);
+  if (a->n_unmask < 0) return fail(TADM_ERR_INVALID, "negative n_unmask");
+  if (!(a->inv_temp > 0) || !std::isfinite(a->inv_temp)) return fail(TADM_ERR_INVALID, "inv_temp must be finite and > 0");
+  (void)Lc;
+  return TADM_OK;
+}
+
+// ============================================================== C ABI =========
+extern "C" {
+
+const char* tadm_last_error(void) { return g_err.c_str(); }
+
+int32_t tadm_unmask_count(int32_t M0, int32_t i, int32_t T) {
+  if (T < 1 || i < 1 || i > T || M0 < 0) return 0;
+  return (int32_t)(((int64_t)M0 * i) / T - ((int64_t)M0 * (i - 1)) / T);
+}
+
+int32_t tadm_weight_count(const tadm_config* cfg) {
+  std::string why;
+  if (!valid_config(cfg, why)) return -1;
+  return (int32_t)make_layout(*cfg).specs.size();
+}
+
+tadm_status tadm_weight_info(const tadm_config* cfg, int32_t index, int64_t* rows, int64_t* cols) {
+  std::string why;
+  if (!valid_config(cfg, why)) return fail(TADM_ERR_INVALID, "config: %s", why.c_str());
+  Layout L = make_layout(*cfg);
+  if (index < 0 || index >= (int32_t)L.specs.size() || !rows || !cols)
+    return fail(TADM_ERR_INVALID, "weight index %d", index);
+  *rows = L.specs[index].rows;
+  *cols = L.specs[index].cols;
+  return TADM_OK;
+}
+
+tadm_status tadm_model_create(const tadm_config* cfg, tadm_model** out) {
+  std::string why;
+  if (!out) return fail(TADM_ERR_INVALID, "null output pointer");
+  *out = nullptr;
+  if (!valid_config(cfg, why)) return fail(TADM_ERR_INVALID, "config: %s", why.c_str());
+  if (cfg->fusion_kind == TADM_FUSION_PAIRED)
+    return fail(TADM_ERR_UNSUPPORTED, "paired-attention fusion is not implemented in this build");
+  if (cfg->dtype == TADM_DTYPE_BF16) {
+    const int ks[] = {cfg->d_model, cfg->n_heads * cfg->head_dim, cfg->d_ffn};
+    for (int k : ks)
+      if (k % 64) return fail(TADM_ERR_UNSUPPORTED, "bf16 contractions need K %% 64 == 0 (got %d)", k);
+    if (cfg->head_dim != 64 && cfg->head_dim != 128)
+      return fail(TADM_ERR_UNSUPPORTED, "bf16 attention supports head_dim 64 or 128");
+  } else if (cfg->head_dim > 128 || cfg->max_seq > 4096) {
+    return fail(TADM_ERR_UNSUPPORTED, "fp32 models support head_dim <= 128 and max_seq <= 4096");
+  }
+  tadm_model* m = new tadm_model();
+  m->cfg = *cfg;
+  m->dt = cfg->dtype == TADM_DTYPE_BF16 ? BF16 : F32;
+  m->esz = m->dt == BF16 ? 2 : 4;
+  m->lay = make_layout(*cfg);
+  finish_layout(m->lay, m->esz);
+  m->loaded.assign(m->lay.specs.size(), 0);
+  hipError_t e = hipGetDevice(&m->device);
+  if (e == hipSuccess) e = hipMalloc((void**)&m->arena, m->lay.bytes);
+  if (e != hipSuccess) {
+    const size_t bytes = m->lay.bytes;
+    delete m;
+    return fail(e == hipErrorOutOfMemory ? TADM_ERR_OOM : TADM_ERR_DEVICE, "weight arena (%zu bytes): %s",
+                bytes, hipGetErrorString(e));
+  }
+  // rotary tables [max_seq, dh/2], angles in double precision
+  const int half = cfg->head_dim / 2;
+  std::vector<float> cs((size_t)cfg->max_seq * half), sn(cs.size());
+  for (int p = 0; p < cfg->max_seq; ++p)
+    for (int j = 0; j < half; ++j) {
+      const double ang = p * std::pow((double)cfg->rope_theta, -2.0 * j / cfg->head_dim);
+      cs[(size_t)p * half + j] = (float)std::cos(ang);
+      sn[(size_t)p * half + j] = (float)std::sin(ang);
+    }
+  e = hipMalloc((void**)&m->rope_cos, cs.size() * 4);
+  if (e == hipSuccess) e = hipMalloc((void**)&m->rope_sin, sn.size() * 4);
+  if (e == hipSuccess) e = hipMemcpy(m->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(m->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    tadm_model_destroy(m);
+    return fail(TADM_ERR_DEVICE, "rope tables: %s", hipGetErrorString(e));
+  }
+  *out = m;
+  return TADM_OK;
+}
+
+tadm_status tadm_model_load_weight(tadm_model* m, int32_t index, const void* src, size_t bytes,
+                                   int32_t src_on_device) {
+  if (!m || !src) return fail(TADM_ERR_INVALID, "null model or source");
+  if (index < 0 || index >= (int32_t)m->lay.specs.size()) return fail(TADM_ERR_INVALID, "weight index %d", index);
+  const Spec& sp = m->lay.specs[index];
+  const long cols = sp.cols ? sp.cols : 1;
+  const size_t want = (size_t)sp.rows * cols * m->esz;
+  if (bytes != want)
+    return fail(TADM_ERR_INVALID, "weight %d (%s): %zu bytes given, %zu expected", index, sp.name.c_str(), bytes, want);
+  const void* dsrc = src;
+  void* staging = nullptr;
+  if (!src_on_device) {
+    HIPCHK(hipMalloc(&staging, bytes));
+    hipError_t e = hipMemcpy(staging, src, bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      (void)hipFree(staging);
+      return fail(TADM_ERR_DEVICE, "weight upload: %s", hipGetErrorString(e));
+    }
+    dsrc = staging;
+  }
+  const Tensor& t = m->lay.tensors[sp.target];
+  hipError_t e = scatter_rows(m->dt, dsrc, sp.rows, (int)cols, m->W(sp.target), t.f32 ? 1 : 0, sp.row_off,
+                              sp.place == P_GLU ? sp.glu_half : -1, nullptr);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (staging) (void)hipFree(staging);
+  if (e != hipSuccess) return fail(TADM_ERR_DEVICE, "weight placement: %s", hipGetErrorString(e));
+  m->loaded[index] = 1;
+  return TADM_OK;
+}
+
+tadm_status tadm_model_destroy(tadm_model* m) {
+  if (!m) return fail(TADM_ERR_INVALID, "null model");
+  (void)hipDeviceSynchronize();
+  if (m->scratch) tadm_cache_destroy(m->scratch);
+  if (m->gcache) tadm_cache_destroy(m->gcache);
+  if (m->gctx) tadm_context_destroy(m->gctx);
+  if (m->gwin) (void)hipFree(m->gwin);
+  for (void* p : m->ws.allocs) (void)hipFree(p);
+  if (m->ws.logits) (void)hipFree(m->ws.logits);
+  if (m->arena) (void)hipFree(m->arena);
+  if (m->rope_cos) (void)hipFree(m->rope_cos);
+  if (m->rope_sin) (void)hipFree(m->rope_sin);
+  for (auto& r : m->recs) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (auto e : m->pool) (void)hipEventDestroy(e);
+  delete m;
+  return TADM_OK;
+}
+
+tadm_status tadm_set_stream(tadm_model* m, void* hip_stream) {
+  if (!m) return fail(TADM_ERR_INVALID, "null model");
+  m->stream = static_cast<hipStream_t>(hip_stream);
+  return TADM_OK;
+}
+
+// ------------------------------------------------------------------ cache ---
+}  // extern "C"
+
+static tadm_status cache_alloc(tadm_model* m, int B, int L, tadm_cache** out) {
+  tadm_cache* c = new tadm_cache();
+  c->model = m;
+  c->B = B;
+  c->L = L;
+  const size_t n = (size_t)B * L * m->cfg.d_model;
+  hipError_t e = hipMalloc((void**)&c->h, n * 4);
+  if (e == hipSuccess) e = hipMalloc((void**)&c->c, n * 4);
+  if (e == hipSuccess) e = hipMalloc(&c->a, n * m->esz);
+  if (e != hipSuccess) {
+    tadm_cache_destroy(c);
+    return fail(e == hipErrorOutOfMemory ? TADM_ERR_OOM : TADM_ERR_DEVICE, "cache: %s", hipGetErrorString(e));
+  }
+  *out = c;
+  return TADM_OK;
+}
+
+extern "C" {
+
+tadm_status tadm_cache_create(tadm_model* m, int32_t B, int32_t L, tadm_cache** out) {
+  if (!m || !out) return fail(TADM_ERR_INVALID, "null argument");
+  *out = nullptr;
+  if (B < 1 || B > m->cfg.max_batch || L < 1 || L > m->cfg.max_seq)
+    return fail(TADM_ERR_INVALID, "cache shape B=%d L=%d outside the model limits", B, L);
+  return cache_alloc(m, B, L, out);
+}
+
+tadm_status tadm_cache_destroy(tadm_cache* c) {
+  if (!c) return fail(TADM_ERR_INVALID, "null cache");
+  (void)hipDeviceSynchronize();
+  if (c->h) (void)hipFree(c->h);
+  if (c->c) (void)hipFree(c->c);
+  if (c->a) (void)hipFree(c->a);
+  delete c;
+  return TADM_OK;
+}
+
+tadm_status tadm_cache_read(const tadm_cache* c, int32_t field, void* dst_dev, size_t bytes) {
+  if (!c || !dst_dev) return fail(TADM_ERR_INVALID, "null argument");
+  const size_t n = (size_t)c->B * c->L * c->model->cfg.d_model;
+  const void* src;
+  size_t sz;
+  switch (field) {
+    case TADM_CACHE_H: src = c->h; sz = n * 4; break;
+    case TADM_CACHE_C: src = c->c; sz = n * 4; break;
+    case TADM_CACHE_A: src = c->a; sz = n * c->model->esz; break;
+    default: return fail(TADM_ERR_INVALID, "cache field %d", field);
+  }
+  if (bytes != sz) return fail(TADM_ERR_INVALID, "cache field %d has %zu bytes, %zu requested", field, sz, bytes);
+  HIPCHK(hipMemcpyAsync(dst_dev, src, sz, hipMemcpyDeviceToDevice, c->model->stream));
+  return TADM_OK;
+}
+
+int32_t tadm_cache_refresh_step(const tadm_cache* c) { return c ? c->refresh_i : 0; }
+
+// ---------------------------------------------------------------- context ---
+tadm_status tadm_context_create(tadm_model* m, int32_t B, int32_t max_ctx, tadm_context** out) {
+  if (!m || !out) return fail(TADM_ERR_INVALID, "null argument");
+  *out = nullptr;
+  if (B < 1 || B > m->cfg.max_batch || max_ctx < 1 || max_ctx > m->cfg.max_seq)
+    return fail(TADM_ERR_INVALID, "context shape B=%d max_ctx=%d outside the model limits", B, max_ctx);
+  tadm_context* x = new tadm_context();
+  x->model = m;
+  x->B = B;
+  x->cap = round64(max_ctx);
+  const size_t per = (size_t)B * m->cfg.n_kv_heads * x->cap * m->cfg.head_dim * m->esz;
+  for (int li = 0; li < m->n_layers(); ++li) {
+    void *k = nullptr, *v = nullptr;
+    hipError_t e = hipMalloc(&k, per);
+    if (e == hipSuccess) e = hipMalloc(&v, per);
+    if (e != hipSuccess) {
+      if (k) (void)hipFree(k);
+      tadm_context_destroy(x);
+      return fail(e == hipErrorOutOfMemory ? TADM_ERR_OOM : TADM_ERR_DEVICE, "context: %s", hipGetErrorString(e));
+    }
+    x->k.push_back(k);
+    x->vt.push_back(v);
+  }
+  *out = x;
+  return TADM_OK;
+}
+
+int32_t tadm_context_length(const tadm_context* ctx) { return ctx ? ctx->len : 0; }
+
+tadm_status tadm_context_reset(tadm_context* ctx) {
+  if (!ctx) return fail(TADM_ERR_INVALID, "null context");
+  ctx->len = 0;
+  return TADM_OK;
+}
+
+tadm_status tadm_context_destroy(tadm_context* ctx) {
+  if (!ctx) return fail(TADM_ERR_INVALID, "null context");
+  (void)hipDeviceSynchronize();
+  for (void* p : ctx->k) (void)hipFree(p);
+  for (void* p : ctx->vt) (void)hipFree(p);
+  delete ctx;
+  return TADM_OK;
+}
+
+// Fresh pass over n clean tokens: S, A, Phi(c, fresh h), D; keeps every layer's K, V.
+// `scratch` receives the anchor state (capacity at least B x n).
+static tadm_status context_append_impl(tadm_model* m, tadm_context* ctx, const int32_t* tok, int B,
+                                       int n, tadm_cache* scratch) {
+  Workspace& s = m->ws;
+  TRY(shared_net(m, ctx, tok, B, n, s.c));
+  TRY(anchor_net(m, ctx, B, n, s.c, scratch));
+  TRY(fusion(m, B, n, s.c, scratch));
+  TRY(run_part(m, m->cfg.n_shared + m->cfg.n_anchor, m->cfg.n_denoise, s.x, B, n, ctx->len, ctx));
+  ctx->len += n;
+  return TADM_OK;
+}
+
+static tadm_status ensure_scratch(tadm_model* m) {
+  if (!m->scratch) TRY(cache_alloc(m, m->cfg.max_batch, m->cfg.max_seq, &m->scratch));
+  return TADM_OK;
+}
+
+tadm_status tadm_context_append(tadm_model* m, tadm_context* ctx, const int32_t* tokens_dev, int32_t B,
+                                int32_t n) {
+  TRY(check_model(m));
+  if (!ctx || !tokens_dev) return fail(TADM_ERR_INVALID, "null argument");
+  TRY(check_window(m, ctx, B, n));
+  TRY(ensure_workspace(m));
+  TRY(ensure_scratch(m));
+  TRY(prof_begin(m, TADM_STAGE_CONTEXT));
+  TRY(context_append_impl(m, ctx, tokens_dev, B, n, m->scratch));
+  return prof_end(m);
+}
+
+// ------------------------------------------------------------------ step ----
+static tadm_status anchor_impl(tadm_model* m, const tadm_context* ctx, const int32_t* canvas, int B,
+                               int L, int i, tadm_cache* cache) {
+  TRY(prof_begin(m, TADM_STAGE_EMBED));
+  TRY(shared_net(m, ctx, canvas, B, L, m->ws.c));
+  TRY(prof_end(m));
+  TRY(prof_begin(m, TADM_STAGE_ANCHOR));
+  TRY(anchor_net(m, ctx, B, L, m->ws.c, cache));
+  TRY(prof_end(m));
+  cache->refresh_i = i;
+  return TADM_OK;
+}
+
+tadm_status tadm_anchor_forward(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev,
+                                int32_t B, int32_t L, int32_t i, int32_t T, tadm_cache* cache) {
+  TRY(check_model(m));
+  if (!canvas_dev || !cache) return fail(TADM_ERR_INVALID, "null argument");
+  TRY(check_window(m, ctx, B, L));
+  if (T < 1 || i < 1 || i > T) return fail(TADM_ERR_INVALID, "step i=%d T=%d", i, T);
+  if (cache->model != m || cache->B != B || cache->L != L)
+    return fail(TADM_ERR_STATE, "cache built for another model or shape");
+  TRY(ensure_workspace(m));
+  return anchor_impl(m, ctx, canvas_dev, B, L, i, cache);
+}
+
+static tadm_status sample_impl(tadm_model* m, const float* logits, const int32_t* canvas, int B, int L,
+                               int off, int pos0, const tadm_step_args* a, int32_t* next,
+                               int32_t* choice, float* conf) {
+  const int mask = m->cfg.vocab;
+  TRY(prof_begin(m, TADM_STAGE_SAMPLE));
+  HIPCHK(sample_tokens(logits, canvas, B, L, off, m->cfg.vocab, mask, pos0, a->step_id, a->seed,
+                       a->inv_temp, choice, conf, m->stream));
+  TRY(prof_end(m));
+  TRY(prof_begin(m, TADM_STAGE_SELECT));
+  HIPCHK(select_unmask(canvas, choice, conf, B, L, off, mask, a->n_unmask, next, m->stream));
+  TRY(prof_end(m));
+  return TADM_OK;
+}
+
+static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const int32_t* canvas, int B,
+                                int L, int off, const tadm_cache* cache, const tadm_step_args* a,
+                                float* logits, int32_t* next) {
+  const tadm_config& cf = m->cfg;
+  Workspace& s = m->ws;
+  const int pos0 = ctx ? ctx->len : 0, Lc = L - off, d = cf.d_model;
+  TRY(prof_begin(m, TADM_STAGE_EMBED));
+  TRY(shared_net(m, ctx, canvas, B, L, s.c));
+  TRY(prof_end(m));
+  TRY(prof_begin(m, TADM_STAGE_FUSION));
+  TRY(fusion(m, B, L, s.c, cache));
+  TRY(prof_end(m));
+  if (m->taps) HIPCHK(copy_f32(s.x, s.ht, (size_t)B * L * d, m->stream));
+  TRY(prof_begin(m, TADM_STAGE_DENOISE));
+  TRY(run_part(m, cf.n_shared + cf.n_anchor, cf.n_denoise, s.x, B, L, pos0, ctx));
+  HIPCHK(rms_norm(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, B * Lc, d, Lc, L, off, s.xn, m->stream));
+  TRY(prof_end(m));
+  if (!logits) {
+    TRY(ensure_logits(m, (size_t)B * Lc * cf.vocab));
+    logits = s.logits;
+  }
+  TRY(prof_begin(m, TADM_STAGE_HEAD));
+  {
+    GemmProblem p{B * Lc, cf.vocab, d, s.xn, d, d, nullptr, 0, m->W(m->lay.w_out), d};
+    EpiParams e;
+    e.out = logits;
+    e.ldo = cf.vocab;
+    HIPCHK(gemm(m->dt, p, EPI_STORE_F32, e, m->stream));
+  }
+  TRY(prof_end(m));
+  m->tap_B = B;
+  m->tap_L = L;
+  m->tap_Lc = Lc;
+  return sample_impl(m, logits, canvas, B, L, off, pos0, a, next, s.choice, s.conf);
+}
+
+tadm_status tadm_denoise_step(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev, int32_t B,
+                              int32_t L, int32_t canvas_off, const tadm_cache* cache,
+                              const tadm_step_args* args, float* logits_dev, int32_t* next_canvas_dev) {
+  TRY(check_model(m));
+  if (!canvas_dev || !cache || !next_canvas_dev) return fail(TADM_ERR_INVALID, "null argument");
+  TRY(check_window(m, ctx, B, L));
+  if (canvas_off < 0 || canvas_off >= L) return fail(TADM_ERR_INVALID, "canvas_off=%d with L=%d", canvas_off, L);
+  TRY(check_args(args, L - canvas_off));
+  if (cache->model != m || cache->B != B || cache->L != L)
+    return fail(TADM_ERR_STATE, "cache built for another model or shape");
+  if (cache->refresh_i == 0) return fail(TADM_ERR_STATE, "cache was never refreshed");
+  if (m->cfg.vocab % 4) return fail(TADM_ERR_UNSUPPORTED, "the vocabulary head needs vocab %% 4 == 0");
+  TRY(ensure_workspace(m));
+  return denoise_impl(m, ctx, canvas_dev, B, L, canvas_off, cache, args, logits_dev, next_canvas_dev);
+}
+
+tadm_status tadm_sample(tadm_model* m, const float* logits_dev, const int32_t* canvas_dev, int32_t B, int32_t L,
+                        int32_t canvas_off, int32_t pos0, const tadm_step_args* args, int32_t* next_canvas_dev,
+                        int32_t* choice_dev, float* conf_dev) {
+  if (!m) return fail(TADM_ERR_INVALID, "null model");
+  if (!logits_dev || !canvas_dev || !next_canvas_dev) return fail(TADM_ERR_INVALID, "null argument");
+  if (B < 1 || B > m->cfg.max_batch || L < 1 || L > m->cfg.max_seq || canvas_off < 0 || canvas_off >= L || pos0 < 0)
+    return fail(TADM_ERR_INVALID, "sample shape B=%d L=%d off=%d", B, L, canvas_off);
+  TRY(check_args(args, L - canvas_off));
+  TRY(ensure_workspace(m));
+  return sample_impl(m, logits_dev, canvas_dev, B, L, canvas_off, pos0, args, next_canvas_dev,
+                     choice_dev ? choice_dev : m->ws.choice, conf_dev ? conf_dev : m->ws.conf);
+}
+
+// --------------------------------------------------------------- generate ---
+// Algorithm 1 per block; the model-owned cache, context and window are reused
+// across calls, so a warm generation allocates nothing and never synchronises.
+tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, int32_t P, int32_t gen_len,
+                          int32_t T, int32_t K, int32_t block_len, uint64_t seed, float temperature,
+                          int32_t* tokens_dev) {
+  TRY(check_model(m));
+  if (!tokens_dev || (P > 0 && !prompt_dev)) return fail(TADM_ERR_INVALID, "null argument");
+  if (B < 1 || B > m->cfg.max_batch) return fail(TADM_ERR_INVALID, "B=%d outside [1, %d]", B, m->cfg.max_batch);
+  if (P < 0 || gen_len < 1 || block_len < 1 || gen_len % block_len)
+    return fail(TADM_ERR_INVALID, "gen_len=%d must be a positive multiple of block_len=%d", gen_len, block_len);
+  if (T < 1 || K < 1) return fail(TADM_ERR_INVALID, "T=%d K=%d", T, K);
+  if (!(temperature > 0) || !std::isfinite(temperature)) return fail(TADM_ERR_INVALID, "temperature must be > 0");
+  if (P + gen_len > m->cfg.max_seq) return fail(TADM_ERR_INVALID, "P + gen_len exceeds max_seq");
+  const bool single = block_len == gen_len;
+  if (!single && P < 1) return fail(TADM_ERR_INVALID, "block mode needs a prompt");
+  if (m->cfg.vocab % 4) return fail(TADM_ERR_UNSUPPORTED, "the vocabulary head needs vocab %% 4 == 0");
+  TRY(ensure_workspace(m));
+  if (!m->gcache) TRY(cache_alloc(m, m->cfg.max_batch, m->cfg.max_seq, &m->gcache));
+  const int L = P + gen_len, mask = m->cfg.vocab;
+  tadm_step_args a{};
+  a.T = T;
+  a.seed = seed;
+  a.inv_temp = (float)(1.0 / (double)temperature);
+  HIPCHK(init_canvas(prompt_dev, B, P, gen_len, mask, tokens_dev, m->stream));
+  tadm_cache* cache = m->gcache;
+  if (single) {
+    cache->B = B;
+    cache->L = L;
+    for (int i = T; i >= 1; --i) {
+      a.i = i;
+      a.step_id = (uint32_t)(T - i);
+      a.n_unmask = tadm_unmask_count(gen_len, i, T);
+      if ((T - i) % K == 0) TRY(anchor_impl(m, nullptr, tokens_dev, B, L, i, cache));
+      TRY(denoise_impl(m, nullptr, tokens_dev, B, L, P, cache, &a, nullptr, tokens_dev));
+    }
+    return TADM_OK;
+  }
+  if (!m->gctx) TRY(tadm_context_create(m, m->cfg.max_batch, m->cfg.max_seq, &m->gctx));
+  if (!m->gwin) HIPCHK(hipMalloc((void**)&m->gwin, (size_t)m->cfg.max_batch * m->cfg.max_seq * 4));
+  TRY(ensure_scratch(m));
+  tadm_context* ctx = m->gctx;
+  ctx->B = B;  // rows [0, B) of the max_batch-row buffers
+  ctx->len = 0;
+  cache->B = B;
+  cache->L = block_len;
+  int32_t* win = m->gwin;
+  TRY(prof_begin(m, TADM_STAGE_CONTEXT));
+  TRY(context_append_impl(m, ctx, prompt_dev, B, P, m->scratch));
+  TRY(prof_end(m));
+  const int nblocks = gen_len / block_len;
+  for (int j = 0; j < nblocks; ++j) {
+    HIPCHK(fill_i32(win, (size_t)B * block_len, mask, m->stream));
+    for (int i = T; i >= 1; --i) {
+      a.i = i;
+      a.step_id = (uint32_t)(j * T + (T - i));
+      a.n_unmask = tadm_unmask_count(block_len, i, T);
+      if ((T - i) % K == 0) TRY(anchor_impl(m, ctx, win, B, block_len, i, cache));
+      TRY(denoise_impl(m, ctx, win, B, block_len, 0, cache, &a, nullptr, win));
+    }
+    HIPCHK(hipMemcpy2DAsync(tokens_dev + P + j * block_len, (size_t)L * 4, win, (size_t)block_len * 4,
+                            (size_t)block_len * 4, B, hipMemcpyDeviceToDevice, m->stream));
+    if (j + 1 < nblocks) {
+      TRY(prof_begin(m, TADM_STAGE_CONTEXT));
+      TRY(context_append_impl(m, ctx, win, B, block_len, m->scratch));
+      TRY(prof_end(m));
+    }
+  }
+  return TADM_OK;
+}
+
+
+// ---------------------------------------------------------- observability ---
+tadm_status tadm_debug_read(tadm_model* m, int32_t tap, float* dst_dev, size_t bytes) {
+  if (!m || !dst_dev) return fail(TADM_ERR_INVALID, "null argument");
+  const size_t d = m->cfg.d_model;
+  switch (tap) {
+    case TADM_TAP_EMBED:
+    case TADM_TAP_FUSED: {
+      if (tap == TADM_TAP_FUSED && !m->taps) return fail(TADM_ERR_STATE, "enable taps before the step");
+      const size_t n = (size_t)m->tap_B * m->tap_L * d;
+      if (bytes != n * 4) return fail(TADM_ERR_INVALID, "tap %d has %zu bytes", tap, n * 4);
+      HIPCHK(hipMemcpyAsync(dst_dev, tap == TADM_TAP_EMBED ? m->ws.c : m->ws.ht, bytes,
+                            hipMemcpyDeviceToDevice, m->stream));
+      return TADM_OK;
+    }
+    case TADM_TAP_FINAL: {
+      const size_t n = (size_t)m->tap_B * m->tap_Lc * d;
+      if (bytes != n * 4) return fail(TADM_ERR_INVALID, "tap %d has %zu bytes", tap, n * 4);
+      HIPCHK(to_f32(m->dt, m->ws.xn, dst_dev, n, m->stream));
+      return TADM_OK;
+    }
+    default:
+      return fail(TADM_ERR_INVALID, "tap %d", tap);
+  }
+}
+
+tadm_status tadm_debug_taps(tadm_model* m, int32_t enable) {
+  if (!m) return fail(TADM_ERR_INVALID, "null model");
+  m->taps = enable != 0;
+  return TADM_OK;
+}
+
+tadm_status tadm_profile_enable(tadm_model* m, int32_t enable) {
+  if (!m) return fail(TADM_ERR_INVALID, "null model");
+  m->prof = enable != 0;
+  return TADM_OK;
+}
+
+tadm_status tadm_profile_reset(tadm_model* m) {
+  if (!m) return fail(TADM_ERR_INVALID, "null model");
+  HIPCHK(hipStreamSynchronize(m->stream));
+  for (auto& r : m->recs) {
+    m->pool.push_back(r.a);
+    m->pool.push_back(r.b);
+  }
+  m->recs.clear();
+  return TADM_OK;
+}
+
+tadm_status tadm_profile_read(tadm_model* m, int32_t stage, double* total_ms, int64_t* count) {
+  if (!m || !total_ms || !count) return fail(TADM_ERR_INVALID, "null argument");
+  if (stage < 0 || stage >= TADM_STAGE_COUNT) return fail(TADM_ERR_INVALID, "stage %d", stage);
+  HIPCHK(hipStreamSynchronize(m->stream));
+  double tot = 0;
+  int64_t n = 0;
+  for (auto& r : m->recs)
+    if (r.stage == stage) {
+      float ms = 0;
+      HIPCHK(hipEventElapsedTime(&ms, r.a, r.b));
+      tot += ms;
+      ++n;
+    }
+  *total_ms = tot;
+  *count = n;
+  return TADM_OK;
+}
+
+}  // extern "C"

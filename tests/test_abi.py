@@ -1,0 +1,72 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared symbol,
+agrees with the seeded input module on the weight order, and rejects bad arguments
+before touching the GPU."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import synth
+from oracle import loop
+
+tadm = pytest.importorskip("paper_2609_37924_amd")
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "tadm.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tadm_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert len(names) >= 25
+    for n in names:
+        assert hasattr(tadm.lib, n), n
+    assert set(tadm.EXPORTED) == set(names)
+
+
+@pytest.mark.parametrize("name", list(synth.CONFIGS))
+def test_weight_order_matches_inputs(name):
+    cfg = synth.get_config(name)
+    if cfg["fusion_kind"] == "paired":
+        pytest.skip("paired-attention fusion weights are not part of this build")
+    c = tadm.make_config(cfg)
+    specs = synth.weight_specs(cfg)
+    assert tadm.tadm_weight_count(c) == len(specs)
+    for i, (nm, shape, _) in enumerate(specs):
+        rows, cols = tadm.tadm_weight_info(c, i)
+        assert (rows, cols) == (shape[0], shape[1] if len(shape) > 1 else 0), nm
+
+
+def test_unmask_count_matches_schedule():
+    for M0, T in [(24, 16), (256, 64), (64, 32), (1024, 128), (7, 3), (0, 5)]:
+        for i in range(1, T + 1):
+            assert tadm.tadm_unmask_count(M0, i, T) == loop.unmask_count(M0, i, T)
+    assert tadm.tadm_unmask_count(5, 0, 4) == 0
+
+
+def test_invalid_arguments_fail_before_device_work():
+    cfg = synth.get_config("tiny")
+    bad = tadm.make_config(cfg)
+    bad.n_heads = 3  # not a multiple of n_kv_heads = 4
+    m = C.c_void_p()
+    assert tadm.lib.tadm_model_create(C.byref(bad), C.byref(m)) == tadm.TADM_ERR_INVALID
+    assert "n_kv_heads" in tadm.last_error()
+    bad = tadm.make_config(cfg)
+    bad.dtype = 7
+    assert tadm.lib.tadm_model_create(C.byref(bad), C.byref(m)) == tadm.TADM_ERR_INVALID
+    good = tadm.make_config(cfg)
+    r, k = C.c_int64(), C.c_int64()
+    assert tadm.lib.tadm_weight_info(C.byref(good), 10_000, C.byref(r), C.byref(k)) == tadm.TADM_ERR_INVALID
+    assert tadm.lib.tadm_generate(None, None, 1, 0, 8, 4, 1, 8, 0, 1.0, None) == tadm.TADM_ERR_INVALID
+    args = tadm.step_args(1, 4, 1, 0, 0, 1.0)
+    assert tadm.lib.tadm_sample(None, None, None, 1, 8, 0, 0, C.byref(args), None, None, None) \
+        == tadm.TADM_ERR_INVALID
+    assert tadm.lib.tadm_cache_destroy(None) == tadm.TADM_ERR_INVALID
+    assert tadm.lib.tadm_context_reset(None) == tadm.TADM_ERR_INVALID
+    with pytest.raises(tadm.TadmError):
+        tadm.check(tadm.lib.tadm_model_destroy(None))

@@ -1,0 +1,254 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Floating point: hidden states and logits within rtol = atol = 1e-4 (float32 models)
+or 2e-2 (bf16 models).  Integers (token choices, unmask order, canvases): bit-exact
+given identical logits; the confidence is compared bit for bit as well.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from helpers import dev, gpu_model, oracle_net, oracle_sample_rows, oracle_step, rows_close
+from oracle import loop
+
+pytestmark = pytest.mark.gpu
+
+tadm = pytest.importorskip("paper_2609_37924_amd")
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+FP32_TOL = dict(rtol=1e-4, atol=1e-4)
+BF16_TOL = dict(rtol=2e-2, atol=2e-2)
+
+
+def sync():
+    torch.cuda.synchronize()
+
+
+# ------------------------------------------------------------------ sampler
+@pytest.mark.parametrize("V,B,L,off,temp,ties", [
+    (256, 2, 40, 8, 1.0, False),
+    (1001, 3, 33, 0, 0.7, False),    # vocab not a multiple of 4: scalar path
+    (32768, 2, 24, 4, 1.0, False),
+    (64, 4, 64, 0, 1.0, True),       # duplicated rows and planted exact ties
+])
+def test_sampler_bit_exact(V, B, L, off, temp, ties):
+    cfg = synth.get_config("tiny", vocab=V)
+    m = tadm.tadm_model_create(tadm.make_config(cfg, max_batch=B, max_seq=L))
+    tadm.tadm_set_stream(m, torch.cuda.current_stream().cuda_stream)
+    try:
+        g = torch.Generator().manual_seed(V + L)
+        canvas = torch.randint(0, V, (B, L), generator=g, dtype=torch.int32)
+        canvas[:, off:][torch.rand(B, L - off, generator=g) < 0.7] = V
+        canvas[0, off:] = V  # one fully masked row
+        if ties:
+            canvas[1] = canvas[0]
+        logits = synth.make_logits(B * (L - off), V, seed=V, std=2.0, ties=ties).view(B, L - off, V)
+        if ties:
+            logits[1] = logits[0]
+        inv_temp = float(np.float32(1.0 / temp))
+        pos0, step_id, seed, n = 17, 5, 0x1234_5678_9ABC, 6
+        args = tadm.step_args(3, 8, n, step_id, seed, inv_temp)
+        d_log, d_can = logits.to(dev()), canvas.to(dev())
+        nxt = torch.empty_like(d_can)
+        choice = torch.empty(B, L - off, dtype=torch.int32, device=dev())
+        conf = torch.empty(B, L - off, dtype=torch.float32, device=dev())
+        tadm.tadm_sample(m, d_log, d_can, B, L, off, pos0, args, nxt, choice, conf)
+        sync()
+        r_next, r_choice, r_conf = oracle_sample_rows(logits.numpy(), canvas.numpy().astype(np.int64),
+                                                      V, n, pos0, off, step_id, seed, inv_temp)
+        masked = canvas[:, off:].numpy() == V
+        np.testing.assert_array_equal(choice.cpu().numpy()[masked], r_choice[masked])
+        np.testing.assert_array_equal(conf.cpu().numpy().view(np.int32)[masked],
+                                      r_conf.view(np.int32)[masked])
+        np.testing.assert_array_equal(nxt.cpu().numpy(), r_next)
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
+# --------------------------------------------------------- one teacher step
+def _teacher_step_parity(cfg, B, tol, rows=None, seed=0, n_masked=(None, None)):
+    """Refresh on canvas z0, then one stale step on canvas z1 (teacher forcing)."""
+    P, G = cfg["prompt_len"], cfg["gen_len"]
+    L = P + G
+    tensors = synth.make_weights(cfg, perturb=True)
+    net = oracle_net(cfg, tensors)
+    m = gpu_model(cfg, tensors, B, L)
+    try:
+        tadm.tadm_debug_taps(m, 1)
+        z0 = synth.make_teacher_canvas(cfg, n_masked[0] or G, batch=B, seed=seed + 11)
+        z1 = synth.make_teacher_canvas(cfg, n_masked[1] or (2 * G) // 3, batch=B, seed=seed + 12)
+        T, i = 16, 13
+        cache = tadm.tadm_cache_create(m, B, L)
+        d = cfg["d_model"]
+        d0, d1 = z0.to(dev()), z1.to(dev())
+        tadm.tadm_anchor_forward(m, None, d0, B, L, 16, T, cache)
+        h_gpu = torch.empty(B, L, d, device=dev())
+        tadm.tadm_cache_read(cache, tadm.CACHE_H, h_gpu)
+        n = tadm.tadm_unmask_count(G, i, T)
+        args = tadm.step_args(i, T, n, T - i, 77, 1.0)
+        logits = torch.empty(B, G, cfg["vocab"], device=dev())
+        nxt = torch.empty_like(d1)
+        tadm.tadm_denoise_step(m, None, d1, B, L, P, cache, args, logits, nxt)
+        taps = {}
+        for tap, shape in ((tadm.TAP_EMBED, (B, L, d)), (tadm.TAP_FUSED, (B, L, d)),
+                           (tadm.TAP_FINAL, (B, G, d))):
+            taps[tap] = torch.empty(shape, device=dev())
+            tadm.tadm_debug_read(m, tap, taps[tap])
+        sync()
+        pos = np.arange(L)
+        rows = range(B) if rows is None else rows
+        ref_logits = np.zeros((B, G, cfg["vocab"]), np.float32)
+        for b in rows:
+            cache_ref = net.anchor_cache(net.shared(z0[b].numpy(), pos), pos)
+            rows_close(h_gpu[b].cpu().numpy(), cache_ref["h"], tol["rtol"], tol["atol"], f"anchor h row {b}")
+            c, ht, xf, lg = oracle_step(net, z1[b].numpy(), pos, cache_ref, P)
+            rows_close(taps[tadm.TAP_EMBED][b].cpu().numpy(), c, tol["rtol"], tol["atol"], f"embed row {b}")
+            rows_close(taps[tadm.TAP_FUSED][b].cpu().numpy(), ht, tol["rtol"], tol["atol"], f"fused row {b}")
+            rows_close(taps[tadm.TAP_FINAL][b].cpu().numpy(), xf, tol["rtol"], tol["atol"], f"final row {b}")
+            rows_close(logits[b].cpu().numpy(), lg, tol["rtol"], tol["atol"], f"logits row {b}")
+            ref_logits[b] = lg
+        # the GPU reverse step on the oracle's logits is bit-exact with the oracle's
+        r_next, _, _ = oracle_sample_rows(ref_logits, z1.numpy().astype(np.int64), cfg["vocab"], n, 0, P,
+                                          T - i, 77, 1.0)
+        nxt2 = torch.empty_like(d1)
+        tadm.tadm_sample(m, torch.from_numpy(ref_logits).to(dev()), d1, B, L, P, 0, args, nxt2)
+        sync()
+        for b in rows:
+            np.testing.assert_array_equal(nxt2[b].cpu().numpy(), r_next[b])
+        tadm.tadm_cache_destroy(cache)
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
+def test_tiny_fp32_step_parity():
+    _teacher_step_parity(synth.get_config("tiny", batch=2), 2, FP32_TOL)
+
+
+def test_tiny_fp32_swiglu_gqa_step_parity():
+    cfg = synth.get_config("tiny", ffn_kind="swiglu", n_kv_heads=2, prompt_len=5, gen_len=70)
+    _teacher_step_parity(cfg, 2, FP32_TOL)
+
+
+def test_small_shape_bf16_step_parity():
+    """The small model's widths (d=768, 12x64 heads, SwiGLU 2048, V=32768) with fewer
+    layers and a ragged sequence (90 positions: 64-row tiles plus a tail)."""
+    cfg = synth.get_config("small", n_anchor=2, n_denoise=2, prompt_len=40, gen_len=50)
+    _teacher_step_parity(cfg, 2, BF16_TOL)
+
+
+def test_small_config_full_size_sampled_rows():
+    """Full small workload (12 anchor + 2 denoiser layers, B=8, 384 positions) in the
+    launch configuration of the benchmark; the oracle checks rows 0 and 7."""
+    cfg = synth.get_config("small")
+    _teacher_step_parity(cfg, 8, BF16_TOL, rows=[0, 7], n_masked=(256, 200))
+
+
+def test_gelu_bf16_step_parity():
+    """GELU feed-forward, d=2048 / 128-wide heads as in the 1B-class model, few layers."""
+    cfg = synth.get_config("1b", n_anchor=1, n_denoise=1, vocab=4096, prompt_len=16, gen_len=112)
+    _teacher_step_parity(cfg, 2, BF16_TOL)
+
+
+# -------------------------------------------------------------- generation
+def _generate(cfg, K, block_len=None, B=None):
+    B = B or cfg["batch"]
+    P, G, T = cfg["prompt_len"], cfg["gen_len"], cfg["T"]
+    bl = block_len or cfg["block_len"]
+    tensors = synth.make_weights(cfg, perturb=True)
+    prompt = synth.make_prompt(cfg, batch=B)
+    m = gpu_model(cfg, tensors, B, P + G)
+    try:
+        out = torch.empty(B, P + G, dtype=torch.int32, device=dev())
+        tadm.tadm_generate(m, prompt.to(dev()) if P else None, B, P, G, T, K, bl, 2, 1.0, out)
+        sync()
+        return tensors, prompt, out.cpu().numpy()
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
+@pytest.mark.parametrize("K", [4, 1])
+def test_tiny_generation_matches_oracle(K):
+    cfg = synth.get_config("tiny", batch=2)
+    tensors, prompt, got = _generate(cfg, K)
+    net = oracle_net(cfg, tensors)
+    ref = loop.generate(net, prompt.numpy(), cfg["gen_len"], cfg["T"], K, cfg["block_len"], 2, 1.0,
+                        synth.mask_id(cfg))
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_tiny_block_generation_matches_oracle():
+    cfg = synth.get_config("tiny", batch=2, n_kv_heads=2)
+    tensors, prompt, got = _generate(cfg, 4, block_len=8)
+    net = oracle_net(cfg, tensors)
+    ref = loop.generate(net, prompt.numpy(), cfg["gen_len"], cfg["T"], 4, 8, 2, 1.0, synth.mask_id(cfg))
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_bf16_generation_invariants():
+    cfg = synth.get_config("small", n_anchor=2, n_denoise=1, batch=3)
+    _, prompt, got = _generate(cfg, 4)
+    P = cfg["prompt_len"]
+    assert np.array_equal(got[:, :P], prompt.numpy())
+    assert (got >= 0).all() and (got < cfg["vocab"]).all()
+
+
+# -------------------------------------------------------------- invariants
+def test_cache_unchanged_between_refreshes_and_split_equals_generate():
+    cfg = synth.get_config("tiny", batch=2)
+    B, P, G, T, K = 2, cfg["prompt_len"], cfg["gen_len"], cfg["T"], 4
+    L = P + G
+    tensors = synth.make_weights(cfg, perturb=True)
+    prompt = synth.make_prompt(cfg, batch=B)
+    m = gpu_model(cfg, tensors, B, L)
+    try:
+        cache = tadm.tadm_cache_create(m, B, L)
+        z = torch.cat([prompt, torch.full((B, G), cfg["vocab"], dtype=torch.int32)], 1).to(dev())
+        snap = torch.empty(B, L, cfg["d_model"], device=dev())
+        for i in range(T, 0, -1):
+            if (T - i) % K == 0:
+                tadm.tadm_anchor_forward(m, None, z, B, L, i, T, cache)
+                tadm.tadm_cache_read(cache, tadm.CACHE_H, snap)
+                ref = snap.clone()
+            args = tadm.step_args(i, T, tadm.tadm_unmask_count(G, i, T), T - i, 2, 1.0)
+            nz = torch.empty_like(z)
+            tadm.tadm_denoise_step(m, None, z, B, L, P, cache, args, None, nz)
+            tadm.tadm_cache_read(cache, tadm.CACHE_H, snap)
+            sync()
+            assert torch.equal(snap, ref)
+            assert tadm.tadm_cache_refresh_step(cache) == T - ((T - i) // K) * K
+            z = nz
+        out = torch.empty(B, L, dtype=torch.int32, device=dev())
+        tadm.tadm_generate(m, prompt.to(dev()), B, P, G, T, K, G, 2, 1.0, out)
+        out2 = torch.empty_like(out)
+        tadm.tadm_generate(m, prompt.to(dev()), B, P, G, T, K, G, 2, 1.0, out2)
+        sync()
+        assert torch.equal(out, z)        # explicit step loop == one-shot generate
+        assert torch.equal(out, out2)     # deterministic
+        tadm.tadm_cache_destroy(cache)
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
+def test_state_errors():
+    cfg = synth.get_config("tiny")
+    tensors = synth.make_weights(cfg)
+    m = gpu_model(cfg, tensors, 1, 32)
+    try:
+        cache = tadm.tadm_cache_create(m, 1, 32)
+        z = torch.zeros(1, 32, dtype=torch.int32, device=dev())
+        args = tadm.step_args(1, 4, 1, 0, 0, 1.0)
+        with pytest.raises(tadm.TadmError) as e:     # never refreshed
+            tadm.tadm_denoise_step(m, None, z, 1, 32, 8, cache, args, None, z)
+        assert e.value.status == tadm.TADM_ERR_STATE
+        with pytest.raises(tadm.TadmError) as e:     # shape mismatch
+            tadm.tadm_anchor_forward(m, None, z, 1, 16, 1, 4, cache)
+        assert e.value.status == tadm.TADM_ERR_STATE
+        with pytest.raises(tadm.TadmError) as e:     # batch too large
+            tadm.tadm_anchor_forward(m, None, z, 2, 32, 1, 4, cache)
+        assert e.value.status == tadm.TADM_ERR_INVALID
+        tadm.tadm_cache_destroy(cache)
+    finally:
+        tadm.tadm_model_destroy(m)
