@@ -11,6 +11,16 @@ of App. C.2 with time conditioning disabled): RMSNorm, multi-head attention with
 rotary positions (rotate-half, base 10^4) and grouped KV heads, residual, RMSNorm,
 feed-forward (GELU, SwiGLU or GeGLU), residual.
 
+Precision.  Weights are the stored values (bf16 or fp32) and all arithmetic is
+float64.  A bf16 model (config dtype "bf16") additionally takes every operand of a
+matrix product in bf16: activations are rounded to bf16 (round to nearest even)
+where they enter a product -- the normalised input of each projection, Q and K after
+the rotary embedding, V, the softmax probabilities, the attention output, the
+feed-forward hidden state, the fusion input u and hidden state, the head input --
+while accumulation, norms, softmax, residual stream and elementwise maths stay in
+float64.  That is the mixed-precision bf16 model (bf16 operands, wide accumulation);
+a float32 model has no rounding.
+
 Each function works on one batch row (arrays [L, ...]); rows are independent.
 """
 import numpy as np
@@ -18,6 +28,18 @@ from scipy.special import erf
 
 
 # --------------------------------------------------------------------------- ops
+def round_bf16(x):
+    """Round to the nearest bf16 value (8 significant bits), ties to even."""
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)                       # x = m 2^e, |m| in [0.5, 1)
+    return np.ldexp(np.round(m * 256.0) / 256.0, e)
+
+
+def operand(cfg, x):
+    """A matrix-product operand in the model's precision (identity for fp32 models)."""
+    return round_bf16(x) if cfg.get("dtype") == "bf16" else x
+
+
 def rms_norm(x, g, eps):
     return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * g
 
@@ -53,12 +75,14 @@ def rope(x, pos, theta):
     return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
 
 
-def attention(q, k, v):
+def attention(q, k, v, op=lambda x: x):
     """Softmax attention where every query sees every key.
 
     q [Lq, H, dh]; k, v [Lk, Hkv, dh]; query head h reads KV head floor(h*Hkv/H).
+    ``op`` maps a matrix-product operand to the model precision.
     """
     H, Hkv, dh = q.shape[1], k.shape[1], q.shape[2]
+    q, k, v = op(q), op(k), op(v)
     out = np.empty((q.shape[0], H, v.shape[2]))
     for h in range(H):
         kh = (h * Hkv) // H
@@ -66,7 +90,7 @@ def attention(q, k, v):
         s = s - s.max(axis=-1, keepdims=True)
         p = np.exp(s)
         p = p / p.sum(axis=-1, keepdims=True)
-        out[:, h, :] = p @ v[:, kh, :]
+        out[:, h, :] = op(p) @ v[:, kh, :]
     return out
 
 
@@ -96,7 +120,8 @@ def transformer_layer(W, li, x, pos, ctx_kv=None):
     eps, theta = cfg["rms_eps"], cfg["rope_theta"]
     p = f"layer{li}."
     L = x.shape[0]
-    xn = rms_norm(x, W[p + "attn_norm"], eps)
+    op = lambda t: operand(cfg, t)  # noqa: E731
+    xn = op(rms_norm(x, W[p + "attn_norm"], eps))
     q = (xn @ W[p + "wq"].T).reshape(L, H, dh)
     k = (xn @ W[p + "wk"].T).reshape(L, Hkv, dh)
     v = (xn @ W[p + "wv"].T).reshape(L, Hkv, dh)
@@ -106,9 +131,9 @@ def transformer_layer(W, li, x, pos, ctx_kv=None):
         v_all = np.concatenate([ctx_kv[1], v], axis=0)
     else:
         k_all, v_all = k, v
-    o = attention(q, k_all, v_all).reshape(L, H * dh)
+    o = op(attention(q, k_all, v_all, op).reshape(L, H * dh))
     x = x + o @ W[p + "wo"].T
-    xn = rms_norm(x, W[p + "ffn_norm"], eps)
+    xn = op(rms_norm(x, W[p + "ffn_norm"], eps))
     kind = cfg["ffn_kind"]
     if kind == "gelu":
         f = gelu(xn @ W[p + "w_up"].T)
@@ -118,7 +143,7 @@ def transformer_layer(W, li, x, pos, ctx_kv=None):
         f = gelu(xn @ W[p + "w_gate"].T) * (xn @ W[p + "w_up"].T)
     else:
         raise ValueError(kind)
-    return x + f @ W[p + "w_down"].T, (k, v)
+    return x + op(f) @ W[p + "w_down"].T, (k, v)
 
 
 def layer_ids(cfg, part):
@@ -156,7 +181,7 @@ def denoiser(W, ht, pos, ctx=None, kv_out=None):
 
 def head(W, xf):
     """Vocabulary projection: one logit per real token (mask id excluded)."""
-    return xf @ W["w_out"].T
+    return operand(W.cfg, xf) @ W["w_out"].T
 
 
 # ----------------------------------------------------------------------- fusion
@@ -169,9 +194,10 @@ def fusion_gated_mlp(W, c, h):
     eps = W.cfg["ln_eps"]
     s = layer_norm(c, W["fusion.ln_s_w"], W["fusion.ln_s_b"], eps)
     a = layer_norm(h, W["fusion.ln_a_w"], W["fusion.ln_a_b"], eps)
-    u = np.concatenate([s, a], axis=-1)
+    u = operand(W.cfg, np.concatenate([s, a], axis=-1))
     g = sigmoid(u @ W["fusion.wg"].T + W["fusion.bg"])
-    delta = gelu(u @ W["fusion.w1"].T + W["fusion.b1"]) @ W["fusion.w2"].T + W["fusion.b2"]
+    hid = operand(W.cfg, gelu(u @ W["fusion.w1"].T + W["fusion.b1"]))
+    delta = hid @ W["fusion.w2"].T + W["fusion.b2"]
     return layer_norm(h + g * delta, W["fusion.ln_o_w"], W["fusion.ln_o_b"], eps)
 
 
@@ -183,14 +209,15 @@ def paired_mixer(W, Z, U):
     phi = R + SiLU(R W_1) W_2.
     """
     nh = W.cfg["paired_heads"]
+    op = lambda t: operand(W.cfg, t)  # noqa: E731
     r = Z.shape[1]
-    J = np.concatenate([Z, U], axis=-1)
+    J = op(np.concatenate([Z, U], axis=-1))
     L = J.shape[0]
     q = (J @ W["fusion.w_q"].T).reshape(L, nh, r // nh)
     k = (J @ W["fusion.w_k"].T).reshape(L, nh, r // nh)
     v = (J @ W["fusion.w_v"].T).reshape(L, nh, r // nh)
-    R = Z + attention(q, k, v).reshape(L, r) @ W["fusion.w_o"].T
-    return R + silu(R @ W["fusion.w_f1"].T) @ W["fusion.w_f2"].T
+    R = Z + op(attention(q, k, v, op).reshape(L, r)) @ W["fusion.w_o"].T
+    return R + op(silu(op(R) @ W["fusion.w_f1"].T)) @ W["fusion.w_f2"].T
 
 
 def fusion_paired(W, C, C0, H0):
@@ -203,15 +230,16 @@ def fusion_paired(W, C, C0, H0):
     H~ = H0 + g * s_H * (M W_up).
     """
     eps = W.cfg["rms_eps"]
+    op = lambda t: operand(W.cfg, t)  # noqa: E731
     sC = np.sqrt(np.mean(C0 * C0, axis=-1, keepdims=True) + eps)
     sH = np.sqrt(np.mean(H0 * H0, axis=-1, keepdims=True) + eps)
-    Z = (C / sC) @ W["fusion.w_c"].T
-    Z0 = (C0 / sC) @ W["fusion.w_c"].T
-    U = (H0 / sH) @ W["fusion.w_h"].T
+    Z = op(C / sC) @ W["fusion.w_c"].T
+    Z0 = op(C0 / sC) @ W["fusion.w_c"].T
+    U = op(H0 / sH) @ W["fusion.w_h"].T
     M = paired_mixer(W, Z, U) - paired_mixer(W, Z0, U)
-    F = np.concatenate([U, Z0, Z - Z0, M], axis=-1)
-    g = sigmoid(silu(F @ W["fusion.w_g1"].T) @ W["fusion.w_g2"].T + W["fusion.b_g"])
-    return H0 + g * sH * (M @ W["fusion.w_up"].T)
+    F = op(np.concatenate([U, Z0, Z - Z0, M], axis=-1))
+    g = sigmoid(op(silu(F @ W["fusion.w_g1"].T)) @ W["fusion.w_g2"].T + W["fusion.b_g"])
+    return H0 + g * sH * (op(M) @ W["fusion.w_up"].T)
 
 
 def fuse(W, c, cache):

@@ -113,3 +113,29 @@ def test_transformer_layer_matches_torch_formulation(ffn, kv):
     out, _ = N.transformer_layer(W, 1, x, np.array(pos), ctx)
     ref = _torch_layer(cfg, Wt, 1, t64(x), pos, (t64(ctx[0]), t64(ctx[1]))).numpy()
     np.testing.assert_allclose(out, ref, rtol=1e-9, atol=1e-11)
+
+
+def test_round_bf16_is_round_to_nearest_even():
+    x = (rng.normal(size=20000) * 10.0 ** rng.integers(-3, 4, size=20000)).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(N.round_bf16(x.astype(np.float64)), ref)
+    # exact ties go to the even neighbour: 1 + 2^-8 lies halfway between 1 and 1 + 2^-7
+    assert N.round_bf16(1.0 + 2.0 ** -8) == 1.0
+    assert N.round_bf16(1.0 + 3 * 2.0 ** -8) == 1.0 + 2.0 ** -6
+
+
+def test_bf16_model_rounds_only_product_operands():
+    """A bf16 layer equals the float64 layer up to bf16 operand rounding, and with
+    operands that are already bf16 values the rounding is a no-op."""
+    cfg32 = synth.get_config("tiny", dtype="f32")
+    cfg16 = synth.get_config("tiny", dtype="bf16")
+    specs = synth.weight_specs(cfg16)
+    ws = synth.make_weights(cfg16, perturb=True)
+    W16 = N.Weights(cfg16, [s[0] for s in specs], ws)
+    W32 = N.Weights(cfg32, [s[0] for s in specs], ws)
+    x = rng.normal(size=(12, 64))
+    a, _ = N.transformer_layer(W16, 0, x, np.arange(12))
+    b, _ = N.transformer_layer(W32, 0, x, np.arange(12))
+    assert 0 < np.abs(a - b).max() < 2e-2
+    v = N.round_bf16(rng.normal(size=100))
+    assert np.array_equal(N.operand(cfg16, v), v) and np.array_equal(N.operand(cfg32, x), x)
