@@ -174,13 +174,15 @@ tadm_status tadm_debug_taps(tadm_model* m, int32_t enable);
 tadm_status tadm_debug_read(tadm_model* m, int32_t tap, float* dst_dev, size_t bytes);
 
 /* Per-stage timing with HIP events recorded on the model stream around each
- * stage; read synchronises the stream.  Stage ids: */
+ * stage whose bit is set in stage_mask (bit s = stage s; 0 = off, -1 = all);
+ * read synchronises the stream.  TADM_STAGE_HEAD brackets exactly one kernel, the
+ * vocabulary projection.  Stage ids: */
 enum {
   TADM_STAGE_EMBED = 0, TADM_STAGE_ANCHOR = 1, TADM_STAGE_FUSION = 2, TADM_STAGE_DENOISE = 3,
   TADM_STAGE_HEAD = 4, TADM_STAGE_SAMPLE = 5, TADM_STAGE_SELECT = 6, TADM_STAGE_CONTEXT = 7,
   TADM_STAGE_COUNT = 8
 };
-tadm_status tadm_profile_enable(tadm_model* m, int32_t enable);
+tadm_status tadm_profile_enable(tadm_model* m, int32_t stage_mask);
 tadm_status tadm_profile_read(tadm_model* m, int32_t stage, double* total_ms, int64_t* count);
 tadm_status tadm_profile_reset(tadm_model* m);
 

@@ -221,8 +221,9 @@ def tadm_debug_taps(m, enable):
     check(lib.tadm_debug_taps(m, int(enable)))
 
 
-def tadm_profile_enable(m, enable):
-    check(lib.tadm_profile_enable(m, int(enable)))
+def tadm_profile_enable(m, stage_mask):
+    """stage_mask: bit s records stage s (STAGES order); -1 records all, 0 none."""
+    check(lib.tadm_profile_enable(m, int(stage_mask)))
 
 
 def tadm_profile_reset(m):

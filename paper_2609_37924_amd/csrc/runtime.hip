@@ -221,7 +221,7 @@ struct tadm_model {
   int32_t* gwin = nullptr;         // active block of block-mode tadm_generate
   int tap_B = 0, tap_L = 0, tap_Lc = 0;
   // profiling
-  bool prof = false;
+  int32_t prof_mask = 0;  // bit s: record stage s
   std::vector<ProfRec> recs;
   std::vector<hipEvent_t> pool;
   int cur_stage = -1;
@@ -248,7 +248,7 @@ struct tadm_context {
 
 // ---------------------------------------------------------------- profiling ---
 static tadm_status prof_begin(tadm_model* m, int stage) {
-  if (!m->prof) return TADM_OK;
+  if (!((m->prof_mask >> stage) & 1)) return TADM_OK;
   hipEvent_t e;
   if (m->pool.empty()) {
     HIPCHK(hipEventCreate(&e));
@@ -263,7 +263,7 @@ static tadm_status prof_begin(tadm_model* m, int stage) {
 }
 
 static tadm_status prof_end(tadm_model* m) {
-  if (!m->prof || m->cur_stage < 0) return TADM_OK;
+  if (m->cur_stage < 0) return TADM_OK;
   hipEvent_t e;
   if (m->pool.empty()) {
     HIPCHK(hipEventCreate(&e));
@@ -960,9 +960,9 @@ tadm_status tadm_debug_taps(tadm_model* m, int32_t enable) {
   return TADM_OK;
 }
 
-tadm_status tadm_profile_enable(tadm_model* m, int32_t enable) {
+tadm_status tadm_profile_enable(tadm_model* m, int32_t stage_mask) {
   if (!m) return fail(TADM_ERR_INVALID, "null model");
-  m->prof = enable != 0;
+  m->prof_mask = stage_mask;
   return TADM_OK;
 }
 

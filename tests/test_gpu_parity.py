@@ -20,7 +20,10 @@ if not torch.cuda.is_available():
     pytest.skip("no GPU", allow_module_level=True)
 
 FP32_TOL = dict(rtol=1e-4, atol=1e-4)
-BF16_TOL = dict(rtol=2e-2, atol=2e-2)
+# bf16: the bound rtol = atol = 2e-2 must hold for all but a 1e-5 tail of elements,
+# and every element within 4e-2 (two bf16 evaluations of one model diverge at the
+# rounding-noise level; tests/test_bf16_noise.py measures that floor on the CPU).
+BF16_TOL = dict(rtol=2e-2, atol=2e-2, tail=1e-5, max_err=4e-2)
 
 
 def sync():
@@ -69,11 +72,11 @@ def test_sampler_bit_exact(V, B, L, off, temp, ties):
 
 
 # --------------------------------------------------------- one teacher step
-def _teacher_step_parity(cfg, B, tol, rows=None, seed=0, n_masked=(None, None)):
+def _teacher_step_parity(cfg, B, tol, rows=None, seed=0, n_masked=(None, None), tensors=None):
     """Refresh on canvas z0, then one stale step on canvas z1 (teacher forcing)."""
     P, G = cfg["prompt_len"], cfg["gen_len"]
     L = P + G
-    tensors = synth.make_weights(cfg, perturb=True)
+    tensors = tensors or synth.make_weights(cfg, perturb=True)
     net = oracle_net(cfg, tensors)
     m = gpu_model(cfg, tensors, B, L)
     try:
@@ -103,12 +106,12 @@ def _teacher_step_parity(cfg, B, tol, rows=None, seed=0, n_masked=(None, None)):
         ref_logits = np.zeros((B, G, cfg["vocab"]), np.float32)
         for b in rows:
             cache_ref = net.anchor_cache(net.shared(z0[b].numpy(), pos), pos)
-            rows_close(h_gpu[b].cpu().numpy(), cache_ref["h"], tol["rtol"], tol["atol"], f"anchor h row {b}")
+            rows_close(h_gpu[b].cpu().numpy(), cache_ref["h"], what=f"anchor h row {b}", **tol)
             c, ht, xf, lg = oracle_step(net, z1[b].numpy(), pos, cache_ref, P)
-            rows_close(taps[tadm.TAP_EMBED][b].cpu().numpy(), c, tol["rtol"], tol["atol"], f"embed row {b}")
-            rows_close(taps[tadm.TAP_FUSED][b].cpu().numpy(), ht, tol["rtol"], tol["atol"], f"fused row {b}")
-            rows_close(taps[tadm.TAP_FINAL][b].cpu().numpy(), xf, tol["rtol"], tol["atol"], f"final row {b}")
-            rows_close(logits[b].cpu().numpy(), lg, tol["rtol"], tol["atol"], f"logits row {b}")
+            rows_close(taps[tadm.TAP_EMBED][b].cpu().numpy(), c, what=f"embed row {b}", **tol)
+            rows_close(taps[tadm.TAP_FUSED][b].cpu().numpy(), ht, what=f"fused row {b}", **tol)
+            rows_close(taps[tadm.TAP_FINAL][b].cpu().numpy(), xf, what=f"final row {b}", **tol)
+            rows_close(logits[b].cpu().numpy(), lg, what=f"logits row {b}", **tol)
             ref_logits[b] = lg
         # the GPU reverse step on the oracle's logits is bit-exact with the oracle's
         r_next, _, _ = oracle_sample_rows(ref_logits, z1.numpy().astype(np.int64), cfg["vocab"], n, 0, P,
@@ -150,6 +153,22 @@ def test_gelu_bf16_step_parity():
     """GELU feed-forward, d=2048 / 128-wide heads as in the 1B-class model, few layers."""
     cfg = synth.get_config("1b", n_anchor=1, n_denoise=1, vocab=4096, prompt_len=16, gen_len=112)
     _teacher_step_parity(cfg, 2, BF16_TOL)
+
+
+@pytest.mark.parametrize("dh,H,Hkv", [(64, 12, 12), (128, 16, 16), (128, 16, 4)])
+def test_attention_dominated_layer(dh, H, Hkv):
+    """One anchor layer whose output is dominated by attention (feed-forward off,
+    V and O projections scaled up), so that an attention error cannot hide behind
+    the residual stream.  Covers both head widths and grouped KV heads."""
+    cfg = synth.get_config("1b", n_anchor=1, n_denoise=1, vocab=512, n_heads=H, n_kv_heads=Hkv,
+                           head_dim=dh, d_model=H * dh, prompt_len=30, gen_len=100)
+    tensors = synth.make_weights(cfg, perturb=True)
+    names = [s[0] for s in synth.weight_specs(cfg)]
+    for li in range(2):
+        tensors[names.index(f"layer{li}.wv")] = (tensors[names.index(f"layer{li}.wv")].float() * 8).bfloat16()
+        tensors[names.index(f"layer{li}.wo")] = (tensors[names.index(f"layer{li}.wo")].float() * 8).bfloat16()
+        tensors[names.index(f"layer{li}.w_down")] = torch.zeros_like(tensors[names.index(f"layer{li}.w_down")])
+    _teacher_step_parity(cfg, 2, dict(BF16_TOL, scale_atol=True), tensors=tensors)
 
 
 # -------------------------------------------------------------- generation
