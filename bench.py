@@ -36,8 +36,12 @@ def parse():
 
 
 def head_flops(cfg, B):
-    """Algorithmic flops of one vocabulary-projection launch: 2 * rows * d * V."""
-    return 2.0 * B * cfg["gen_len"] * cfg["d_model"] * cfg["vocab"]
+    """Algorithmic flops of the average vocabulary-projection launch, 2 * rows * d * V,
+    where rows = the masked positions entering step i: B * floor(M0 * i / T) with M0
+    the block length (the head only runs on masked positions)."""
+    M0, T = cfg["block_len"], cfg["T"]
+    rows = sum(B * ((M0 * i) // T) for i in range(1, T + 1)) / T
+    return 2.0 * rows * cfg["d_model"] * cfg["vocab"]
 
 
 def workload_name(cfg):

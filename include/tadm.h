@@ -130,8 +130,10 @@ tadm_status tadm_anchor_forward(tadm_model* m, const tadm_context* ctx, const in
  * MDLM posterior with carry-over, App. B.1.1):
  * c = S(canvas), h~ = Phi(c, cache), x = D(h~), logits = head(x) for the canvas
  * columns [canvas_off, L), then tadm_sample.  logits_dev (float32
- * [B, L - canvas_off, V]) may be NULL; next_canvas_dev [B, L] receives the canvas
- * after the step.  The cache is read only. */
+ * [B, L - canvas_off, V]) may be NULL: then the head runs only on the masked
+ * positions (the only ones whose logits the reverse step uses).  next_canvas_dev
+ * [B, L] receives the canvas after the step (it may alias canvas_dev).  The cache
+ * is read only. */
 tadm_status tadm_denoise_step(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev,
                               int32_t B, int32_t L, int32_t canvas_off, const tadm_cache* cache,
                               const tadm_step_args* args, float* logits_dev,
@@ -167,7 +169,8 @@ int32_t tadm_unmask_count(int32_t M0, int32_t i, int32_t T);
 /* Copies (float32) a buffer of the last step into dst_dev:
  *   TADM_TAP_EMBED  c = S(z)          [B, L, d]
  *   TADM_TAP_FUSED  h~ = Phi(c, h')   [B, L, d]
- *   TADM_TAP_FINAL  final-normed D output of the canvas columns [B, L - off, d] */
+ *   TADM_TAP_FINAL  final-normed D output of the canvas columns [B, L - off, d]
+ *                   (only after a step that was given logits_dev) */
 enum { TADM_TAP_EMBED = 0, TADM_TAP_FUSED = 1, TADM_TAP_FINAL = 2 };
 /* Keep a copy of h~ for TADM_TAP_FUSED (one extra [B, L, d] copy per step; off by default). */
 tadm_status tadm_debug_taps(tadm_model* m, int32_t enable);

@@ -1,136 +1,169 @@
 // Dense contractions of the TADM step: C = A W^T with fused epilogues.
 //
-// bf16 path: v_mfma_f32_16x16x32_bf16 on LDS-staged, double-buffered 64-deep K
-// tiles.  The weight tile is the MFMA "A" operand and the activation tile the "B"
-// operand, so each lane ends with 4 consecutive output features of one row and
-// stores them as one 8/16-byte vector.  256 threads = 4 wave64s in a 2x2 grid.
-// float32 path (small fp32 models): a register-blocked VALU kernel with the same
-// epilogues.
+// bf16 path (gfx950): WGM x WGN wave64s per block, block tile BM x BN, K tiles of
+// 64.  Tiles move global -> LDS with global_load_lds_dwordx4 (no register staging) through a STAGES-deep ring of LDS buffers, so that STAGES-1 tiles are in
+// flight while one is multiplied.  LDS rows are 128 B (64 bf16); the 16-byte chunk c
+// of row r is stored in slot c ^ (r & 7), which makes the MFMA fragment reads
+// (16 rows x one chunk) hit distinct banks; the permutation is applied through the
+// global addresses because each lane's 16 bytes land at a fixed LDS slot.
+// Products use v_mfma_f32_16x16x32_bf16 with the weight tile as the "A" operand and
+// the activation tile as "B", so every lane ends with 4 consecutive output features
+// of one row and stores them as one vector.  Blocks are renumbered so that the
+// tiles sharing a weight panel run on the same XCD (each XCD has its own L2).
+// float32 path (small fp32 models): a register-blocked VALU kernel, same epilogues.
 #include "common.h"
 #include "kernels.h"
 
 namespace tadm {
 namespace {
 
-template <class T>
-struct Epi {
-  EpiKind kind;
-  EpiParams e;
+// ------------------------------------------------------------------ epilogues
+template <EpiKind K, class T>
+struct Epi;
 
-  __device__ __forceinline__ void operator()(int m, int n, f32x4 v) const {
-    switch (kind) {
-      case EPI_STORE: {
-        T* o = static_cast<T*>(e.out) + (size_t)m * e.ldo + n;
-        store4(o, v[0], v[1], v[2], v[3]);
-        break;
-      }
-      case EPI_STORE_F32: {
-        float* o = static_cast<float*>(e.out) + (size_t)m * e.ldo + n;
-        store4(o, v[0], v[1], v[2], v[3]);
-        break;
-      }
-      case EPI_RESID: {
-        float4* r = reinterpret_cast<float4*>(e.resid + (size_t)m * e.ldr + n);
-        float4 x = *r;
-        x.x += v[0]; x.y += v[1]; x.z += v[2]; x.w += v[3];
-        *r = x;
-        break;
-      }
-      case EPI_GELU: {
-        T* o = static_cast<T*>(e.out) + (size_t)m * e.ldo + n;
-        store4(o, gelu_erf(v[0]), gelu_erf(v[1]), gelu_erf(v[2]), gelu_erf(v[3]));
-        break;
-      }
-      case EPI_FUSION1: {
-        const float4 b = *reinterpret_cast<const float4*>(e.bias + n);
-        if (n < e.split) {
-          T* o = static_cast<T*>(e.out) + (size_t)m * e.ldo + n;
-          store4(o, gelu_erf(v[0] + b.x), gelu_erf(v[1] + b.y), gelu_erf(v[2] + b.z),
-                 gelu_erf(v[3] + b.w));
-        } else {
-          float* o = e.out2 + (size_t)m * e.ldo2 + (n - e.split);
-          store4(o, sigmoidf_(v[0] + b.x), sigmoidf_(v[1] + b.y), sigmoidf_(v[2] + b.z),
-                 sigmoidf_(v[3] + b.w));
-        }
-        break;
-      }
-      case EPI_FUSION2: {
-        const float4 b = *reinterpret_cast<const float4*>(e.bias + n);
-        const float4 h = *reinterpret_cast<const float4*>(e.aux + (size_t)m * e.ld_aux + n);
-        const float4 g = *reinterpret_cast<const float4*>(e.gate + (size_t)m * e.ldg + n);
-        float* o = e.resid + (size_t)m * e.ldr + n;
-        store4(o, h.x + g.x * (v[0] + b.x), h.y + g.y * (v[1] + b.y), h.z + g.z * (v[2] + b.z),
-               h.w + g.w * (v[3] + b.w));
-        break;
-      }
-      default:
-        break;
+template <class T>
+struct Epi<EPI_STORE, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + n, v[0], v[1], v[2], v[3]);
+  }
+};
+template <class T>
+struct Epi<EPI_STORE_F32, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    store4(static_cast<float*>(e.out) + (size_t)m * e.ldo + n, v[0], v[1], v[2], v[3]);
+  }
+};
+template <class T>
+struct Epi<EPI_RESID, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    float4* r = reinterpret_cast<float4*>(e.resid + (size_t)m * e.ldr + n);
+    float4 x = *r;
+    x.x += v[0]; x.y += v[1]; x.z += v[2]; x.w += v[3];
+    *r = x;
+  }
+};
+template <class T>
+struct Epi<EPI_GELU, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + n, gelu_erf(v[0]), gelu_erf(v[1]),
+           gelu_erf(v[2]), gelu_erf(v[3]));
+  }
+};
+template <class T>
+struct Epi<EPI_FUSION1, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    const float4 b = *reinterpret_cast<const float4*>(e.bias + n);
+    if (n < e.split) {
+      store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + n, gelu_erf(v[0] + b.x),
+             gelu_erf(v[1] + b.y), gelu_erf(v[2] + b.z), gelu_erf(v[3] + b.w));
+    } else {
+      store4(e.out2 + (size_t)m * e.ldo2 + (n - e.split), sigmoidf_(v[0] + b.x),
+             sigmoidf_(v[1] + b.y), sigmoidf_(v[2] + b.z), sigmoidf_(v[3] + b.w));
     }
   }
-
-  // Gate/up pair of a GLU feed-forward: features f .. f+3.
-  __device__ __forceinline__ void glu(int m, int f, f32x4 g, f32x4 u) const {
-    T* o = static_cast<T*>(e.out) + (size_t)m * e.ldo + f;
-    if (kind == EPI_GLU_SILU)
-      store4(o, siluf_(g[0]) * u[0], siluf_(g[1]) * u[1], siluf_(g[2]) * u[2], siluf_(g[3]) * u[3]);
-    else
-      store4(o, gelu_erf(g[0]) * u[0], gelu_erf(g[1]) * u[1], gelu_erf(g[2]) * u[2],
-             gelu_erf(g[3]) * u[3]);
+};
+template <class T>
+struct Epi<EPI_FUSION2, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    const float4 b = *reinterpret_cast<const float4*>(e.bias + n);
+    const float4 h = *reinterpret_cast<const float4*>(e.aux + (size_t)m * e.ld_aux + n);
+    const float4 g = *reinterpret_cast<const float4*>(e.gate + (size_t)m * e.ldg + n);
+    store4(e.resid + (size_t)m * e.ldr + n, h.x + g.x * (v[0] + b.x), h.y + g.y * (v[1] + b.y),
+           h.z + g.z * (v[2] + b.z), h.w + g.w * (v[3] + b.w));
   }
-
-  __device__ __forceinline__ bool is_glu() const { return kind == EPI_GLU_SILU || kind == EPI_GLU_GELU; }
+};
+template <class T>
+struct Epi<EPI_GLU_SILU, T> {
+  static constexpr bool kGlu = true;
+  __device__ static void glu(const EpiParams& e, int m, int f, f32x4 g, f32x4 u) {
+    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + f, siluf_(g[0]) * u[0], siluf_(g[1]) * u[1],
+           siluf_(g[2]) * u[2], siluf_(g[3]) * u[3]);
+  }
+};
+template <class T>
+struct Epi<EPI_GLU_GELU, T> {
+  static constexpr bool kGlu = true;
+  __device__ static void glu(const EpiParams& e, int m, int f, f32x4 g, f32x4 u) {
+    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + f, gelu_erf(g[0]) * u[0],
+           gelu_erf(g[1]) * u[1], gelu_erf(g[2]) * u[2], gelu_erf(g[3]) * u[3]);
+  }
 };
 
-// ------------------------------------------------------------ bf16 MFMA kernel
-constexpr int BK = 64;
-constexpr int LDS_STRIDE = BK + 8;  // elements; 144-byte rows keep 16-byte alignment
+// waitcnt immediate for "at most n vector-memory operations outstanding" (gfx9 encoding)
+constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
 
-template <int BM, int BN>
-__global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmProblem p, Epi<bf16> epi) {
-  constexpr int CA = BM / 32, CW = BN / 32;      // 16-byte chunks per thread per stage
-  constexpr int TM = BM / 32, TN = BN / 32;      // 16x16 subtiles per wave
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * LDS_STRIDE];
-  __shared__ __attribute__((aligned(16))) bf16 sW[2][BN * LDS_STRIDE];
+typedef __attribute__((address_space(3))) void* lds_ptr;
+typedef const __attribute__((address_space(1))) void* gbl_ptr;
+
+// Block index -> (m tile, n tile), keeping consecutive tiles on one XCD.
+__device__ __forceinline__ void tile_of(int tiles_m, int tiles, int& tm, int& tn) {
+  const int b = blockIdx.x;
+  const int per = (tiles + 7) / 8;  // tiles per XCD
+  const int x = b % 8, i = b / 8;
+  int t = x * per + i;
+  if (per * 8 != tiles) t = b;  // uneven split: keep the plain order
+  tm = t % tiles_m;
+  tn = t / tiles_m;
+}
+
+// ------------------------------------------------------------ bf16 MFMA kernel
+template <int BM, int BN, int STAGES, int WGM, int WGN, int MINB, EpiKind KIND>
+__global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmProblem p, EpiParams ep) {
+  using E = Epi<KIND, bf16>;
+  constexpr int NW = WGM * WGN;                 // waves per block
+  constexpr int ROW = 128;                      // bytes per LDS row (64 bf16)
+  constexpr int STAGE_BYTES = (BM + BN) * ROW;
+  constexpr int LA = BM / 8 / NW, LW = BN / 8 / NW;  // load instructions per wave per stage
+  static_assert(LA * 8 * NW == BM && LW * 8 * NW == BN, "tile rows must split evenly over waves");
+  constexpr int LPS = LA + LW;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN; // wave tile
+  constexpr int TM = WTM / 16, TN = WTN / 16;   // 16x16 subtiles per wave
+  static_assert(WTN % 32 == 0, "GLU pairs need 32-row weight blocks per wave");
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
-  const int tiles_m = (p.M + BM - 1) / BM;
-  const int m0 = (blockIdx.x % tiles_m) * BM;
-  const int n0 = (blockIdx.x / tiles_m) * BN;
+  const int wm = wave % WGM, wn = wave / WGM;
+  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
+  int tmi, tni;
+  tile_of(tiles_m, tiles_m * tiles_n, tmi, tni);
+  const int m0 = tmi * BM, n0 = tni * BN;
+  if (p.M_dev) {  // rows present this call; the grid was sized for p.M
+    p.M = min(*p.M_dev, p.M);
+    if (m0 >= p.M) return;
+  }
 
   const bf16* A1 = static_cast<const bf16*>(p.A1);
   const bf16* A2 = static_cast<const bf16*>(p.A2);
   const bf16* W = static_cast<const bf16*>(p.W);
 
-  uint4 ra[CA], rw[CW];
-  auto gload = [&](int kt) {
-    const int k0 = kt * BK;
+  // this lane's source row inside an 8-row group and its swizzled chunk
+  const int lrow = lane >> 3, lchunk = (lane & 7) ^ (lane >> 3);
+
+  auto issue = [&](int kt, int buf) {
+    const int k0 = kt * 64;
     const bf16* Ab = A1;
     int lda = p.lda1, kk = k0;
     if (k0 >= p.K1) { Ab = A2; lda = p.lda2; kk = k0 - p.K1; }
+    char* sb = smem + buf * STAGE_BYTES;
 #pragma unroll
-    for (int i = 0; i < CA; ++i) {
-      const int c = tid + 256 * i, r = c >> 3, ch = c & 7;
-      const int gr = min(m0 + r, p.M - 1);
-      ra[i] = *reinterpret_cast<const uint4*>(Ab + (size_t)gr * lda + kk + ch * 8);
+    for (int j = 0; j < LA; ++j) {
+      const int g = wave + NW * j;              // 8-row group
+      const int r = min(m0 + g * 8 + lrow, p.M - 1);
+      const bf16* src = Ab + (size_t)r * lda + kk + lchunk * 8;
+      __builtin_amdgcn_global_load_lds((gbl_ptr)src, (lds_ptr)(sb + g * 1024), 16, 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < CW; ++i) {
-      const int c = tid + 256 * i, r = c >> 3, ch = c & 7;
-      const int gn = min(n0 + r, p.N - 1);
-      rw[i] = *reinterpret_cast<const uint4*>(W + (size_t)gn * p.ldw + k0 + ch * 8);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < CA; ++i) {
-      const int c = tid + 256 * i, r = c >> 3, ch = c & 7;
-      *reinterpret_cast<uint4*>(&sA[buf][r * LDS_STRIDE + ch * 8]) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < CW; ++i) {
-      const int c = tid + 256 * i, r = c >> 3, ch = c & 7;
-      *reinterpret_cast<uint4*>(&sW[buf][r * LDS_STRIDE + ch * 8]) = rw[i];
+    for (int j = 0; j < LW; ++j) {
+      const int g = wave + NW * j;
+      const int r = min(n0 + g * 8 + lrow, p.N - 1);
+      const bf16* src = W + (size_t)r * p.ldw + k0 + lchunk * 8;
+      __builtin_amdgcn_global_load_lds((gbl_ptr)src, (lds_ptr)(sb + BM * ROW + g * 1024), 16, 0, 0);
     }
   };
 
@@ -140,62 +173,67 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmProblem p, Epi<bf
 #pragma unroll
     for (int b = 0; b < TM; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = p.K / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
+  const int nk = p.K / 64;
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 32) {
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s, s);
+
+  const int fr = lane & 15, fq = lane >> 4, sw = lane & 7;
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + STAGES - 2 < nk)
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm((STAGES - 2) * LPS));
+    else
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __syncthreads();
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+    const char* sa = smem + (kt % STAGES) * STAGE_BYTES;
+    const char* swt = sa + BM * ROW;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int slot = ((kk * 4 + fq) ^ sw) * 16;
       bf16x8 fa[TM], fw[TN];
 #pragma unroll
-      for (int t = 0; t < TM; ++t) {
-        const int row = wm * (BM / 2) + t * 16 + (lane & 15);
-        fa[t] = *reinterpret_cast<const bf16x8*>(&sA[buf][row * LDS_STRIDE + kk + (lane >> 4) * 8]);
-      }
+      for (int t = 0; t < TM; ++t)
+        fa[t] = *reinterpret_cast<const bf16x8*>(sa + (wm * WTM + t * 16 + fr) * ROW + slot);
 #pragma unroll
-      for (int t = 0; t < TN; ++t) {
-        const int row = wn * (BN / 2) + t * 16 + (lane & 15);
-        fw[t] = *reinterpret_cast<const bf16x8*>(&sW[buf][row * LDS_STRIDE + kk + (lane >> 4) * 8]);
-      }
+      for (int t = 0; t < TN; ++t)
+        fw[t] = *reinterpret_cast<const bf16x8*>(swt + (wn * WTN + t * 16 + fr) * ROW + slot);
 #pragma unroll
       for (int a = 0; a < TN; ++a)
 #pragma unroll
         for (int b = 0; b < TM; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[a], fa[b], acc[a][b], 0, 0, 0);
     }
-    if (kt + 1 < nk) sstore(buf ^ 1);
-    __syncthreads();
   }
 
   // lane holds C[n = nb + 4*(lane>>4) + j][m = mb + (lane & 15)]
-  const int mw = m0 + wm * (BM / 2) + (lane & 15);
-  const int nw = n0 + wn * (BN / 2) + 4 * (lane >> 4);
-  if (epi.is_glu()) {
+  const int mw = m0 + wm * WTM + fr;
+  if constexpr (E::kGlu) {
 #pragma unroll
     for (int a = 0; a < TN; a += 2)
 #pragma unroll
       for (int b = 0; b < TM; ++b) {
         const int m = mw + b * 16;
-        const int ng = n0 + wn * (BN / 2) + a * 16;  // multiple of 32: gate block
-        if (m < p.M && ng < p.N) epi.glu(m, ng / 2 + 4 * (lane >> 4), acc[a][b], acc[a + 1][b]);
+        const int ng = n0 + wn * WTN + a * 16;  // multiple of 32: gate rows of a 32-row block
+        if (m < p.M && ng < p.N) E::glu(ep, m, ng / 2 + 4 * fq, acc[a][b], acc[a + 1][b]);
       }
   } else {
+    const int nw = n0 + wn * WTN + 4 * fq;
 #pragma unroll
     for (int a = 0; a < TN; ++a)
 #pragma unroll
       for (int b = 0; b < TM; ++b) {
         const int m = mw + b * 16, n = nw + a * 16;
-        if (m < p.M && n < p.N) epi(m, n, acc[a][b]);
+        if (m < p.M && n < p.N) E::apply(ep, m, n, acc[a][b]);
       }
   }
 }
 
 // ------------------------------------------------------------ fp32 VALU kernel
 // Tile 64 (rows) x 64 (features), K step 16; each thread computes 4 x 4 outputs.
-__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmProblem p, Epi<float> epi) {
+template <EpiKind KIND>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmProblem p, EpiParams ep) {
+  using E = Epi<KIND, float>;
   __shared__ float sA[16][64 + 4];
   __shared__ float sW[16][64 + 4];
   __shared__ float xch[64][64 + 4];
@@ -233,7 +271,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmProblem p, Epi<float>
     __syncthreads();
   }
   const int n = n0 + tx * 4;
-  if (epi.is_glu()) {
+  if constexpr (E::kGlu) {
     // features of the up half (offset 16 inside each 32-row block) come from thread tx + 4
     const bool up = ((tx * 4) & 31) >= 16;
     if (up)
@@ -249,41 +287,58 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmProblem p, Epi<float>
         if (m >= p.M) continue;
         const float* u = &xch[ty * 4 + i][tx * 4 + 16];
         const int f = ((n >> 5) << 4) + (n & 15);
-        epi.glu(m, f, f32x4{acc[i][0], acc[i][1], acc[i][2], acc[i][3]}, f32x4{u[0], u[1], u[2], u[3]});
+        E::glu(ep, m, f, f32x4{acc[i][0], acc[i][1], acc[i][2], acc[i][3]}, f32x4{u[0], u[1], u[2], u[3]});
       }
-    return;
-  }
-  if (n >= p.N) return;
+  } else {
+    if (n >= p.N) return;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = m0 + ty * 4 + i;
-    if (m < p.M) epi(m, n, f32x4{acc[i][0], acc[i][1], acc[i][2], acc[i][3]});
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + ty * 4 + i;
+      if (m < p.M) E::apply(ep, m, n, f32x4{acc[i][0], acc[i][1], acc[i][2], acc[i][3]});
+    }
   }
 }
 
-template <int BM, int BN>
-hipError_t launch_bf16(const GemmProblem& p, const Epi<bf16>& epi, hipStream_t s) {
+template <int BM, int BN, int ST, int WGM, int WGN, int MINB, EpiKind K>
+hipError_t launch_bf16(const GemmProblem& p, const EpiParams& e, hipStream_t s) {
   const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN>), dim3(tiles), dim3(256), 0, s, p, epi);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, ST, WGM, WGN, MINB, K>), dim3(tiles), dim3(64 * WGM * WGN), 0,
+                     s, p, e);
   return hipGetLastError();
+}
+
+template <EpiKind K>
+hipError_t dispatch(DType dt, const GemmProblem& p, const EpiParams& e, hipStream_t s) {
+  if (dt == F32) {
+    const int tiles = ((p.M + 63) / 64) * ((p.N + 63) / 64);
+    hipLaunchKernelGGL(gemm_f32_kernel<K>, dim3(tiles), dim3(256), 0, s, p, e);
+    return hipGetLastError();
+  }
+  // tile choice by how many blocks each shape yields (256 CUs): large GEMMs take
+  // 256 x 256 tiles on 8 waves, mid-size 128 x 128 at two blocks per CU, and the
+  // narrow (N = d_model) projections 64 x 64 at three blocks per CU
+  const long t256 = (long)((p.M + 255) / 256) * ((p.N + 255) / 256);
+  const long t128 = (long)((p.M + 127) / 128) * ((p.N + 127) / 128);
+  if (t256 >= 256) return launch_bf16<256, 256, 2, 2, 4, 1, K>(p, e, s);
+  if (t128 >= 256) return launch_bf16<128, 128, 2, 2, 2, 2, K>(p, e, s);
+  return launch_bf16<64, 64, 2, 2, 2, 3, K>(p, e, s);
 }
 
 }  // namespace
 
 hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
-  if (dt == F32) {
-    Epi<float> epi{kind, e};
-    const int tiles = ((p.M + 63) / 64) * ((p.N + 63) / 64);
-    hipLaunchKernelGGL(gemm_f32_kernel, dim3(tiles), dim3(256), 0, s, p, epi);
-    return hipGetLastError();
+  switch (kind) {
+    case EPI_STORE: return dispatch<EPI_STORE>(dt, p, e, s);
+    case EPI_STORE_F32: return dispatch<EPI_STORE_F32>(dt, p, e, s);
+    case EPI_RESID: return dispatch<EPI_RESID>(dt, p, e, s);
+    case EPI_GELU: return dispatch<EPI_GELU>(dt, p, e, s);
+    case EPI_GLU_SILU: return dispatch<EPI_GLU_SILU>(dt, p, e, s);
+    case EPI_GLU_GELU: return dispatch<EPI_GLU_GELU>(dt, p, e, s);
+    case EPI_FUSION1: return dispatch<EPI_FUSION1>(dt, p, e, s);
+    case EPI_FUSION2: return dispatch<EPI_FUSION2>(dt, p, e, s);
   }
-  Epi<bf16> epi{kind, e};
-  const long t128 = (long)((p.M + 127) / 128) * ((p.N + 127) / 128);
-  const long t64 = (long)((p.M + 63) / 64) * ((p.N + 127) / 128);
-  if (t128 >= 512) return launch_bf16<128, 128>(p, epi, s);
-  if (t64 >= 512) return launch_bf16<64, 128>(p, epi, s);
-  return launch_bf16<64, 64>(p, epi, s);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace tadm

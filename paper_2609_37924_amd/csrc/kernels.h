@@ -16,6 +16,7 @@ struct GemmProblem {
   const void* A1; int lda1; int K1;
   const void* A2; int lda2;
   const void* W;  int ldw;
+  const int* M_dev = nullptr;  // if set: rows actually present (<= M; M sizes the grid)
 };
 
 enum EpiKind {
@@ -51,6 +52,11 @@ hipError_t embed_gather(DType dt, const int32_t* tok, int n_tok, const void* emb
 // (a gather of the canvas columns); pass rows_per_b = n_rows, in_stride_b = 0, in_off = 0 for identity.
 hipError_t rms_norm(DType dt, const float* x, const float* g, float eps, int n_rows, int d,
                     int rows_per_b, int in_stride_b, int in_off, void* y, hipStream_t s);
+// Gathered RMSNorm: output row r < *count is input token row
+// (c / Lc) * L + off + c % Lc with c = canvas_idx[r]; rows >= *count are skipped.
+hipError_t rms_norm_gather(DType dt, const float* x, const float* g, float eps, const int32_t* canvas_idx,
+                           const int* count, int max_rows, int Lc, int L, int off, int d, void* y,
+                           hipStream_t s);
 // LayerNorm with affine; output as T (y_t) or float (y_f), whichever is non-null.
 hipError_t layer_norm(DType dt, const float* x, const float* w, const float* b, float eps,
                       int n_rows, int d, void* y_t, float* y_f, hipStream_t s);
@@ -71,10 +77,15 @@ hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, voi
                      int Hkv, int Lq, int Lk, int kv_cap, int dh, hipStream_t s);
 
 // ---- sampler (sampler.hip)
+// List of masked canvas positions: idx[r] = b * Lc + j for the r-th masked entry
+// (row-major order), row_map[b * Lc + j] = r or -1, *count = number of entries.
+hipError_t compact_masked(const int32_t* canvas, int B, int L, int canvas_off, int mask_id,
+                          int32_t* idx, int32_t* row_map, int* count, hipStream_t s);
 // For every masked canvas position: Gumbel-max token and fixed-point confidence.
-hipError_t sample_tokens(const float* logits, const int32_t* canvas, int B, int L, int canvas_off,
-                         int V, int mask_id, int pos0, uint32_t step_id, uint64_t seed,
-                         float inv_temp, int32_t* choice, float* conf, hipStream_t s);
+// Logits row of position (b, j) is row_map[b * Lc + j] if row_map is set, else b * Lc + j.
+hipError_t sample_tokens(const float* logits, const int32_t* row_map, const int32_t* canvas, int B,
+                         int L, int canvas_off, int V, int mask_id, int pos0, uint32_t step_id,
+                         uint64_t seed, float inv_temp, int32_t* choice, float* conf, hipStream_t s);
 // Per row: reveal the n_unmask most confident masked positions; copy the rest.
 hipError_t select_unmask(const int32_t* canvas, const int32_t* choice, const float* conf, int B,
                          int L, int canvas_off, int mask_id, int n_unmask, int32_t* next,

@@ -55,6 +55,29 @@ __global__ __launch_bounds__(256) void rms_kernel(const float* x, const float* g
 }
 
 template <class T>
+__global__ __launch_bounds__(256) void rms_gather_kernel(const float* x, const float* g, float eps,
+                                                         const int32_t* cidx, const int* count,
+                                                         int Lc, int L, int off, int d, T* y) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= *count) return;
+  const int c = cidx[r];
+  const float* xr = x + ((size_t)(c / Lc) * L + off + c % Lc) * d;
+  float ss = 0.f;
+  for (int k = lane * 4; k < d; k += 256) {
+    const float4 v = *reinterpret_cast<const float4*>(xr + k);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = wave_sum(ss);
+  const float rs = rsqrtf(ss / d + eps);
+  T* yr = y + (size_t)r * d;
+  for (int k = lane * 4; k < d; k += 256) {
+    const float4 v = *reinterpret_cast<const float4*>(xr + k);
+    const float4 w = *reinterpret_cast<const float4*>(g + k);
+    store4(yr + k, v.x * rs * w.x, v.y * rs * w.y, v.z * rs * w.z, v.w * rs * w.w);
+  }
+}
+
+template <class T>
 __global__ __launch_bounds__(256) void ln_kernel(const float* x, const float* w, const float* b,
                                                  float eps, int n_rows, int d, T* y_t, float* y_f) {
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -130,6 +153,19 @@ hipError_t rms_norm(DType dt, const float* x, const float* g, float eps, int n_r
   else
     hipLaunchKernelGGL(rms_kernel<float>, dim3(blocks(n_rows, 4)), dim3(256), 0, s, x, g, eps, n_rows,
                        d, rows_per_b, in_stride_b, in_off, static_cast<float*>(y));
+  return hipGetLastError();
+}
+
+hipError_t rms_norm_gather(DType dt, const float* x, const float* g, float eps, const int32_t* cidx,
+                           const int* count, int max_rows, int Lc, int L, int off, int d, void* y,
+                           hipStream_t s) {
+  if (max_rows == 0) return hipSuccess;
+  if (dt == BF16)
+    hipLaunchKernelGGL(rms_gather_kernel<bf16>, dim3(blocks(max_rows, 4)), dim3(256), 0, s, x, g, eps, cidx,
+                       count, Lc, L, off, d, static_cast<bf16*>(y));
+  else
+    hipLaunchKernelGGL(rms_gather_kernel<float>, dim3(blocks(max_rows, 4)), dim3(256), 0, s, x, g, eps, cidx,
+                       count, Lc, L, off, d, static_cast<float*>(y));
   return hipGetLastError();
 }
 

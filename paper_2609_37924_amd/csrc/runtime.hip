@@ -6,6 +6,7 @@
 // generation is enqueued without any device-to-host synchronisation.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -191,6 +192,8 @@ struct Workspace {
        *ffn = nullptr, *fus_h = nullptr;
   float* ffn_pre = nullptr;  // fp32 GLU pre-activations
   int32_t* choice = nullptr;
+  int32_t *cidx = nullptr, *row_map = nullptr;  // masked-position list and its inverse
+  int* count = nullptr;                         // number of masked positions (device)
   float* logits = nullptr;
   size_t logits_cap = 0;
   int kv_cap = 0;
@@ -214,6 +217,7 @@ struct tadm_model {
   float *rope_cos = nullptr, *rope_sin = nullptr;
   Workspace ws;
   bool taps = false;
+  bool tap_final = false;  // TADM_TAP_FINAL holds every canvas row (full-logits step)
   // objects reused across calls so that a generation allocates nothing after warm-up
   tadm_cache* scratch = nullptr;   // anchor state of context appends (capacity max_batch x max_seq)
   tadm_cache* gcache = nullptr;    // anchor cache of tadm_generate
@@ -307,6 +311,9 @@ static tadm_status ensure_workspace(tadm_model* m) {
     TRY(ws_alloc(m, (void**)&w.fus_g, N * d * 4));
   }
   TRY(ws_alloc(m, (void**)&w.choice, N * 4));
+  TRY(ws_alloc(m, (void**)&w.cidx, N * 4));
+  TRY(ws_alloc(m, (void**)&w.row_map, N * 4));
+  TRY(ws_alloc(m, (void**)&w.count, 256));
   TRY(ws_alloc(m, (void**)&w.conf, N * 4));
   w.n_tok = (int)N;
   w.n_canvas = (int)N;
@@ -778,12 +785,12 @@ tadm_status tadm_anchor_forward(tadm_model* m, const tadm_context* ctx, const in
   return anchor_impl(m, ctx, canvas_dev, B, L, i, cache);
 }
 
-static tadm_status sample_impl(tadm_model* m, const float* logits, const int32_t* canvas, int B, int L,
-                               int off, int pos0, const tadm_step_args* a, int32_t* next,
-                               int32_t* choice, float* conf) {
+static tadm_status sample_impl(tadm_model* m, const float* logits, const int32_t* row_map,
+                               const int32_t* canvas, int B, int L, int off, int pos0,
+                               const tadm_step_args* a, int32_t* next, int32_t* choice, float* conf) {
   const int mask = m->cfg.vocab;
   TRY(prof_begin(m, TADM_STAGE_SAMPLE));
-  HIPCHK(sample_tokens(logits, canvas, B, L, off, m->cfg.vocab, mask, pos0, a->step_id, a->seed,
+  HIPCHK(sample_tokens(logits, row_map, canvas, B, L, off, m->cfg.vocab, mask, pos0, a->step_id, a->seed,
                        a->inv_temp, choice, conf, m->stream));
   TRY(prof_end(m));
   TRY(prof_begin(m, TADM_STAGE_SELECT));
@@ -792,9 +799,12 @@ static tadm_status sample_impl(tadm_model* m, const float* logits, const int32_t
   return TADM_OK;
 }
 
+// One reverse step.  With caller logits every canvas row goes through the head;
+// otherwise only the masked positions do (carry-over makes the others' logits
+// unused), at most max_masked of them (an exact bound the caller guarantees, or B*Lc).
 static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const int32_t* canvas, int B,
                                 int L, int off, const tadm_cache* cache, const tadm_step_args* a,
-                                float* logits, int32_t* next) {
+                                float* logits, int32_t* next, int max_masked) {
   const tadm_config& cf = m->cfg;
   Workspace& s = m->ws;
   const int pos0 = ctx ? ctx->len : 0, Lc = L - off, d = cf.d_model;
@@ -805,17 +815,26 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
   TRY(fusion(m, B, L, s.c, cache));
   TRY(prof_end(m));
   if (m->taps) HIPCHK(copy_f32(s.x, s.ht, (size_t)B * L * d, m->stream));
+  const bool full = logits != nullptr;
+  const int rows = full ? B * Lc : std::min(max_masked, B * Lc);
   TRY(prof_begin(m, TADM_STAGE_DENOISE));
   TRY(run_part(m, cf.n_shared + cf.n_anchor, cf.n_denoise, s.x, B, L, pos0, ctx));
-  HIPCHK(rms_norm(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, B * Lc, d, Lc, L, off, s.xn, m->stream));
+  if (full) {
+    HIPCHK(rms_norm(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, B * Lc, d, Lc, L, off, s.xn, m->stream));
+  } else {
+    HIPCHK(compact_masked(canvas, B, L, off, cf.vocab, s.cidx, s.row_map, s.count, m->stream));
+    HIPCHK(rms_norm_gather(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, s.cidx, s.count, rows, Lc, L,
+                           off, d, s.xn, m->stream));
+  }
   TRY(prof_end(m));
-  if (!logits) {
+  if (!full) {
     TRY(ensure_logits(m, (size_t)B * Lc * cf.vocab));
     logits = s.logits;
   }
   TRY(prof_begin(m, TADM_STAGE_HEAD));
   {
-    GemmProblem p{B * Lc, cf.vocab, d, s.xn, d, d, nullptr, 0, m->W(m->lay.w_out), d};
+    GemmProblem p{rows, cf.vocab, d, s.xn, d, d, nullptr, 0, m->W(m->lay.w_out), d};
+    if (!full) p.M_dev = s.count;
     EpiParams e;
     e.out = logits;
     e.ldo = cf.vocab;
@@ -825,7 +844,9 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
   m->tap_B = B;
   m->tap_L = L;
   m->tap_Lc = Lc;
-  return sample_impl(m, logits, canvas, B, L, off, pos0, a, next, s.choice, s.conf);
+  m->tap_final = full;
+  return sample_impl(m, logits, full ? nullptr : s.row_map, canvas, B, L, off, pos0, a, next, s.choice,
+                     s.conf);
 }
 
 tadm_status tadm_denoise_step(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev, int32_t B,
@@ -841,7 +862,8 @@ tadm_status tadm_denoise_step(tadm_model* m, const tadm_context* ctx, const int3
   if (cache->refresh_i == 0) return fail(TADM_ERR_STATE, "cache was never refreshed");
   if (m->cfg.vocab % 4) return fail(TADM_ERR_UNSUPPORTED, "the vocabulary head needs vocab %% 4 == 0");
   TRY(ensure_workspace(m));
-  return denoise_impl(m, ctx, canvas_dev, B, L, canvas_off, cache, args, logits_dev, next_canvas_dev);
+  return denoise_impl(m, ctx, canvas_dev, B, L, canvas_off, cache, args, logits_dev, next_canvas_dev,
+                      B * (L - canvas_off));
 }
 
 tadm_status tadm_sample(tadm_model* m, const float* logits_dev, const int32_t* canvas_dev, int32_t B, int32_t L,
@@ -853,7 +875,7 @@ tadm_status tadm_sample(tadm_model* m, const float* logits_dev, const int32_t* c
     return fail(TADM_ERR_INVALID, "sample shape B=%d L=%d off=%d", B, L, canvas_off);
   TRY(check_args(args, L - canvas_off));
   TRY(ensure_workspace(m));
-  return sample_impl(m, logits_dev, canvas_dev, B, L, canvas_off, pos0, args, next_canvas_dev,
+  return sample_impl(m, logits_dev, nullptr, canvas_dev, B, L, canvas_off, pos0, args, next_canvas_dev,
                      choice_dev ? choice_dev : m->ws.choice, conf_dev ? conf_dev : m->ws.conf);
 }
 
@@ -891,7 +913,9 @@ tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, i
       a.step_id = (uint32_t)(T - i);
       a.n_unmask = tadm_unmask_count(gen_len, i, T);
       if ((T - i) % K == 0) TRY(anchor_impl(m, nullptr, tokens_dev, B, L, i, cache));
-      TRY(denoise_impl(m, nullptr, tokens_dev, B, L, P, cache, &a, nullptr, tokens_dev));
+      // every row started with gen_len masked positions and reveals n_i per step
+      const int masked = (int)(((int64_t)gen_len * i) / T);
+      TRY(denoise_impl(m, nullptr, tokens_dev, B, L, P, cache, &a, nullptr, tokens_dev, B * masked));
     }
     return TADM_OK;
   }
@@ -915,7 +939,8 @@ tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, i
       a.step_id = (uint32_t)(j * T + (T - i));
       a.n_unmask = tadm_unmask_count(block_len, i, T);
       if ((T - i) % K == 0) TRY(anchor_impl(m, ctx, win, B, block_len, i, cache));
-      TRY(denoise_impl(m, ctx, win, B, block_len, 0, cache, &a, nullptr, win));
+      const int masked = (int)(((int64_t)block_len * i) / T);
+      TRY(denoise_impl(m, ctx, win, B, block_len, 0, cache, &a, nullptr, win, B * masked));
     }
     HIPCHK(hipMemcpy2DAsync(tokens_dev + P + j * block_len, (size_t)L * 4, win, (size_t)block_len * 4,
                             (size_t)block_len * 4, B, hipMemcpyDeviceToDevice, m->stream));
@@ -944,6 +969,7 @@ tadm_status tadm_debug_read(tadm_model* m, int32_t tap, float* dst_dev, size_t b
       return TADM_OK;
     }
     case TADM_TAP_FINAL: {
+      if (!m->tap_final) return fail(TADM_ERR_STATE, "the last step computed the head for masked rows only");
       const size_t n = (size_t)m->tap_B * m->tap_Lc * d;
       if (bytes != n * 4) return fail(TADM_ERR_INVALID, "tap %d has %zu bytes", tap, n * 4);
       HIPCHK(to_f32(m->dt, m->ws.xn, dst_dev, n, m->stream));

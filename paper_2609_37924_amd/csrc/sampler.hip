@@ -98,7 +98,8 @@ __device__ __forceinline__ Best better(Best a, Best b) {
 
 // grid (Lc, B); one workgroup per canvas position; only masked positions work.
 template <bool VEC4>
-__global__ __launch_bounds__(256) void sample_kernel(const float* logits, const int32_t* canvas,
+__global__ __launch_bounds__(256) void sample_kernel(const float* logits, const int32_t* row_map,
+                                                     const int32_t* canvas,
                                                      int L, int off, int Lc, int V, int mask_id,
                                                      int pos0, uint32_t step_id, uint32_t k0,
                                                      uint32_t k1, float inv_temp, int32_t* choice,
@@ -115,7 +116,7 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
     }
     return;
   }
-  const float* lg = logits + (size_t)row * V;
+  const float* lg = logits + (size_t)(row_map ? row_map[row] : row) * V;
   const uint32_t pos = (uint32_t)(pos0 + off + j);
   const int ngroups = (V + 3) / 4;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -194,6 +195,42 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
   }
 }
 
+// One workgroup of 1024 threads scans every canvas entry in row-major order.
+__global__ __launch_bounds__(1024) void compact_kernel(const int32_t* canvas, int B, int L, int off,
+                                                       int mask_id, int32_t* idx, int32_t* row_map,
+                                                       int* count) {
+  __shared__ int wsum[16];
+  __shared__ int base;
+  const int Lc = L - off, n = B * Lc;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (threadIdx.x == 0) base = 0;
+  __syncthreads();
+  for (int c0 = 0; c0 < n; c0 += 1024) {
+    const int c = c0 + threadIdx.x;
+    const int m = c < n && canvas[(size_t)(c / Lc) * L + off + c % Lc] == mask_id;
+    // wave prefix via ballot
+    const unsigned long long bal = __ballot(m);
+    const int before = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) wsum[wave] = __popcll(bal);
+    __syncthreads();
+    int woff = 0;
+    for (int w = 0; w < wave; ++w) woff += wsum[w];
+    const int r = base + woff + before;
+    if (c < n) {
+      row_map[c] = m ? r : -1;
+      if (m) idx[r] = c;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int t = 0;
+      for (int w = 0; w < 16; ++w) t += wsum[w];
+      base += t;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *count = base;
+}
+
 // one workgroup per row; rank by (conf desc, position asc) among masked positions.
 __global__ __launch_bounds__(256) void select_kernel(const int32_t* canvas, const int32_t* choice,
                                                      const float* conf, int L, int off, int Lc,
@@ -229,18 +266,25 @@ __global__ __launch_bounds__(256) void select_kernel(const int32_t* canvas, cons
 
 }  // namespace
 
-hipError_t sample_tokens(const float* logits, const int32_t* canvas, int B, int L, int canvas_off,
-                         int V, int mask_id, int pos0, uint32_t step_id, uint64_t seed,
-                         float inv_temp, int32_t* choice, float* conf, hipStream_t s) {
+hipError_t compact_masked(const int32_t* canvas, int B, int L, int canvas_off, int mask_id,
+                          int32_t* idx, int32_t* row_map, int* count, hipStream_t s) {
+  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, s, canvas, B, L, canvas_off, mask_id, idx,
+                     row_map, count);
+  return hipGetLastError();
+}
+
+hipError_t sample_tokens(const float* logits, const int32_t* row_map, const int32_t* canvas, int B,
+                         int L, int canvas_off, int V, int mask_id, int pos0, uint32_t step_id,
+                         uint64_t seed, float inv_temp, int32_t* choice, float* conf, hipStream_t s) {
   const int Lc = L - canvas_off;
   if (B * Lc == 0) return hipSuccess;
   const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
   const dim3 grid(Lc, B);
   if (V % 4 == 0)
-    hipLaunchKernelGGL(sample_kernel<true>, grid, dim3(256), 0, s, logits, canvas, L, canvas_off, Lc, V,
+    hipLaunchKernelGGL(sample_kernel<true>, grid, dim3(256), 0, s, logits, row_map, canvas, L, canvas_off, Lc, V,
                        mask_id, pos0, step_id, k0, k1, inv_temp, choice, conf);
   else
-    hipLaunchKernelGGL(sample_kernel<false>, grid, dim3(256), 0, s, logits, canvas, L, canvas_off, Lc,
+    hipLaunchKernelGGL(sample_kernel<false>, grid, dim3(256), 0, s, logits, row_map, canvas, L, canvas_off, Lc,
                        V, mask_id, pos0, step_id, k0, k1, inv_temp, choice, conf);
   return hipGetLastError();
 }

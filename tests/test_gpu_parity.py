@@ -251,6 +251,32 @@ def test_cache_unchanged_between_refreshes_and_split_equals_generate():
         tadm.tadm_model_destroy(m)
 
 
+def test_masked_only_head_equals_full_head():
+    """Without caller logits the head runs on the masked positions only; the reverse
+    step must be bit-identical to the one computed from the full logits."""
+    cfg = synth.get_config("small", n_anchor=1, n_denoise=1, prompt_len=40, gen_len=50)
+    B, P, G = 3, 40, 50
+    L = P + G
+    tensors = synth.make_weights(cfg, perturb=True)
+    m = gpu_model(cfg, tensors, B, L)
+    try:
+        cache = tadm.tadm_cache_create(m, B, L)
+        z0 = synth.make_teacher_canvas(cfg, G, batch=B, seed=3).to(dev())
+        tadm.tadm_anchor_forward(m, None, z0, B, L, 8, 8, cache)
+        for n_masked, seed in ((37, 4), (1, 5), (0, 6)):
+            z = synth.make_teacher_canvas(cfg, n_masked, batch=B, seed=seed).to(dev())
+            args = tadm.step_args(7, 8, 3, 1, 9, 1.0)
+            full, part = torch.empty_like(z), torch.empty_like(z)
+            logits = torch.empty(B, G, cfg["vocab"], device=dev())
+            tadm.tadm_denoise_step(m, None, z, B, L, P, cache, args, logits, full)
+            tadm.tadm_denoise_step(m, None, z, B, L, P, cache, args, None, part)
+            sync()
+            assert torch.equal(full, part), n_masked
+        tadm.tadm_cache_destroy(cache)
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
 def test_state_errors():
     cfg = synth.get_config("tiny")
     tensors = synth.make_weights(cfg)
