@@ -34,7 +34,8 @@ __global__ __launch_bounds__(256) void rope_split_kernel(const T* qkv, int B, in
       const T* src = qkv + ((size_t)b * L + l) * width + slot * dh;
       const float x1 = f32_of(src[j]), x2 = f32_of(src[j + half]);
       const int pos = pos0 + l;
-      const float c = cos_t[(size_t)pos * half + j], s = sin_t[(size_t)pos * half + j];
+      const float c = cos_t ? cos_t[(size_t)pos * half + j] : 1.f;
+      const float s = sin_t ? sin_t[(size_t)pos * half + j] : 0.f;
       T* dst = isq ? Q + (((size_t)b * H + hh) * L + l) * dh
                    : K + (((size_t)b * Hkv + hh) * kv_cap + kv_off + l) * dh;
       dst[j] = from_f32<T>(x1 * c - x2 * s);

@@ -13,7 +13,7 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
-SOURCES = ["runtime.hip", "gemm.hip", "attention.hip", "norm.hip", "sampler.hip"]
+SOURCES = ["runtime.hip", "gemm.hip", "attention.hip", "norm.hip", "sampler.hip", "fusion.hip"]
 EXTRA = {"sampler.hip": ["-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt"]}
 OUT = os.path.join(PKG, "libtadm.so")
 

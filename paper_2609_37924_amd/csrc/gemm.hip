@@ -79,6 +79,53 @@ struct Epi<EPI_FUSION2, T> {
   }
 };
 template <class T>
+struct Epi<EPI_SILU, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + n, siluf_(v[0]), siluf_(v[1]), siluf_(v[2]),
+           siluf_(v[3]));
+  }
+};
+template <class T>
+struct Epi<EPI_ADD_F32, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    const float4 a = *reinterpret_cast<const float4*>(e.aux + (size_t)m * e.ld_aux + n);
+    store4(static_cast<float*>(e.out) + (size_t)m * e.ldo + n, a.x + v[0], a.y + v[1], a.z + v[2],
+           a.w + v[3]);
+  }
+};
+template <class T>
+struct Epi<EPI_ADD_BOTH, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    const float4 a = *reinterpret_cast<const float4*>(e.aux + (size_t)m * e.ld_aux + n);
+    const float r0 = a.x + v[0], r1 = a.y + v[1], r2 = a.z + v[2], r3 = a.w + v[3];
+    store4(static_cast<float*>(e.out) + (size_t)m * e.ldo + n, r0, r1, r2, r3);
+    store4(static_cast<T*>(e.out_t) + (size_t)m * e.ld_out_t + n, r0, r1, r2, r3);
+  }
+};
+template <class T>
+struct Epi<EPI_ADD_SUB, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    const float4 a = *reinterpret_cast<const float4*>(e.aux + (size_t)m * e.ld_aux + n);
+    const float4 b = *reinterpret_cast<const float4*>(e.aux2 + (size_t)m * e.ld_aux2 + n);
+    store4(static_cast<T*>(e.out_t) + (size_t)m * e.ld_out_t + n, (a.x + v[0]) - b.x, (a.y + v[1]) - b.y,
+           (a.z + v[2]) - b.z, (a.w + v[3]) - b.w);
+  }
+};
+template <class T>
+struct Epi<EPI_PAIRED, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    const float4 h = *reinterpret_cast<const float4*>(e.aux + (size_t)m * e.ld_aux + n);
+    const float f = e.row1[m] * e.row2[m];
+    store4(static_cast<float*>(e.out) + (size_t)m * e.ldo + n, h.x + f * v[0], h.y + f * v[1],
+           h.z + f * v[2], h.w + f * v[3]);
+  }
+};
+template <class T>
 struct Epi<EPI_GLU_SILU, T> {
   static constexpr bool kGlu = true;
   __device__ static void glu(const EpiParams& e, int m, int f, f32x4 g, f32x4 u) {
@@ -337,6 +384,11 @@ hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e
     case EPI_GLU_GELU: return dispatch<EPI_GLU_GELU>(dt, p, e, s);
     case EPI_FUSION1: return dispatch<EPI_FUSION1>(dt, p, e, s);
     case EPI_FUSION2: return dispatch<EPI_FUSION2>(dt, p, e, s);
+    case EPI_SILU: return dispatch<EPI_SILU>(dt, p, e, s);
+    case EPI_ADD_F32: return dispatch<EPI_ADD_F32>(dt, p, e, s);
+    case EPI_ADD_BOTH: return dispatch<EPI_ADD_BOTH>(dt, p, e, s);
+    case EPI_ADD_SUB: return dispatch<EPI_ADD_SUB>(dt, p, e, s);
+    case EPI_PAIRED: return dispatch<EPI_PAIRED>(dt, p, e, s);
   }
   return hipErrorInvalidValue;
 }

@@ -28,6 +28,11 @@ enum EpiKind {
   EPI_GLU_GELU,       // out(T)[m, f] = gelu(gate) * up
   EPI_FUSION1,        // n < split: out(T)[m, n] = gelu(acc + bias[n]);  else out2(float)[m, n-split] = sigmoid(acc + bias[n])
   EPI_FUSION2,        // resid(float)[m, n] = aux[m, n] + gate[m, n] * (acc + bias[n])
+  EPI_SILU,           // out(T)[m, n] = silu(acc)
+  EPI_ADD_F32,        // out(float)[m, n] = aux[m, n] + acc
+  EPI_ADD_BOTH,       // out(float)[m, n] = aux[m, n] + acc and out_t(T)[m, n] = the same value
+  EPI_ADD_SUB,        // out_t(T)[m, n] = (aux[m, n] + acc) - aux2[m, n]
+  EPI_PAIRED,         // out(float)[m, n] = aux[m, n] + row1[m] * row2[m] * acc
 };
 
 struct EpiParams {
@@ -38,6 +43,10 @@ struct EpiParams {
   const float* gate = nullptr; int ldg = 0;
   float* out2 = nullptr; int ldo2 = 0;
   int split = 0;
+  const float* aux2 = nullptr; int ld_aux2 = 0;
+  const float* row1 = nullptr;   // per-row factors
+  const float* row2 = nullptr;
+  void* out_t = nullptr; int ld_out_t = 0;
 };
 
 hipError_t gemm(DType dt, const GemmProblem& p, EpiKind epi, const EpiParams& e, hipStream_t s);
@@ -65,10 +74,25 @@ hipError_t to_f32(DType dt, const void* src, float* dst, size_t n, hipStream_t s
 // out[r, f] = act(pre[r, gate_row(f)]) * pre[r, up_row(f)] for the fp32 GLU path.
 hipError_t glu_f32(const float* pre, int n_rows, int F, int silu, float* out, hipStream_t s);
 
+// ---- paired-attention fusion helpers (fusion.hip)
+// s[r] = sqrt(mean_j x[r, j]^2 + eps)
+hipError_t row_rms(const float* x, int n_rows, int d, float eps, float* s, hipStream_t st);
+// y(T)[r, :] = x[r, :] / s[r]
+hipError_t scale_rows(DType dt, const float* x, const float* s, int n_rows, int d, void* y, hipStream_t st);
+// y(T) = x (float -> model type), n elements
+hipError_t to_type(DType dt, const float* x, size_t n, void* y, hipStream_t st);
+// F(T) [N, 4r] = [U; Z0; Z - Z0; M] (feature concatenation); U, Z0, Z float, M in T
+hipError_t paired_features(DType dt, const float* U, const float* Z0, const float* Z, const void* M, int n_rows,
+                           int r, void* F, hipStream_t st);
+// g[r] = sigmoid(sum_j G1(T)[r, j] * w[j] + b)
+hipError_t row_gate(DType dt, const void* G1, const float* w, const float* b, int n_rows, int r, float* g,
+                    hipStream_t st);
+
 // ---- rotary + head split (attention.hip)
 // qkv(T) [B*L, (H + 2*Hkv)*dh] -> Q(T) [B, H, L, dh] (rotated), K(T) rows
 // [b, hk, off + l, :] of a [B, Hkv, kv_cap, dh] buffer (rotated), Vt(T) [b, hk, :, off + l]
-// of a [B, Hkv, dh, kv_cap] buffer.  Positions pos0 + l; cos/sin tables [max_pos, dh/2].
+// of a [B, Hkv, dh, kv_cap] buffer.  Positions pos0 + l; cos/sin tables [max_pos, dh/2];
+// with null tables the heads are split without rotation.
 hipError_t rope_split(DType dt, const void* qkv, int B, int L, int H, int Hkv, int dh, int pos0,
                       const float* cos_t, const float* sin_t, void* Q, void* K, void* Vt,
                       int kv_cap, int kv_off, hipStream_t s);

@@ -79,6 +79,7 @@ struct Layout {
   std::vector<Tensor> tensors;
   int embed, final_norm, w_out;
   int ln_s_w, ln_s_b, ln_a_w, ln_a_b, w1g, b1g, w2, b2, ln_o_w, ln_o_b;  // gated MLP
+  int p_wc, p_wh, p_wqkv, p_wo, p_w1, p_w2, p_wg1, p_wg2, p_bg, p_wup;   // paired attention
   std::vector<LayerIdx> layers;
   size_t bytes;
 };
@@ -126,6 +127,30 @@ Layout make_layout(const tadm_config& c) {
     add_spec(L, "fusion.b2", d, 0, L.b2, P_VEC);
     add_spec(L, "fusion.ln_o_w", d, 0, L.ln_o_w, P_VEC);
     add_spec(L, "fusion.ln_o_b", d, 0, L.ln_o_b, P_VEC);
+  } else {
+    const long r = c.fusion_rank;
+    L.p_wc = add_tensor(L, r, d, false);
+    L.p_wh = add_tensor(L, r, d, false);
+    L.p_wqkv = add_tensor(L, 3 * r, 2 * r, false);  // rows W_Q, W_K, W_V
+    L.p_wo = add_tensor(L, r, r, false);
+    L.p_w1 = add_tensor(L, 2 * r, r, false);
+    L.p_w2 = add_tensor(L, r, 2 * r, false);
+    L.p_wg1 = add_tensor(L, r, 4 * r, false);
+    L.p_wg2 = add_tensor(L, 1, r, true);
+    L.p_bg = add_tensor(L, 1, 1, true);
+    L.p_wup = add_tensor(L, d, r, false);
+    add_spec(L, "fusion.w_c", r, d, L.p_wc, P_COPY);
+    add_spec(L, "fusion.w_h", r, d, L.p_wh, P_COPY);
+    add_spec(L, "fusion.w_q", r, 2 * r, L.p_wqkv, P_ROWS, 0);
+    add_spec(L, "fusion.w_k", r, 2 * r, L.p_wqkv, P_ROWS, r);
+    add_spec(L, "fusion.w_v", r, 2 * r, L.p_wqkv, P_ROWS, 2 * r);
+    add_spec(L, "fusion.w_o", r, r, L.p_wo, P_COPY);
+    add_spec(L, "fusion.w_f1", 2 * r, r, L.p_w1, P_COPY);
+    add_spec(L, "fusion.w_f2", r, 2 * r, L.p_w2, P_COPY);
+    add_spec(L, "fusion.w_g1", r, 4 * r, L.p_wg1, P_COPY);
+    add_spec(L, "fusion.w_g2", 1, r, L.p_wg2, P_COPY);
+    add_spec(L, "fusion.b_g", 1, 0, L.p_bg, P_VEC);
+    add_spec(L, "fusion.w_up", d, r, L.p_wup, P_COPY);
   }
   const int nl = c.n_shared + c.n_anchor + c.n_denoise;
   const bool glu = c.ffn_kind != TADM_FFN_GELU;
@@ -176,6 +201,13 @@ bool valid_config(const tadm_config* c, std::string& why) {
   if (c->head_dim % 2) { why = "odd head_dim"; return false; }
   if (c->ffn_kind < 0 || c->ffn_kind > 2) { why = "ffn_kind"; return false; }
   if (c->fusion_kind < 0 || c->fusion_kind > 1) { why = "fusion_kind"; return false; }
+  if (c->fusion_kind == TADM_FUSION_PAIRED &&
+      (c->fusion_rank < 4 || c->paired_heads < 1 || c->fusion_rank % (4 * c->paired_heads) ||
+       c->fusion_rank > c->n_kv_heads * c->head_dim || c->fusion_rank > c->n_heads * c->head_dim ||
+       2 * c->fusion_rank > c->d_ffn)) {
+    why = "paired fusion needs rank a multiple of 4*heads and at most the KV width";
+    return false;
+  }
   if (c->d_ffn % 16) { why = "d_ffn must be a multiple of 16"; return false; }
   if (c->d_model % 4 || (c->n_heads * c->head_dim) % 4) { why = "widths must be multiples of 4"; return false; }
   if (!(c->rms_eps > 0) || !(c->ln_eps > 0) || !(c->rope_theta > 0)) { why = "eps/theta"; return false; }
@@ -191,6 +223,9 @@ struct Workspace {
   void *xn = nullptr, *qkv = nullptr, *q = nullptr, *k = nullptr, *vt = nullptr, *ao = nullptr,
        *ffn = nullptr, *fus_h = nullptr;
   float* ffn_pre = nullptr;  // fp32 GLU pre-activations
+  // paired-attention fusion
+  float *pz = nullptr, *pr = nullptr, *pgate = nullptr;
+  void *pzb = nullptr, *pqkv = nullptr, *prb = nullptr, *pmb = nullptr, *pf = nullptr, *pg1 = nullptr;
   int32_t* choice = nullptr;
   int32_t *cidx = nullptr, *row_map = nullptr;  // masked-position list and its inverse
   int* count = nullptr;                         // number of masked positions (device)
@@ -241,6 +276,9 @@ struct tadm_cache {
   int B, L;
   float *h = nullptr, *c = nullptr;
   void* a = nullptr;
+  // paired attention: token scales, anchor-side projections and phi(Z0, U)
+  float *sC = nullptr, *sH = nullptr, *Z0 = nullptr, *U = nullptr, *phi0 = nullptr;
+  void* Ub = nullptr;
   int refresh_i = 0;
 };
 
@@ -309,6 +347,17 @@ static tadm_status ensure_workspace(tadm_model* m) {
   if (c.fusion_kind == TADM_FUSION_GATED_MLP) {
     TRY(ws_alloc(m, &w.fus_h, N * 4 * d * es));
     TRY(ws_alloc(m, (void**)&w.fus_g, N * d * 4));
+  } else {
+    const size_t r = c.fusion_rank;
+    TRY(ws_alloc(m, (void**)&w.pz, N * r * 4));
+    TRY(ws_alloc(m, (void**)&w.pr, N * r * 4));
+    TRY(ws_alloc(m, (void**)&w.pgate, N * 4));
+    TRY(ws_alloc(m, &w.pzb, N * r * es));
+    TRY(ws_alloc(m, &w.pqkv, N * 3 * r * es));
+    TRY(ws_alloc(m, &w.prb, N * r * es));
+    TRY(ws_alloc(m, &w.pmb, N * r * es));
+    TRY(ws_alloc(m, &w.pf, N * 4 * r * es));
+    TRY(ws_alloc(m, &w.pg1, N * r * es));
   }
   TRY(ws_alloc(m, (void**)&w.choice, N * 4));
   TRY(ws_alloc(m, (void**)&w.cidx, N * 4));
@@ -412,6 +461,134 @@ static tadm_status shared_net(tadm_model* m, const tadm_context* ctx, const int3
   return run_part(m, 0, m->cfg.n_shared, c, B, L, pos0, ctx);
 }
 
+// ---------------------------------------------------- paired-attention fusion
+// phi(Z, U) = R + SiLU(R W_1) W_2 with R = Z + MHA(J W_Q, J W_K, J W_V) W_O, J = [Z, U],
+// the attention bidirectional over the L positions of each row (App. C.1).  With
+// phi0 == nullptr the result goes to cache->phi0 (refresh); otherwise M = phi - phi0 is
+// written to ws.pmb in the model type.
+static tadm_status paired_mixer(tadm_model* m, int B, int L, const float* Zf, const void* Zb,
+                                tadm_cache* cache, bool to_phi0) {
+  const tadm_config& cf = m->cfg;
+  Workspace& s = m->ws;
+  const Layout& Y = m->lay;
+  const int N = B * L, r = cf.fusion_rank, nh = cf.paired_heads, dh = r / nh;
+  const hipStream_t st = m->stream;
+  {
+    GemmProblem p{N, 3 * r, 2 * r, Zb, r, r, cache->Ub, r, m->W(Y.p_wqkv), 2 * r};
+    EpiParams e;
+    e.out = s.pqkv;
+    e.ldo = 3 * r;
+    HIPCHK(gemm(m->dt, p, EPI_STORE, e, st));
+  }
+  HIPCHK(rope_split(m->dt, s.pqkv, B, L, nh, nh, dh, 0, nullptr, nullptr, s.q, s.k, s.vt, s.kv_cap, 0, st));
+  HIPCHK(attention(m->dt, s.q, s.k, s.vt, s.ao, B, nh, nh, L, L, s.kv_cap, dh, st));
+  {
+    GemmProblem p{N, r, r, s.ao, r, r, nullptr, 0, m->W(Y.p_wo), r};
+    EpiParams e;
+    e.out = s.pr;
+    e.ldo = r;
+    e.aux = Zf;
+    e.ld_aux = r;
+    e.out_t = s.prb;
+    e.ld_out_t = r;
+    HIPCHK(gemm(m->dt, p, EPI_ADD_BOTH, e, st));
+  }
+  {
+    GemmProblem p{N, 2 * r, r, s.prb, r, r, nullptr, 0, m->W(Y.p_w1), r};
+    EpiParams e;
+    e.out = s.ffn;
+    e.ldo = 2 * r;
+    HIPCHK(gemm(m->dt, p, EPI_SILU, e, st));
+  }
+  {
+    GemmProblem p{N, r, 2 * r, s.ffn, 2 * r, 2 * r, nullptr, 0, m->W(Y.p_w2), 2 * r};
+    EpiParams e;
+    e.aux = s.pr;
+    e.ld_aux = r;
+    if (to_phi0) {
+      e.out = cache->phi0;
+      e.ldo = r;
+      HIPCHK(gemm(m->dt, p, EPI_ADD_F32, e, st));
+    } else {
+      e.aux2 = cache->phi0;
+      e.ld_aux2 = r;
+      e.out_t = s.pmb;
+      e.ld_out_t = r;
+      HIPCHK(gemm(m->dt, p, EPI_ADD_SUB, e, st));
+    }
+  }
+  return TADM_OK;
+}
+
+// Z = (C / s_C) W_C into ws.pz (float) and ws.pzb (model type).
+static tadm_status paired_project(tadm_model* m, int N, const float* C, const float* sC, float* Zf, void* Zb) {
+  const tadm_config& cf = m->cfg;
+  Workspace& s = m->ws;
+  const int d = cf.d_model, r = cf.fusion_rank;
+  HIPCHK(scale_rows(m->dt, C, sC, N, d, s.xn, m->stream));
+  GemmProblem p{N, r, d, s.xn, d, d, nullptr, 0, m->W(m->lay.p_wc), d};
+  EpiParams e;
+  e.out = Zf;
+  e.ldo = r;
+  HIPCHK(gemm(m->dt, p, EPI_STORE_F32, e, m->stream));
+  HIPCHK(to_type(m->dt, Zf, (size_t)N * r, Zb, m->stream));
+  return TADM_OK;
+}
+
+// Refresh: token scales of C0 and H0, Z0, U and phi(Z0, U) into the cache.
+static tadm_status paired_prepare(tadm_model* m, int B, int L, tadm_cache* cache) {
+  const tadm_config& cf = m->cfg;
+  Workspace& s = m->ws;
+  const int N = B * L, d = cf.d_model, r = cf.fusion_rank;
+  const hipStream_t st = m->stream;
+  HIPCHK(row_rms(cache->c, N, d, cf.rms_eps, cache->sC, st));
+  HIPCHK(row_rms(cache->h, N, d, cf.rms_eps, cache->sH, st));
+  HIPCHK(scale_rows(m->dt, cache->h, cache->sH, N, d, s.xn, st));
+  {
+    GemmProblem p{N, r, d, s.xn, d, d, nullptr, 0, m->W(m->lay.p_wh), d};
+    EpiParams e;
+    e.out = cache->U;
+    e.ldo = r;
+    HIPCHK(gemm(m->dt, p, EPI_STORE_F32, e, st));
+  }
+  HIPCHK(to_type(m->dt, cache->U, (size_t)N * r, cache->Ub, st));
+  TRY(paired_project(m, N, cache->c, cache->sC, cache->Z0, s.pzb));
+  return paired_mixer(m, B, L, cache->Z0, s.pzb, cache, true);
+}
+
+// Step: H~ = H0 + g * s_H * (M W_up) into ws.x.
+static tadm_status paired_fuse(tadm_model* m, int B, int L, const float* c, const tadm_cache* ccache) {
+  tadm_cache* cache = const_cast<tadm_cache*>(ccache);  // phi0 is only read here
+  const tadm_config& cf = m->cfg;
+  Workspace& s = m->ws;
+  const Layout& Y = m->lay;
+  const int N = B * L, d = cf.d_model, r = cf.fusion_rank;
+  const hipStream_t st = m->stream;
+  TRY(paired_project(m, N, c, cache->sC, s.pz, s.pzb));
+  TRY(paired_mixer(m, B, L, s.pz, s.pzb, cache, false));
+  HIPCHK(paired_features(m->dt, cache->U, cache->Z0, s.pz, s.pmb, N, r, s.pf, st));
+  {
+    GemmProblem p{N, r, 4 * r, s.pf, 4 * r, 4 * r, nullptr, 0, m->W(Y.p_wg1), 4 * r};
+    EpiParams e;
+    e.out = s.pg1;
+    e.ldo = r;
+    HIPCHK(gemm(m->dt, p, EPI_SILU, e, st));
+  }
+  HIPCHK(row_gate(m->dt, s.pg1, m->Wf(Y.p_wg2), m->Wf(Y.p_bg), N, r, s.pgate, st));
+  {
+    GemmProblem p{N, d, r, s.pmb, r, r, nullptr, 0, m->W(Y.p_wup), r};
+    EpiParams e;
+    e.out = s.x;
+    e.ldo = d;
+    e.aux = cache->h;
+    e.ld_aux = d;
+    e.row1 = s.pgate;
+    e.row2 = cache->sH;
+    HIPCHK(gemm(m->dt, p, EPI_PAIRED, e, st));
+  }
+  return TADM_OK;
+}
+
 // anchor refresh: h = A(c) into the cache, with the fusion's anchor-side input.
 static tadm_status anchor_net(tadm_model* m, const tadm_context* ctx, int B, int L, const float* c,
                               tadm_cache* cache) {
@@ -423,12 +600,15 @@ static tadm_status anchor_net(tadm_model* m, const tadm_context* ctx, int B, int
   if (cf.fusion_kind == TADM_FUSION_GATED_MLP)
     HIPCHK(layer_norm(m->dt, cache->h, m->Wf(m->lay.ln_a_w), m->Wf(m->lay.ln_a_b), cf.ln_eps, B * L,
                       cf.d_model, cache->a, nullptr, m->stream));
+  else
+    TRY(paired_prepare(m, B, L, cache));
   return TADM_OK;
 }
 
-// h~ = Phi(c, cache) into ws.x (gated residual MLP).
+// h~ = Phi(c, cache) into ws.x.
 static tadm_status fusion(tadm_model* m, int B, int L, const float* c, const tadm_cache* cache) {
   const tadm_config& cf = m->cfg;
+  if (cf.fusion_kind == TADM_FUSION_PAIRED) return paired_fuse(m, B, L, c, cache);
   Workspace& s = m->ws;
   const int N = B * L, d = cf.d_model;
   const Layout& Y = m->lay;
@@ -524,12 +704,14 @@ tadm_status tadm_model_create(const tadm_config* cfg, tadm_model** out) {
   if (!out) return fail(TADM_ERR_INVALID, "null output pointer");
   *out = nullptr;
   if (!valid_config(cfg, why)) return fail(TADM_ERR_INVALID, "config: %s", why.c_str());
-  if (cfg->fusion_kind == TADM_FUSION_PAIRED)
-    return fail(TADM_ERR_UNSUPPORTED, "paired-attention fusion is not implemented in this build");
   if (cfg->dtype == TADM_DTYPE_BF16) {
-    const int ks[] = {cfg->d_model, cfg->n_heads * cfg->head_dim, cfg->d_ffn};
+    const int ks[] = {cfg->d_model, cfg->n_heads * cfg->head_dim, cfg->d_ffn,
+                      cfg->fusion_kind == TADM_FUSION_PAIRED ? cfg->fusion_rank : 64};
     for (int k : ks)
       if (k % 64) return fail(TADM_ERR_UNSUPPORTED, "bf16 contractions need K %% 64 == 0 (got %d)", k);
+    if (cfg->fusion_kind == TADM_FUSION_PAIRED && cfg->fusion_rank / cfg->paired_heads != 64 &&
+        cfg->fusion_rank / cfg->paired_heads != 128)
+      return fail(TADM_ERR_UNSUPPORTED, "bf16 paired attention needs heads of width 64 or 128");
     if (cfg->head_dim != 64 && cfg->head_dim != 128)
       return fail(TADM_ERR_UNSUPPORTED, "bf16 attention supports head_dim 64 or 128");
   } else if (cfg->head_dim > 128 || cfg->max_seq > 4096) {
@@ -640,6 +822,15 @@ static tadm_status cache_alloc(tadm_model* m, int B, int L, tadm_cache** out) {
   hipError_t e = hipMalloc((void**)&c->h, n * 4);
   if (e == hipSuccess) e = hipMalloc((void**)&c->c, n * 4);
   if (e == hipSuccess) e = hipMalloc(&c->a, n * m->esz);
+  if (e == hipSuccess && m->cfg.fusion_kind == TADM_FUSION_PAIRED) {
+    const size_t rows = (size_t)B * L, r = m->cfg.fusion_rank;
+    e = hipMalloc((void**)&c->sC, rows * 4);
+    if (e == hipSuccess) e = hipMalloc((void**)&c->sH, rows * 4);
+    if (e == hipSuccess) e = hipMalloc((void**)&c->Z0, rows * r * 4);
+    if (e == hipSuccess) e = hipMalloc((void**)&c->U, rows * r * 4);
+    if (e == hipSuccess) e = hipMalloc((void**)&c->phi0, rows * r * 4);
+    if (e == hipSuccess) e = hipMalloc(&c->Ub, rows * r * m->esz);
+  }
   if (e != hipSuccess) {
     tadm_cache_destroy(c);
     return fail(e == hipErrorOutOfMemory ? TADM_ERR_OOM : TADM_ERR_DEVICE, "cache: %s", hipGetErrorString(e));
@@ -661,9 +852,9 @@ tadm_status tadm_cache_create(tadm_model* m, int32_t B, int32_t L, tadm_cache** 
 tadm_status tadm_cache_destroy(tadm_cache* c) {
   if (!c) return fail(TADM_ERR_INVALID, "null cache");
   (void)hipDeviceSynchronize();
-  if (c->h) (void)hipFree(c->h);
-  if (c->c) (void)hipFree(c->c);
-  if (c->a) (void)hipFree(c->a);
+  for (void* p : {(void*)c->h, (void*)c->c, c->a, (void*)c->sC, (void*)c->sH, (void*)c->Z0, (void*)c->U,
+                  (void*)c->phi0, c->Ub})
+    if (p) (void)hipFree(p);
   delete c;
   return TADM_OK;
 }

@@ -32,8 +32,6 @@ def test_every_declared_symbol_is_exported():
 @pytest.mark.parametrize("name", list(synth.CONFIGS))
 def test_weight_order_matches_inputs(name):
     cfg = synth.get_config(name)
-    if cfg["fusion_kind"] == "paired":
-        pytest.skip("paired-attention fusion weights are not part of this build")
     c = tadm.make_config(cfg)
     specs = synth.weight_specs(cfg)
     assert tadm.tadm_weight_count(c) == len(specs)

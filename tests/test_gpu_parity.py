@@ -171,6 +171,61 @@ def test_attention_dominated_layer(dh, H, Hkv):
     _teacher_step_parity(cfg, 2, dict(BF16_TOL, scale_atol=True), tensors=tensors)
 
 
+def test_tiny_fp32_paired_step_parity():
+    cfg = synth.get_config("tiny", fusion_kind="paired", fusion_rank=32, batch=2)
+    _teacher_step_parity(cfg, 2, FP32_TOL)
+
+
+def test_paired_bf16_step_parity():
+    """Paired-attention fusion at rank 256 (4 heads of 64) with GQA and GeGLU as in the
+    26B-class shape, narrower model and few layers."""
+    cfg = synth.get_config("26b", d_model=1024, n_heads=8, n_kv_heads=4, head_dim=128, d_ffn=2048,
+                           n_anchor=2, n_denoise=1, vocab=4096, prompt_len=20, gen_len=100, block_len=100)
+    _teacher_step_parity(cfg, 2, BF16_TOL)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_paired_fresh_anchor_identity_bitwise(dtype):
+    """At a refresh step C = C0, so the fused state must equal the cached anchor H0
+    exactly (App. C.1): both mixer evaluations run the same deterministic kernels."""
+    over = dict(fusion_kind="paired", batch=2, dtype=dtype)
+    if dtype == "bf16":
+        over.update(d_model=512, n_heads=8, n_kv_heads=8, head_dim=64, d_ffn=1024, fusion_rank=256)
+    else:
+        over.update(fusion_rank=32)
+    cfg = synth.get_config("tiny", **over)
+    B, P, G = 2, cfg["prompt_len"], cfg["gen_len"]
+    L = P + G
+    tensors = synth.make_weights(cfg, perturb=True)
+    m = gpu_model(cfg, tensors, B, L)
+    try:
+        tadm.tadm_debug_taps(m, 1)
+        cache = tadm.tadm_cache_create(m, B, L)
+        z = synth.make_teacher_canvas(cfg, 11, batch=B, seed=8).to(dev())
+        tadm.tadm_anchor_forward(m, None, z, B, L, 5, 5, cache)
+        args = tadm.step_args(5, 5, 2, 0, 1, 1.0)
+        nz = torch.empty_like(z)
+        tadm.tadm_denoise_step(m, None, z, B, L, P, cache, args, None, nz)
+        fused = torch.empty(B, L, cfg["d_model"], device=dev())
+        h0 = torch.empty_like(fused)
+        tadm.tadm_debug_read(m, tadm.TAP_FUSED, fused)
+        tadm.tadm_cache_read(cache, tadm.CACHE_H, h0)
+        sync()
+        assert torch.equal(fused, h0)
+        tadm.tadm_cache_destroy(cache)
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
+def test_tiny_paired_generation_matches_oracle():
+    cfg = synth.get_config("tiny", batch=2, fusion_kind="paired", fusion_rank=32)
+    tensors, prompt, got = _generate(cfg, 4)
+    net = oracle_net(cfg, tensors)
+    ref = loop.generate(net, prompt.numpy(), cfg["gen_len"], cfg["T"], 4, cfg["block_len"], 2, 1.0,
+                        synth.mask_id(cfg))
+    np.testing.assert_array_equal(got, ref)
+
+
 # -------------------------------------------------------------- generation
 def _generate(cfg, K, block_len=None, B=None):
     B = B or cfg["batch"]
