@@ -14,6 +14,6 @@ norm gains and biases around their defaults so that a dropped gain or bias shows
 up in parity tests.
 """
 from .configs import CONFIGS, MASK_OFFSET, get_config, mask_id  # noqa: F401
-from .weights import weight_specs, make_weights, tensor_seed  # noqa: F401
+from .weights import weight_specs, make_weights, make_tensor, tensor_seed  # noqa: F401
 from .inputs import (make_prompt, make_timing_canvas, make_logits,  # noqa: F401
                      make_teacher_canvas)
