@@ -126,6 +126,34 @@ struct Epi<EPI_PAIRED, T> {
   }
 };
 template <class T>
+struct Epi<EPI_QKV_ROPE, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    const int b = m / e.L, l = m % e.L;
+    const int slot = n / e.dh, c = n % e.dh;  // c is a multiple of 4
+    if (slot < e.H + e.Hkv) {
+      // (v0, v1) = pair j, (v2, v3) = pair j + 1 with j = c / 2
+      const int j = c >> 1, half = e.dh >> 1;
+      const float* cs = e.cos_t + (size_t)(e.pos0 + l) * half + j;
+      const float* sn = e.sin_t + (size_t)(e.pos0 + l) * half + j;
+      const float a0 = v[0] * cs[0] - v[1] * sn[0], b0 = v[1] * cs[0] + v[0] * sn[0];
+      const float a1 = v[2] * cs[1] - v[3] * sn[1], b1 = v[3] * cs[1] + v[2] * sn[1];
+      T* row = slot < e.H
+                   ? static_cast<T*>(e.q) + (((size_t)b * e.H + slot) * e.L + l) * e.dh
+                   : static_cast<T*>(e.k) + (((size_t)b * e.Hkv + (slot - e.H)) * e.kv_cap + e.kv_off + l) * e.dh;
+      row[j] = from_f32<T>(a0);
+      row[j + 1] = from_f32<T>(a1);
+      row[j + half] = from_f32<T>(b0);
+      row[j + half + 1] = from_f32<T>(b1);
+    } else {
+      T* col = static_cast<T*>(e.vt) + (((size_t)b * e.Hkv + (slot - e.H - e.Hkv)) * e.dh + c) * e.kv_cap +
+               e.kv_off + l;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) col[(size_t)t * e.kv_cap] = from_f32<T>(v[t]);
+    }
+  }
+};
+template <class T>
 struct Epi<EPI_GLU_SILU, T> {
   static constexpr bool kGlu = true;
   __device__ static void glu(const EpiParams& e, int m, int f, f32x4 g, f32x4 u) {
@@ -361,12 +389,12 @@ hipError_t dispatch(DType dt, const GemmProblem& p, const EpiParams& e, hipStrea
     hipLaunchKernelGGL(gemm_f32_kernel<K>, dim3(tiles), dim3(256), 0, s, p, e);
     return hipGetLastError();
   }
-  // tile choice by how many blocks each shape yields (256 CUs): large GEMMs take
-  // 256 x 256 tiles on 8 waves, mid-size 128 x 128 at two blocks per CU, and the
-  // narrow (N = d_model) projections 64 x 64 at three blocks per CU
+  // tile choice by how many blocks each shape yields (256 CUs): GEMMs with many rows
+  // take 256 x 256 tiles on 8 waves, mid-size ones 128 x 128 at two blocks per CU, and
+  // the narrow (N = d_model) projections 64 x 64 at three blocks per CU
   const long t256 = (long)((p.M + 255) / 256) * ((p.N + 255) / 256);
   const long t128 = (long)((p.M + 127) / 128) * ((p.N + 127) / 128);
-  if (t256 >= 256) return launch_bf16<256, 256, 2, 2, 4, 1, K>(p, e, s);
+  if (p.M >= 4096 && t256 >= 256) return launch_bf16<256, 256, 2, 2, 4, 1, K>(p, e, s);
   if (t128 >= 256) return launch_bf16<128, 128, 2, 2, 2, 2, K>(p, e, s);
   return launch_bf16<64, 64, 2, 2, 2, 3, K>(p, e, s);
 }
@@ -389,6 +417,7 @@ hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e
     case EPI_ADD_BOTH: return dispatch<EPI_ADD_BOTH>(dt, p, e, s);
     case EPI_ADD_SUB: return dispatch<EPI_ADD_SUB>(dt, p, e, s);
     case EPI_PAIRED: return dispatch<EPI_PAIRED>(dt, p, e, s);
+    case EPI_QKV_ROPE: return dispatch<EPI_QKV_ROPE>(dt, p, e, s);
   }
   return hipErrorInvalidValue;
 }

@@ -33,6 +33,8 @@ enum EpiKind {
   EPI_ADD_BOTH,       // out(float)[m, n] = aux[m, n] + acc and out_t(T)[m, n] = the same value
   EPI_ADD_SUB,        // out_t(T)[m, n] = (aux[m, n] + acc) - aux2[m, n]
   EPI_PAIRED,         // out(float)[m, n] = aux[m, n] + row1[m] * row2[m] * acc
+  EPI_QKV_ROPE,       // q/k/v projection: rotary embedding on q, k (pair-interleaved
+                      // weight rows) and scatter into the attention layouts (see EpiParams)
 };
 
 struct EpiParams {
@@ -47,6 +49,17 @@ struct EpiParams {
   const float* row1 = nullptr;   // per-row factors
   const float* row2 = nullptr;
   void* out_t = nullptr; int ld_out_t = 0;
+  // EPI_QKV_ROPE: token m is (row m / L, position pos0 + m % L).  Output feature n is in
+  // head slot n / dh (q heads, then k heads, then v heads); within a q/k head the weight
+  // rows are ordered (0, dh/2, 1, dh/2 + 1, ...), so features 2j, 2j + 1 are the rotary
+  // pair (j, j + dh/2).  Q [B, H, L, dh], K rows kv_off + l of [B, Hkv, kv_cap, dh],
+  // V^T columns kv_off + l of [B, Hkv, dh, kv_cap].
+  int L = 0, pos0 = 0, H = 0, Hkv = 0, dh = 0, kv_cap = 0, kv_off = 0;
+  const float* cos_t = nullptr;
+  const float* sin_t = nullptr;
+  void* q = nullptr;
+  void* k = nullptr;
+  void* vt = nullptr;
 };
 
 hipError_t gemm(DType dt, const GemmProblem& p, EpiKind epi, const EpiParams& e, hipStream_t s);
@@ -122,8 +135,9 @@ namespace tadm {
 // dst row map(r) <- src row r (cols elements) for r < rows.  map(r) = row_off + r,
 // or, for glu_half >= 0, row_off + 32*(r/16) + 16*glu_half + r%16 (gate/up interleave
 // in 16-row blocks).  Elements keep the model type (dst_f32 = 0) or become float32.
+// rope_dh > 0: rows are heads of rope_dh rows reordered as (0, h, 1, h + 1, ...), h = rope_dh / 2.
 hipError_t scatter_rows(DType dt, const void* src, long rows, int cols, void* dst, int dst_f32,
-                        long row_off, int glu_half, hipStream_t s);
+                        long row_off, int glu_half, int rope_dh, hipStream_t s);
 // canvas rows: dst[b, :] = concat(prompt[b, :P], mask_id * gen)
 hipError_t init_canvas(const int32_t* prompt, int B, int P, int gen, int mask_id, int32_t* dst,
                        hipStream_t s);

@@ -212,12 +212,17 @@ hipError_t glu_f32(const float* pre, int n_rows, int F, int silu, float* out, hi
 namespace tadm {
 namespace {
 template <class T, class D>
-__global__ void scatter_kernel(const T* src, long rows, int cols, D* dst, long row_off, int glu_half) {
+__global__ void scatter_kernel(const T* src, long rows, int cols, D* dst, long row_off, int glu_half,
+                               int rope_dh) {
   const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= rows * cols) return;
   const long r = i / cols;
   const int c = (int)(i % cols);
-  const long dr = glu_half < 0 ? row_off + r : row_off + 32 * (r / 16) + 16 * glu_half + r % 16;
+  long dr = glu_half < 0 ? row_off + r : row_off + 32 * (r / 16) + 16 * glu_half + r % 16;
+  if (rope_dh > 0) {
+    const int h = rope_dh / 2, w = (int)(r % rope_dh);
+    dr = row_off + (r / rope_dh) * rope_dh + (w < h ? 2 * w : 2 * (w - h) + 1);
+  }
   dst[dr * cols + c] = from_f32<D>(f32_of(src[i]));
 }
 __global__ void init_canvas_kernel(const int32_t* prompt, int B, int P, int gen, int mask_id,
@@ -235,7 +240,7 @@ __global__ void fill_kernel(int32_t* dst, size_t n, int32_t v) {
 }  // namespace
 
 hipError_t scatter_rows(DType dt, const void* src, long rows, int cols, void* dst, int dst_f32,
-                        long row_off, int glu_half, hipStream_t s) {
+                        long row_off, int glu_half, int rope_dh, hipStream_t s) {
   const long n = rows * cols;
   if (n == 0) return hipSuccess;
   const unsigned g = (unsigned)((n + 255) / 256);
@@ -243,15 +248,15 @@ hipError_t scatter_rows(DType dt, const void* src, long rows, int cols, void* ds
     if (dst_f32)
       hipLaunchKernelGGL((scatter_kernel<bf16, float>), dim3(g), dim3(256), 0, s,
                          static_cast<const bf16*>(src), rows, cols, static_cast<float*>(dst), row_off,
-                         glu_half);
+                         glu_half, rope_dh);
     else
       hipLaunchKernelGGL((scatter_kernel<bf16, bf16>), dim3(g), dim3(256), 0, s,
                          static_cast<const bf16*>(src), rows, cols, static_cast<bf16*>(dst), row_off,
-                         glu_half);
+                         glu_half, rope_dh);
   } else {
     hipLaunchKernelGGL((scatter_kernel<float, float>), dim3(g), dim3(256), 0, s,
                        static_cast<const float*>(src), rows, cols, static_cast<float*>(dst), row_off,
-                       glu_half);
+                       glu_half, rope_dh);
   }
   return hipGetLastError();
 }

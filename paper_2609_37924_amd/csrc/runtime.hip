@@ -62,6 +62,7 @@ struct Spec {
   Place place;
   long row_off;
   int glu_half;
+  int rope_dh;      // > 0: q/k rows reordered so rotary pairs are adjacent
 };
 
 struct Tensor {
@@ -90,8 +91,8 @@ int add_tensor(Layout& L, long rows, long cols, bool f32) {
 }
 
 void add_spec(Layout& L, const std::string& n, long rows, long cols, int target, Place p,
-              long row_off = 0, int glu_half = -1) {
-  L.specs.push_back(Spec{n, rows, cols, target, p, row_off, glu_half});
+              long row_off = 0, int glu_half = -1, int rope_dh = 0) {
+  L.specs.push_back(Spec{n, rows, cols, target, p, row_off, glu_half, rope_dh});
 }
 
 Layout make_layout(const tadm_config& c) {
@@ -165,8 +166,8 @@ Layout make_layout(const tadm_config& c) {
     x.wdown = add_tensor(L, d, F, false);
     L.layers.push_back(x);
     add_spec(L, p + "attn_norm", d, 0, x.attn_norm, P_VEC);
-    add_spec(L, p + "wq", H * dh, d, x.wqkv, P_ROWS, 0);
-    add_spec(L, p + "wk", Hk * dh, d, x.wqkv, P_ROWS, H * dh);
+    add_spec(L, p + "wq", H * dh, d, x.wqkv, P_ROWS, 0, -1, (int)dh);
+    add_spec(L, p + "wk", Hk * dh, d, x.wqkv, P_ROWS, H * dh, -1, (int)dh);
     add_spec(L, p + "wv", Hk * dh, d, x.wqkv, P_ROWS, (H + Hk) * dh);
     add_spec(L, p + "wo", d, H * dh, x.wo, P_COPY);
     add_spec(L, p + "ffn_norm", d, 0, x.ffn_norm, P_VEC);
@@ -394,14 +395,23 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
   const hipStream_t st = m->stream;
   HIPCHK(rms_norm(m->dt, x, m->Wf(w.attn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
   {
+    // q/k/v projection with the rotary embedding and head split in the epilogue
     GemmProblem p{N, (H + 2 * Hk) * dh, d, s.xn, d, d, nullptr, 0, m->W(w.wqkv), d};
     EpiParams e;
-    e.out = s.qkv;
-    e.ldo = (H + 2 * Hk) * dh;
-    HIPCHK(gemm(m->dt, p, EPI_STORE, e, st));
+    e.L = L;
+    e.pos0 = pos0;
+    e.H = H;
+    e.Hkv = Hk;
+    e.dh = dh;
+    e.kv_cap = kv.cap;
+    e.kv_off = kv.off;
+    e.cos_t = m->rope_cos;
+    e.sin_t = m->rope_sin;
+    e.q = s.q;
+    e.k = kv.k;
+    e.vt = kv.vt;
+    HIPCHK(gemm(m->dt, p, EPI_QKV_ROPE, e, st));
   }
-  HIPCHK(rope_split(m->dt, s.qkv, B, L, H, Hk, dh, pos0, m->rope_cos, m->rope_sin, s.q, kv.k, kv.vt,
-                    kv.cap, kv.off, st));
   HIPCHK(attention(m->dt, s.q, kv.k, kv.vt, s.ao, B, H, Hk, L, kv.off + L, kv.cap, dh, st));
   {
     GemmProblem p{N, d, H * dh, s.ao, H * dh, H * dh, nullptr, 0, m->W(w.wo), H * dh};
@@ -775,7 +785,7 @@ tadm_status tadm_model_load_weight(tadm_model* m, int32_t index, const void* src
   }
   const Tensor& t = m->lay.tensors[sp.target];
   hipError_t e = scatter_rows(m->dt, dsrc, sp.rows, (int)cols, m->W(sp.target), t.f32 ? 1 : 0, sp.row_off,
-                              sp.place == P_GLU ? sp.glu_half : -1, nullptr);
+                              sp.place == P_GLU ? sp.glu_half : -1, sp.rope_dh, nullptr);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (staging) (void)hipFree(staging);
   if (e != hipSuccess) return fail(TADM_ERR_DEVICE, "weight placement: %s", hipGetErrorString(e));
