@@ -394,7 +394,7 @@ hipError_t dispatch(DType dt, const GemmProblem& p, const EpiParams& e, hipStrea
   // the narrow (N = d_model) projections 64 x 64 at three blocks per CU
   const long t256 = (long)((p.M + 255) / 256) * ((p.N + 255) / 256);
   const long t128 = (long)((p.M + 127) / 128) * ((p.N + 127) / 128);
-  if (p.M >= 4096 && t256 >= 256) return launch_bf16<256, 256, 2, 2, 4, 1, K>(p, e, s);
+  if ((p.M >= 4096 || p.N >= 16384) && t256 >= 128) return launch_bf16<256, 256, 2, 2, 4, 1, K>(p, e, s);
   if (t128 >= 256) return launch_bf16<128, 128, 2, 2, 2, 2, K>(p, e, s);
   return launch_bf16<64, 64, 2, 2, 2, 3, K>(p, e, s);
 }

@@ -96,7 +96,55 @@ __device__ __forceinline__ Best better(Best a, Best b) {
   return (b.score > a.score || (b.score == a.score && b.v < a.v)) ? b : a;
 }
 
+// Screening logarithm: the same exponent/mantissa split and atanh series as own_log,
+// with an approximate reciprocal and a shorter series.  Relative error below 1e-6 on
+// the sampler's arguments; it only ranks entries and never decides a token.
+__device__ __forceinline__ float screen_log(float x) {
+  const float LN2 = bits_f(0x3F317218u);
+  const uint32_t bits = __float_as_uint(x);
+  int e = (int)(bits >> 23) - 127;
+  uint32_t mb = (bits & 0x007FFFFFu) | 0x3F800000u;
+  if (mb > 0x3FB504F3u) {
+    mb -= 0x00800000u;
+    e += 1;
+  }
+  const float f = __uint_as_float(mb) - 1.0f;
+  const float s = f * __builtin_amdgcn_rcpf(2.0f + f);
+  const float z = s * s;
+  const float p = fmaf(z, fmaf(z, fmaf(z, 0.2857142857f, 0.4f), 0.6666666667f), 2.0f);
+  return fmaf((float)e, LN2, s * p);
+}
+
+// Exact contract score of entry v: l'_v + G_v with G = -log(-log u), u from Philox.
+__device__ __forceinline__ float exact_score(const float* lg, int v, uint32_t pos, uint32_t b,
+                                             uint32_t step_id, uint32_t k0, uint32_t k1, float inv_temp) {
+  uint32_t c[4] = {(uint32_t)(v >> 2), pos, b, step_id};
+  philox4x32_10(c, k0, k1);
+  const float E = -own_log(uniform01(c[v & 3]));
+  const float G = -own_log(E);
+  return lg[v] * inv_temp + G;
+}
+
+template <bool VEC4>
+__device__ __forceinline__ void load4(const float* lg, int g, int V, float l4[4]) {
+  if (VEC4) {
+    const float4 v4 = *reinterpret_cast<const float4*>(lg + 4 * g);
+    l4[0] = v4.x; l4[1] = v4.y; l4[2] = v4.z; l4[3] = v4.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) l4[e] = 4 * g + e < V ? lg[4 * g + e] : 0.f;
+  }
+}
+
 // grid (Lc, B); one workgroup per canvas position; only masked positions work.
+//
+// Pass 1: m = max_v l'_v.  Pass 2: the fixed-point normaliser S (exact, every entry)
+// and a screening value r_v = exp(l'_v - m) / E_v with E_v = -log u_v from the
+// screening log, so log r_v approximates the contract score minus m to within
+// ~2e-5 (|logits| < 1e3).  Only entries with r_v >= w * max r (a window of 1e-3 plus
+// the rounding of large scores, in log space) can hold the contract argmax; when each
+// thread has at most one such entry they are evaluated exactly and compared as
+// (score, smaller v); otherwise the row falls back to the exact scan of every entry.
 template <bool VEC4>
 __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const int32_t* row_map,
                                                      const int32_t* canvas,
@@ -104,8 +152,10 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
                                                      int pos0, uint32_t step_id, uint32_t k0,
                                                      uint32_t k1, float inv_temp, int32_t* choice,
                                                      float* conf) {
-  __shared__ float s_max[4], s_score[4];
+  __shared__ float s_f[4];
+  __shared__ float s_score[4];
   __shared__ int s_v[4];
+  __shared__ int s_flag[4];
   __shared__ long long s_sum[4];
   const int j = blockIdx.x, b = blockIdx.y;
   const int row = b * Lc + j;
@@ -121,71 +171,99 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
   const int ngroups = (V + 3) / 4;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 
-  Best best{-INFINITY, 0x7FFFFFFF};
+  // ---- pass 1: max scaled logit
   float mx = -INFINITY;
   for (int g = threadIdx.x; g < ngroups; g += 256) {
+    float l4[4];
+    load4<VEC4>(lg, g, V, l4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (VEC4 || 4 * g + e < V) mx = fmaxf(mx, l4[e] * inv_temp);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  if (lane == 0) s_f[wave] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(s_f[0], s_f[1]), fmaxf(s_f[2], s_f[3]));
+  __syncthreads();
+
+  // ---- pass 2: exact normaliser, screening values (top two per thread)
+  long long S = 0;
+  float r1 = 0.f, r2 = 0.f;
+  int v1 = 0x7FFFFFFF;
+  for (int g = threadIdx.x; g < ngroups; g += 256) {
+    float l4[4];
+    load4<VEC4>(lg, g, V, l4);
     uint32_t c[4] = {(uint32_t)g, pos, (uint32_t)b, step_id};
     philox4x32_10(c, k0, k1);
-    float l4[4];
-    if (VEC4) {
-      const float4 v4 = *reinterpret_cast<const float4*>(lg + 4 * g);
-      l4[0] = v4.x; l4[1] = v4.y; l4[2] = v4.z; l4[3] = v4.w;
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) l4[e] = 4 * g + e < V ? lg[4 * g + e] : 0.f;
-    }
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int v = 4 * g + e;
       if (!VEC4 && v >= V) break;
-      const float lp = l4[e] * inv_temp;
-      mx = fmaxf(mx, lp);
-      const float E = -own_log(uniform01(c[e]));
-      const float G = -own_log(E);
-      const float sc = lp + G;
-      if (sc > best.score) best = Best{sc, v};
+      const float ev = own_exp(l4[e] * inv_temp - mx);
+      S += (long long)rintf(ev * 1099511627776.0f);  // * 2^40, exact
+      const float r = ev * __builtin_amdgcn_rcpf(-screen_log(uniform01(c[e])));
+      if (r > r1) {
+        r2 = r1;
+        r1 = r;
+        v1 = v;
+      } else if (r > r2) {
+        r2 = r;
+      }
     }
   }
-  // block reductions: max logit and best (score, v)
+  float rmax = r1;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
-    mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    S += __shfl_xor(S, o, 64);
+    rmax = fmaxf(rmax, __shfl_xor(rmax, o, 64));
+  }
+  if (lane == 0) {
+    s_sum[wave] = S;
+    s_f[wave] = rmax;
+  }
+  __syncthreads();
+  rmax = fmaxf(fmaxf(s_f[0], s_f[1]), fmaxf(s_f[2], s_f[3]));
+  const float delta = 1e-3f + 2.4e-6f * (fabsf(mx) + 32.f);   // bound on |log r - (score - m)|, x 100
+  const float w = 1.f - 2.5f * delta;                           // below exp(-2 delta)
+  const bool cand = r1 >= w * rmax;
+  // ---- exact decision among candidates (or all entries if a thread has two)
+  const int multi = __any(r2 >= w * rmax) ? 1 : 0;
+  if (lane == 0) s_flag[wave] = multi;
+  __syncthreads();
+  const bool slow = s_flag[0] | s_flag[1] | s_flag[2] | s_flag[3];
+  Best best{-INFINITY, 0x7FFFFFFF};
+  if (!slow) {
+    if (cand) best = Best{exact_score(lg, v1, pos, (uint32_t)b, step_id, k0, k1, inv_temp), v1};
+  } else {
+    for (int g = threadIdx.x; g < ngroups; g += 256) {
+      float l4[4];
+      load4<VEC4>(lg, g, V, l4);
+      uint32_t c[4] = {(uint32_t)g, pos, (uint32_t)b, step_id};
+      philox4x32_10(c, k0, k1);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int v = 4 * g + e;
+        if (!VEC4 && v >= V) break;
+        const float E = -own_log(uniform01(c[e]));
+        const float sc = l4[e] * inv_temp + (-own_log(E));
+        if (sc > best.score) best = Best{sc, v};
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
     const Best other{__shfl_xor(best.score, o, 64), __shfl_xor(best.v, o, 64)};
     best = better(best, other);
   }
   if (lane == 0) {
-    s_max[wave] = mx;
     s_score[wave] = best.score;
     s_v[wave] = best.v;
   }
   __syncthreads();
-  mx = fmaxf(fmaxf(s_max[0], s_max[1]), fmaxf(s_max[2], s_max[3]));
-  best = Best{s_score[0], s_v[0]};
-  for (int w = 1; w < 4; ++w) best = better(best, Best{s_score[w], s_v[w]});
-
-  long long S = 0;
-  for (int g = threadIdx.x; g < ngroups; g += 256) {
-    float l4[4];
-    if (VEC4) {
-      const float4 v4 = *reinterpret_cast<const float4*>(lg + 4 * g);
-      l4[0] = v4.x; l4[1] = v4.y; l4[2] = v4.z; l4[3] = v4.w;
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) l4[e] = 4 * g + e < V ? lg[4 * g + e] : 0.f;
-    }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (!VEC4 && 4 * g + e >= V) break;
-      const float lp = l4[e] * inv_temp;
-      const float ev = own_exp(lp - mx);
-      S += (long long)rintf(ev * 1099511627776.0f);  // * 2^40, exact
-    }
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) S += __shfl_xor(S, o, 64);
-  if (lane == 0) s_sum[wave] = S;
-  __syncthreads();
   if (threadIdx.x == 0) {
+    best = Best{s_score[0], s_v[0]};
+    for (int k = 1; k < 4; ++k) best = better(best, Best{s_score[k], s_v[k]});
     S = s_sum[0] + s_sum[1] + s_sum[2] + s_sum[3];
     if (best.v >= V) best.v = 0;  // only reachable with non-finite logits
     const float lpx = lg[best.v] * inv_temp;

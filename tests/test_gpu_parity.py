@@ -31,13 +31,16 @@ def sync():
 
 
 # ------------------------------------------------------------------ sampler
-@pytest.mark.parametrize("V,B,L,off,temp,ties", [
-    (256, 2, 40, 8, 1.0, False),
-    (1001, 3, 33, 0, 0.7, False),    # vocab not a multiple of 4: scalar path
-    (32768, 2, 24, 4, 1.0, False),
-    (64, 4, 64, 0, 1.0, True),       # duplicated rows and planted exact ties
+@pytest.mark.parametrize("V,B,L,off,temp,ties,std", [
+    (256, 2, 40, 8, 1.0, False, 2.0),
+    (1001, 3, 33, 0, 0.7, False, 2.0),    # vocab not a multiple of 4: scalar path
+    (32768, 2, 24, 4, 1.0, False, 2.0),
+    (64, 4, 64, 0, 1.0, True, 2.0),       # duplicated rows and planted exact ties
+    (8, 32, 1024, 0, 1.0, False, 1e-3),   # near-equal scores: many rows take the exact fallback
+    (4, 16, 256, 0, 1.0, False, 0.0),     # all logits equal: the Gumbel noise alone decides
+    (50304, 1, 6, 2, 1.3, False, 30.0),   # wide, peaked distribution
 ])
-def test_sampler_bit_exact(V, B, L, off, temp, ties):
+def test_sampler_bit_exact(V, B, L, off, temp, ties, std):
     cfg = synth.get_config("tiny", vocab=V)
     m = tadm.tadm_model_create(tadm.make_config(cfg, max_batch=B, max_seq=L))
     tadm.tadm_set_stream(m, torch.cuda.current_stream().cuda_stream)
@@ -48,7 +51,7 @@ def test_sampler_bit_exact(V, B, L, off, temp, ties):
         canvas[0, off:] = V  # one fully masked row
         if ties:
             canvas[1] = canvas[0]
-        logits = synth.make_logits(B * (L - off), V, seed=V, std=2.0, ties=ties).view(B, L - off, V)
+        logits = synth.make_logits(B * (L - off), V, seed=V, std=std, ties=ties).view(B, L - off, V)
         if ties:
             logits[1] = logits[0]
         inv_temp = float(np.float32(1.0 / temp))
