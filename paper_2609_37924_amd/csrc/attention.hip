@@ -1,8 +1,8 @@
 // Rotary embedding + head split, and bidirectional softmax attention.
 //
 // bf16 attention: one workgroup = 64 queries of one (row, head); 4 wave64s with
-// 16 queries each.  K (64 keys x dh) and V^T (dh x 64 keys) tiles are staged in LDS,
-// double-buffered.  Scores are computed transposed, S^T = K Q^T with
+// 16 queries each.  K (64 keys x dh) and V^T (dh x 64 keys) tiles move global -> LDS
+// with global_load_lds_dwordx4 into a 2-stage ring (16-byte chunks swizzled by row).  Scores are computed transposed, S^T = K Q^T with
 // v_mfma_f32_16x16x32_bf16, so that each lane owns one query: the online-softmax
 // statistics live in the lane and the probabilities feed the O^T = V^T P^T MFMA
 // directly from registers (the k index of that product walks keys in the order the
@@ -56,63 +56,50 @@ __global__ __launch_bounds__(256) void rope_split_kernel(const T* qkv, int B, in
   }
 }
 
+typedef __attribute__((address_space(3))) void* lds_ptr;
+typedef const __attribute__((address_space(1))) void* gbl_ptr;
+constexpr int vmcnt_all() { return (7 << 4) | (15 << 8); }  // s_waitcnt vmcnt(0)
+
+// K tile: 64 keys x DH, stored as DH/64 planes of [64 keys][128 B]; V^T tile: DH rows x
+// 64 keys of 128 B.  Chunk c (8 bf16) of LDS row r sits in slot c ^ (r & 7).
 template <int DH>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const bf16* K,
                                                            const bf16* Vt, bf16* O, int H, int Hkv,
                                                            int Lq, int Lk, int kv_cap,
                                                            float scale_log2) {
   constexpr int KT = 64;
-  constexpr int KS = DH + 8;  // K tile row stride (elements)
-  constexpr int VS = KT + 8;  // V^T tile row stride
-  constexpr int NC = DH / 32; // 16-byte chunks per thread per tile (K and V each)
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][KT * KS];
-  __shared__ __attribute__((aligned(16))) bf16 sV[2][DH * VS];
+  constexpr int KBYTES = KT * DH * 2, VBYTES = DH * KT * 2, STAGE = KBYTES + VBYTES;
+  constexpr int LK = KBYTES / 1024 / 4, LV = VBYTES / 1024 / 4;  // load instructions per wave
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, grp = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, grp = lane >> 4, fr = lane & 15;
   const int h = blockIdx.y, b = blockIdx.z;
   const int hk = (h * Hkv) / H;
   const bf16* Kb = K + ((size_t)b * Hkv + hk) * kv_cap * DH;
   const bf16* Vb = Vt + ((size_t)b * Hkv + hk) * DH * kv_cap;
-  const int q = blockIdx.x * 64 + wave * 16 + (lane & 15);
+  const int q = blockIdx.x * 64 + wave * 16 + fr;
   const bf16* Qr = Q + (((size_t)b * H + h) * Lq + min(q, Lq - 1)) * DH;
 
   bf16x8 qf[DH / 32];
 #pragma unroll
   for (int kc = 0; kc < DH / 32; ++kc) qf[kc] = *reinterpret_cast<const bf16x8*>(Qr + 32 * kc + 8 * grp);
 
-  uint4 rk[NC], rv[NC];
-  auto gload = [&](int t) {
+  const int lrow = lane >> 3, lchunk = (lane & 7) ^ (lane >> 3);
+  const int nt = (Lk + KT - 1) / KT;
+  auto issue = [&](int t, int buf) {
     const int k0 = t * KT;
+    char* sb = smem + buf * STAGE;
 #pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      const int c = tid + 256 * i, key = c / (DH / 8), ch = c % (DH / 8);
-      rk[i] = *reinterpret_cast<const uint4*>(Kb + (size_t)min(k0 + key, Lk - 1) * DH + ch * 8);
+    for (int j = 0; j < LK; ++j) {  // 8-row groups of the K planes
+      const int g = wave + 4 * j, plane = g / 8, r = (g % 8) * 8 + lrow;
+      const bf16* src = Kb + (size_t)min(k0 + r, Lk - 1) * DH + plane * 64 + lchunk * 8;
+      __builtin_amdgcn_global_load_lds((gbl_ptr)src, (lds_ptr)(sb + g * 1024), 16, 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, ch = c & 7;
-      const int key0 = k0 + ch * 8;  // < kv_cap (a multiple of 64): in bounds
-      uint4 v = *reinterpret_cast<const uint4*>(Vb + (size_t)row * kv_cap + key0);
-      if (key0 + 8 > Lk) {  // zero keys past the end so that p = 0 meets finite values
-        bf16x8 w = *reinterpret_cast<bf16x8*>(&v);
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (key0 + e >= Lk) w[e] = (bf16)0.f;
-        v = *reinterpret_cast<uint4*>(&w);
-      }
-      rv[i] = v;
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      const int c = tid + 256 * i, key = c / (DH / 8), ch = c % (DH / 8);
-      *reinterpret_cast<uint4*>(&sK[buf][key * KS + ch * 8]) = rk[i];
-    }
-#pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, ch = c & 7;
-      *reinterpret_cast<uint4*>(&sV[buf][row * VS + ch * 8]) = rv[i];
+    for (int j = 0; j < LV; ++j) {  // 8-row groups of V^T
+      const int g = wave + 4 * j, r = g * 8 + lrow;
+      const bf16* src = Vb + (size_t)r * kv_cap + k0 + lchunk * 8;  // k0 + 64 <= kv_cap
+      __builtin_amdgcn_global_load_lds((gbl_ptr)src, (lds_ptr)(sb + KBYTES + g * 1024), 16, 0, 0);
     }
   };
 
@@ -121,21 +108,35 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
   for (int d = 0; d < DH / 16; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  const int nt = (Lk + KT - 1) / KT;
-  gload(0);
-  sstore(0);
-  __syncthreads();
+  issue(0, 0);
   for (int t = 0; t < nt; ++t) {
     const int buf = t & 1;
-    if (t + 1 < nt) gload(t + 1);
+    __builtin_amdgcn_s_waitcnt(vmcnt_all());
+    __syncthreads();
+    const char* sk = smem + buf * STAGE;
+    const char* sv = sk + KBYTES;
+    if ((t + 1) * KT > Lk) {
+      // last, partial tile: keys past the end get V = 0 so that p = 0 meets finite values
+      char* svw = const_cast<char*>(sv);
+      for (int idx = tid; idx < DH * KT; idx += 256) {
+        const int r = idx / KT, key = idx % KT;
+        if (t * KT + key >= Lk) {
+          const int slot = (key >> 3) ^ (r & 7);
+          *reinterpret_cast<bf16*>(svw + r * 128 + slot * 16 + (key & 7) * 2) = (bf16)0.f;
+        }
+      }
+      __syncthreads();
+    }
+    if (t + 1 < nt) issue(t + 1, buf ^ 1);
     f32x4 s[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       s[ks] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int r = ks * 16 + fr;
 #pragma unroll
       for (int kc = 0; kc < DH / 32; ++kc) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
-            &sK[buf][(ks * 16 + (lane & 15)) * KS + 32 * kc + 8 * grp]);
+        const int plane = kc >> 1, c = (kc & 1) * 4 + grp;
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + plane * 8192 + r * 128 + ((c ^ (r & 7)) * 16));
         s[ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kc], s[ks], 0, 0, 0);
       }
     }
@@ -175,19 +176,18 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
         pf[j] = (bf16)s[2 * kc2][j];
         pf[4 + j] = (bf16)s[2 * kc2 + 1][j];
       }
+      // keys 32*kc2 + 4*grp + [0,4) and 32*kc2 + 16 + 4*grp + [0,4): chunks 4*kc2 + grp/2
+      // and 4*kc2 + 2 + grp/2, at byte (grp & 1) * 8 inside the chunk
+      const int c0 = 4 * kc2 + (grp >> 1), c1 = c0 + 2, inb = (grp & 1) * 8;
 #pragma unroll
       for (int d = 0; d < DH / 16; ++d) {
-        const bf16* vr = &sV[buf][(d * 16 + (lane & 15)) * VS + 32 * kc2 + 4 * grp];
-        const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(vr);
-        const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(vr + 16);
-        bf16x8 vf;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) { vf[j] = v0[j]; vf[4 + j] = v1[j]; }
+        const int r = d * 16 + fr;
+        const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(sv + r * 128 + ((c0 ^ (r & 7)) * 16) + inb);
+        const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(sv + r * 128 + ((c1 ^ (r & 7)) * 16) + inb);
+        const bf16x8 vf = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
         o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[d], 0, 0, 0);
       }
     }
-    if (t + 1 < nt) sstore(buf ^ 1);
-    __syncthreads();
   }
   float l_tot = l_run + __shfl_xor(l_run, 16, 64);
   l_tot += __shfl_xor(l_tot, 32, 64);

@@ -176,15 +176,20 @@ constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >>
 typedef __attribute__((address_space(3))) void* lds_ptr;
 typedef const __attribute__((address_space(1))) void* gbl_ptr;
 
-// Block index -> (m tile, n tile), keeping consecutive tiles on one XCD.
-__device__ __forceinline__ void tile_of(int tiles_m, int tiles, int& tm, int& tn) {
+// Block index -> (m tile, n tile).  Workgroups are dealt to the 8 XCDs round-robin,
+// so block b runs on XCD b % 8 as its (b / 8)-th block.  When the tile grid splits
+// into 8 regions of rm x rn tiles, XCD x works through region x (m fastest), so the
+// A rows and W rows it reads (rm*BM + rn*BN rows) stay in its own L2.
+__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int rm, int rn, int& tm, int& tn) {
   const int b = blockIdx.x;
-  const int per = (tiles + 7) / 8;  // tiles per XCD
-  const int x = b % 8, i = b / 8;
-  int t = x * per + i;
-  if (per * 8 != tiles) t = b;  // uneven split: keep the plain order
-  tm = t % tiles_m;
-  tn = t / tiles_m;
+  if (rm > 0) {
+    const int x = b % 8, i = b / 8, regions_m = tiles_m / rm;
+    tm = (x % regions_m) * rm + i % rm;
+    tn = (x / regions_m) * rn + i / rm;
+    return;
+  }
+  tm = b % tiles_m;
+  tn = b / tiles_m;
 }
 
 // ------------------------------------------------------------ bf16 MFMA kernel
@@ -206,7 +211,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
   const int wm = wave % WGM, wn = wave / WGM;
   const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
   int tmi, tni;
-  tile_of(tiles_m, tiles_m * tiles_n, tmi, tni);
+  tile_of(tiles_m, tiles_n, p.rm, p.rn, tmi, tni);
   const int m0 = tmi * BM, n0 = tni * BN;
   if (p.M_dev) {  // rows present this call; the grid was sized for p.M
     p.M = min(*p.M_dev, p.M);
@@ -374,11 +379,30 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmProblem p, EpiParams 
   }
 }
 
+// Per-XCD region rm x rn with (tiles_m / rm) * (tiles_n / rn) = 8 that minimises the
+// rows each XCD reads (rm * BM + rn * BN); 0 when the grid does not split evenly.
+inline void xcd_regions(int tiles_m, int tiles_n, int BM, int BN, int& rm, int& rn) {
+  rm = rn = 0;
+  long best = -1;
+  for (int gm = 1; gm <= 8; gm *= 2) {
+    const int gn = 8 / gm;
+    if (tiles_m % gm || tiles_n % gn) continue;
+    const long cost = (long)(tiles_m / gm) * BM + (long)(tiles_n / gn) * BN;
+    if (best < 0 || cost < best) {
+      best = cost;
+      rm = tiles_m / gm;
+      rn = tiles_n / gn;
+    }
+  }
+}
+
 template <int BM, int BN, int ST, int WGM, int WGN, int MINB, EpiKind K>
-hipError_t launch_bf16(const GemmProblem& p, const EpiParams& e, hipStream_t s) {
-  const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, ST, WGM, WGN, MINB, K>), dim3(tiles), dim3(64 * WGM * WGN), 0,
-                     s, p, e);
+hipError_t launch_bf16(const GemmProblem& p0, const EpiParams& e, hipStream_t s) {
+  GemmProblem p = p0;
+  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
+  xcd_regions(tiles_m, tiles_n, BM, BN, p.rm, p.rn);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, ST, WGM, WGN, MINB, K>), dim3(tiles_m * tiles_n),
+                     dim3(64 * WGM * WGN), 0, s, p, e);
   return hipGetLastError();
 }
 

@@ -17,6 +17,7 @@ struct GemmProblem {
   const void* A2; int lda2;
   const void* W;  int ldw;
   const int* M_dev = nullptr;  // if set: rows actually present (<= M; M sizes the grid)
+  int rm = 0, rn = 0;          // per-XCD tile region (set by the launcher)
 };
 
 enum EpiKind {
