@@ -5,16 +5,28 @@ refreshes included) of a batch of synthetic prompts, enqueued by tadm_generate w
 inputs already resident in HBM.  value = B * gen_len / time per step at the headline
 refresh interval; the other refresh intervals of the workload are reported beside it.
 
-Prints one JSON line.  Extra fields: the K sweep, per-stage time, the roofline of
-the dominant kernel (algorithmic flops over its HIP-event-timed duration) and the
-CPU oracle timed on a bounded sample.
+Prints one JSON line.  Extra fields: the K sweep, per-stage time, a table of the
+timed kernels (algorithmic flops or bytes of the schedule over their event-timed
+durations), the roofline of the dominant kernel and the CPU oracle timed on a bounded
+sample.  The per-kernel table comes from a pass of its own with timers on every
+stage; the dominant kernel is then timed again inside the headline timed region, on
+its launches of the last generation (each timed launch adds a few microseconds).
+Its HBM traffic comes from the committed counter summary of the workload while the
+kernel's sources are unchanged since the counters were taken.
+
+--render-stats and --render-counters turn rocprofv3 output into those summaries.
 """
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
+from collections import defaultdict
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -33,16 +45,222 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-sweep", action="store_true", help="only the headline K")
     ap.add_argument("--out", default=None, help="also write the JSON line to this file")
+    ap.add_argument("--render-stats", metavar="DIR", default=None,
+                    help="print a markdown summary of the rocprofv3 --stats output under DIR and exit")
+    ap.add_argument("--render-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None,
+                    help="print per-kernel HBM traffic from two rocprofv3 --pmc runs "
+                         "(FETCH_SIZE, then WRITE_SIZE) and exit")
+    ap.add_argument("--command", default="", help="command line quoted in a rendered summary")
     return ap.parse_args()
 
 
-def head_flops(cfg, B):
-    """Algorithmic flops of the average vocabulary-projection launch, 2 * rows * d * V,
-    where rows = the masked positions entering step i: B * floor(M0 * i / T) with M0
-    the block length (the head only runs on masked positions)."""
-    M0, T = cfg["block_len"], cfg["T"]
-    rows = sum(B * ((M0 * i) // T) for i in range(1, T + 1)) / T
-    return 2.0 * rows * cfg["d_model"] * cfg["vocab"]
+# --------------------------------------------------------------- work model ----
+# Algorithmic work of one generation per timed kernel stage: flops of each launch
+# summed over the schedule of Algorithm 1 (refresh iff (T - i) mod K == 0, one head
+# launch per step over the masked rows, block mode with its context passes), and the
+# number of launches.  Matrix products count 2 flops per multiply-add; attention counts
+# QK^T and PV (4 * L * Lk * head_dim per head); the sampler counts the bytes of one
+# read of the masked rows' logits (the bound of an HBM-bound kernel).
+def layer_work(cfg, B, L, Lk):
+    d, H, Hk, dh, F = (cfg[k] for k in ("d_model", "n_heads", "n_kv_heads", "head_dim", "d_ffn"))
+    N = B * L
+    glu = 2 if cfg["ffn_kind"] != "gelu" else 1
+    return {"qkv": 2.0 * N * d * (H + 2 * Hk) * dh, "attn": 4.0 * B * H * L * Lk * dh,
+            "oproj": 2.0 * N * H * dh * d, "ffn_up": 2.0 * N * d * F * glu, "ffn_down": 2.0 * N * F * d}
+
+
+def schedule_work(cfg, B, K):
+    work, launches = defaultdict(float), defaultdict(int)
+    d, V = cfg["d_model"], cfg["vocab"]
+    P, G, T, bl = cfg["prompt_len"], cfg["gen_len"], cfg["T"], cfg["block_len"]
+
+    def layers(count, L, Lk):
+        for name, w in layer_work(cfg, B, L, Lk).items():
+            work[name] += count * w
+            launches[name] += count
+
+    def fusion(L):
+        if cfg["fusion_kind"] == "gated_mlp":  # the paired fusion has no single-kernel stages
+            work["fusion1"] += 2.0 * B * L * (2 * d) * (5 * d)
+            work["fusion2"] += 2.0 * B * L * (4 * d) * d
+            launches["fusion1"] += 1
+            launches["fusion2"] += 1
+
+    def step(i, L, Lk):
+        ns, na, nd = cfg["n_shared"], cfg["n_anchor"], cfg["n_denoise"]
+        if (T - i) % K == 0:
+            layers(ns + na, L, Lk)
+        layers(ns + nd, L, Lk)
+        fusion(L)
+        rows = B * ((bl * i) // T)
+        work["head"] += 2.0 * rows * d * V
+        work["sample"] += 4.0 * rows * V
+        launches["head"] += 1
+        launches["sample"] += 1
+
+    all_layers = cfg["n_shared"] + cfg["n_anchor"] + cfg["n_denoise"]
+    if bl == G:
+        for i in range(T, 0, -1):
+            step(i, P + G, P + G)
+    else:
+        layers(all_layers, P, P)  # prompt prefill into the context
+        fusion(P)
+        ctx = P
+        for j in range(G // bl):
+            for i in range(T, 0, -1):
+                step(i, bl, ctx + bl)
+            if j + 1 < G // bl:  # fresh pass appending the finished block
+                layers(all_layers, bl, ctx + bl)
+                fusion(bl)
+                ctx += bl
+    return work, launches
+
+
+# Kernel groups: the stages that launch one kernel on these workloads (the attention
+# output and FFN down projections share the residual-epilogue GEMM), the bound, the
+# pattern of its rocprofv3 kernel name and the source it is built from.
+KERNELS = [
+    ("residual-epilogue GEMM (attention output + FFN down projections, bf16 MFMA)", ("oproj", "ffn_down"),
+     "mfma", r"gemm_bf16_kernel<.*EpiKind\)2>", "gemm.hip"),
+    ("FFN gate/up GEMM with GLU epilogue (bf16 MFMA)", ("ffn_up",), "mfma",
+     r"gemm_bf16_kernel<.*EpiKind\)[345]>", "gemm.hip"),
+    ("q/k/v GEMM with rotary epilogue (bf16 MFMA)", ("qkv",), "mfma", r"gemm_bf16_kernel<.*EpiKind\)13>",
+     "gemm.hip"),
+    ("attention (bf16 MFMA)", ("attn",), "mfma", r"attn_bf16_kernel", "attention.hip"),
+    ("vocabulary projection GEMM (bf16 MFMA, fp32 logits)", ("head",), "mfma",
+     r"gemm_bf16_kernel<.*EpiKind\)1>", "gemm.hip"),
+    ("fusion GEMM 1 (LN inputs -> hidden + gate, bf16 MFMA)", ("fusion1",), "mfma",
+     r"gemm_bf16_kernel<.*EpiKind\)6>", "gemm.hip"),
+    ("fusion GEMM 2 (gated residual, bf16 MFMA)", ("fusion2",), "mfma", r"gemm_bf16_kernel<.*EpiKind\)7>",
+     "gemm.hip"),
+    ("Gumbel-max sampler + confidence", ("sample",), "hbm", r"sample_kernel", "sampler.hip"),
+]
+
+
+def kernel_table(cfg, B, K, stages):
+    """Per kernel group: time per generation, launches, algorithmic work and roofline."""
+    work, launches = schedule_work(cfg, B, K)
+    out = []
+    for desc, names, bound, _, _ in KERNELS:
+        ms = sum(stages[n]["ms_per_step"] for n in names if n in stages)
+        n = sum(stages[n]["launches"] for n in names if n in stages)
+        w = sum(work[n] for n in names)
+        if not n or not w:
+            continue
+        expect = sum(launches[x] for x in names)
+        peak, unit, scale = (PEAK_BF16_TFLOPS, "TFLOP/s", 1e12) if bound == "mfma" else (PEAK_HBM_GBS, "GB/s", 1e9)
+        achieved = w / (ms / 1e3) / scale
+        out.append({"kernel": desc, "stages": list(names), "bound": bound, "ms_per_step": ms,
+                    "launches": n, "launches_expected": expect, "achieved": achieved, "peak": peak,
+                    "unit": unit, "frac": achieved / peak, "work_per_launch": w / expect})
+    return sorted(out, key=lambda r: -r["ms_per_step"])
+
+
+def source_digest(source):
+    """Hash of the sources a kernel is built from: a stored traffic figure is used only
+    while it matches."""
+    src = os.path.join(ROOT, "paper_2609_37924_amd", "csrc")
+    h = hashlib.sha256()
+    for f in ("common.h", "kernels.h", source):
+        with open(os.path.join(src, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_path(config, K):
+    return os.path.join(ROOT, "profiles", f"{config}_k{K}_hbm_traffic.md")
+
+
+TRAFFIC_LINE = re.compile(r"^traffic stage=(\S+) bytes_per_launch=(\S+) sources=(\S+)$")
+
+
+def stored_traffic(config, K, stage, source):
+    """HBM bytes per launch of a kernel from the committed counter summary of this
+    workload, or None when there is none or the kernel's sources changed since."""
+    path = traffic_path(config, K)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        for line in f:
+            mt = TRAFFIC_LINE.match(line.strip())
+            if mt and mt.group(1) == stage and mt.group(3) == source_digest(source):
+                return float(mt.group(2))
+    return None
+
+
+# ------------------------------------------------------------ profile render ---
+def short_name(n):
+    n = re.sub(r"\(tadm::GemmProblem, tadm::EpiParams\)", "", n)
+    n = n.replace("void ", "").replace("tadm::(anonymous namespace)::", "")
+    if "gemm" not in n:
+        n = re.sub(r"\(.*$", "", n)
+    n = n.replace("(tadm::EpiKind)", "epi")
+    mt = re.match(r"_ZN4tadm12_GLOBAL__N_1\d+(\w+?)(I|E)", n)
+    if mt:
+        n = mt.group(1)
+    return n[:90]
+
+
+def render_stats(d, command):
+    files = glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True)
+    rows = list(csv.DictReader(open(files[0])))
+    print("rocprofv3 `--kernel-trace --stats` summary (kernel_stats.csv, every dispatch of the run, top 16 by "
+          "total time).  Command, from the repository root on one MI355X:\n")
+    print(f"```\n{command}\n```\n")
+    print("| kernel | calls | total ms | avg us | % |\n|---|---|---|---|---|")
+    for r in rows[:16]:
+        print(f"| `{short_name(r['Name'])}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
+              f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['Percentage']):.1f} |")
+
+
+def counter_rows(d, counter):
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    return [r for r in csv.DictReader(open(files[0])) if r["Counter_Name"] == counter]
+
+
+def render_counter_summary(fetch_dir, write_dir, command):
+    """HBM traffic per dispatch from FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
+    scaled by the ratio of known bytes to the same counter on copy_kernel (one thread per
+    16 bytes, grid = bytes / 16 on these shapes) in the same run."""
+    fetch, write = counter_rows(fetch_dir, "FETCH_SIZE"), counter_rows(write_dir, "WRITE_SIZE")
+
+    def scale(rows):
+        cp = [r for r in rows if r["Kernel_Name"].startswith("tadm::(anonymous namespace)::copy_kernel(")]
+        known = sum(int(r["Grid_Size"]) * 16 for r in cp)
+        return known / (sum(float(r["Counter_Value"]) for r in cp) * 1024.0), len(cp)
+
+    sf, ncf = scale(fetch)
+    sw, ncw = scale(write)
+    per = defaultdict(lambda: [0, 0.0, 0, 0.0])
+    for r in fetch:
+        e = per[r["Kernel_Name"]]
+        e[0] += 1
+        e[1] += float(r["Counter_Value"]) * 1024.0 * sf
+    for r in write:
+        e = per[r["Kernel_Name"]]
+        e[2] += 1
+        e[3] += float(r["Counter_Value"]) * 1024.0 * sw
+    print("HBM traffic per dispatch from two rocprofv3 `--pmc` runs, FETCH_SIZE then WRITE_SIZE (KiB per "
+          "dispatch), each scaled by known bytes / counter on copy_kernel of the same run "
+          f"(FETCH x{sf:.4f} over {ncf} copies, WRITE x{sw:.4f} over {ncw} copies).  Commands, from the "
+          "repository root on one MI355X:\n")
+    print(f"```\n{command}\n```\n")
+    print("| kernel | dispatches | read MB | written MB | total MB per dispatch |\n|---|---|---|---|---|")
+    order = sorted(per.items(), key=lambda kv: -(kv[1][1] + kv[1][3]))
+    for name, (nf, bf, nw, bw) in order[:16]:
+        rd, wr = bf / max(nf, 1) / 1e6, bw / max(nw, 1) / 1e6
+        print(f"| `{short_name(name)}` | {nf} | {rd:.3f} | {wr:.3f} | {rd + wr:.3f} |")
+    print("\nPer kernel group (the lines bench.py reads; `sources` hashes the group's kernel sources):\n")
+    for desc, names, _, pat, source in KERNELS:
+        rx = re.compile(pat)
+        fk = [r for r in fetch if rx.search(r["Kernel_Name"])]
+        wk = [r for r in write if rx.search(r["Kernel_Name"])]
+        if not fk or len(fk) != len(wk):
+            continue
+        b = (sum(float(r["Counter_Value"]) for r in fk) * sf + sum(float(r["Counter_Value"]) for r in wk) * sw) \
+            * 1024.0 / len(fk)
+        print(f"    traffic stage={names[0]} bytes_per_launch={b:.0f} sources={source_digest(source)}")
+        print(f"      ({desc}: {len(fk)} dispatches, {b / 1e6:.3f} MB per launch)")
 
 
 def workload_name(cfg):
@@ -53,11 +271,13 @@ def workload_name(cfg):
             f"(block {cfg['block_len']}), T={cfg['T']}")
 
 
-def cpu_baseline(cfg, K):
-    """The oracle on one row of the workload's first block: one refresh step and one
-    stale step (the first two reverse steps), each timed, scaled to the whole job
-    (rows x blocks x (ceil(T/K) refresh steps + the other steps)).  Context prefill
-    of block mode is not part of the sample."""
+def cpu_baseline(cfg, K, budget_s=10.0):
+    """The oracle on whole rows of the workload's first block, one row at a time until
+    about budget_s seconds have passed: each row runs one refresh cycle (the first K
+    reverse steps: one refresh step, K - 1 stale steps), each step timed.  The mean
+    refresh and stale step times are scaled to the whole job: rows x blocks x
+    (ceil(T/K) refresh + the other stale steps).  Context prefill of block mode is not
+    part of the sample."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
@@ -68,41 +288,56 @@ def cpu_baseline(cfg, K):
     tensors = synth.make_weights(cfg)
     net = N.Network(N.Weights(cfg, [s[0] for s in specs], tensors))
     del tensors
-    P, G, T, bl = cfg["prompt_len"], cfg["gen_len"], cfg["T"], cfg["block_len"]
+    B, P, G, T, bl = cfg["batch"], cfg["prompt_len"], cfg["gen_len"], cfg["T"], cfg["block_len"]
     single = bl == G
     mask = synth.mask_id(cfg)
-    prompt = synth.make_prompt(cfg, batch=1).numpy()[0]
-    if single:
-        seq = np.concatenate([prompt, np.full(G, mask)])
-        pos, off, ctx = np.arange(P + G), P, None
-    else:  # first block after the prompt; the prompt context is built outside the timing
-        seq = np.full(bl, mask)
-        pos, off = np.arange(P, P + bl), 0
-        ctx = net.fresh_kv(prompt, np.arange(P))
-    times = []
-    cache = None
-    for k, refresh in enumerate((True, False)):
-        i = T - k
-        t0 = time.perf_counter()
-        c = net.shared(seq, pos, ctx)
-        if refresh:
-            cache = net.anchor_cache(c, pos, ctx)
-        xf = net.denoise(net.fuse(c, cache), pos, ctx)
-        lg = net.head(xf[off:]).astype(np.float32)
-        seq[off:], _, _ = S.reverse_step(lg, seq[off:], mask, loop.unmask_count(bl, i, T),
-                                         pos[0] + off, 0, T - i, 2, np.float32(1.0))
-        times.append(time.perf_counter() - t0)
+    prompts = synth.make_prompt(cfg).numpy() if P else np.zeros((B, 0), dtype=np.int64)
+    t_ref, t_stale = [], []
+    t_start = time.perf_counter()
+    rows = 0
+    for r in range(B):
+        if single:
+            seq = np.concatenate([prompts[r], np.full(G, mask)])
+            pos, off, ctx = np.arange(P + G), P, None
+        else:  # first block after the prompt; the prompt context is built outside the timing
+            seq = np.full(bl, mask)
+            pos, off = np.arange(P, P + bl), 0
+            ctx = net.fresh_kv(prompts[r], np.arange(P))
+        cache = None
+        for k in range(min(K, T)):
+            i = T - k
+            t0 = time.perf_counter()
+            c = net.shared(seq, pos, ctx)
+            if k == 0:
+                cache = net.anchor_cache(c, pos, ctx)
+            xf = net.denoise(net.fuse(c, cache), pos, ctx)
+            lg = net.head(xf[off:]).astype(np.float32)
+            seq[off:], _, _ = S.reverse_step(lg, seq[off:], mask, loop.unmask_count(bl, i, T), pos[0] + off, r,
+                                             T - i, cfg["sampler_seed"], np.float32(1.0))
+            (t_ref if k == 0 else t_stale).append(time.perf_counter() - t0)
+        rows += 1
+        if time.perf_counter() - t_start >= budget_s:
+            break
+    tr = float(np.mean(t_ref))
+    ts = float(np.mean(t_stale)) if t_stale else tr
     n_ref = math.ceil(T / K)
-    job_s = cfg["batch"] * (G // bl) * (n_ref * times[0] + (T - n_ref) * times[1])
+    job_s = B * (G // bl) * (n_ref * tr + (T - n_ref) * ts)
     threads = max([t.get("num_threads", 1) for t in threadpool_info()] + [1])
-    return {"value": cfg["batch"] * G / job_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"1 of {cfg['batch']} rows, first block: one refresh step ({times[0]:.1f} s) and one "
-                      f"stale step ({times[1]:.1f} s) at the full shape; scaled to rows x blocks x "
-                      f"({n_ref} refresh + {T - n_ref} stale steps) per block, context prefill excluded"}
+    return {"value": B * G / job_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{rows} of {B} rows, first block, one refresh cycle each (1 refresh step, mean "
+                      f"{tr:.2f} s; {min(K, T) - 1} stale steps, mean {ts:.2f} s) at the full shape, "
+                      f"{time.perf_counter() - t_start:.1f} s in all; scaled to rows x blocks x ({n_ref} refresh + "
+                      f"{T - n_ref} stale steps) per block, context prefill excluded"}
 
 
 def main():
     args = parse()
+    if args.render_stats:
+        render_stats(args.render_stats, args.command)
+        return
+    if args.render_counters:
+        render_counter_summary(*args.render_counters, args.command)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build runs the path on a single MI355X "
               "(multi-GPU sharding is design only).", file=sys.stderr)
@@ -132,18 +367,22 @@ def main():
     def gen(K):
         tadm.tadm_generate(m, prompt, B, P, G, T, K, bl, cfg["sampler_seed"], cfg["temperature"], out)
 
-    def timed(K, steps, warmup, profile=0):
-        """profile: stage bit mask recorded with HIP events inside the timed region."""
+    def timed(K, steps, warmup, profile=0, profiled_steps=None):
+        """Time `steps` generations.  profile: stage bit mask timed during the last
+        `profiled_steps` of them (all by default); the timers add GPU time per timed
+        launch, so the headline pass times only its last generation's dominant kernel."""
+        profiled_steps = steps if profiled_steps is None else profiled_steps
         for _ in range(warmup):
             gen(K)
         torch.cuda.synchronize()
         tadm.tadm_profile_reset(m)
-        tadm.tadm_profile_enable(m, profile)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         e0.record(stream)
-        for _ in range(steps):
+        for k in range(steps):
+            if k == steps - profiled_steps:
+                tadm.tadm_profile_enable(m, profile)
             gen(K)
         e1.record(stream)
         torch.cuda.synchronize()
@@ -155,19 +394,26 @@ def main():
             for si, name in enumerate(tadm.STAGES):
                 tot, n = tadm.tadm_profile_read(m, si)
                 if n:
-                    stages[name] = {"ms_per_step": tot / steps, "launches": n // steps, "avg_ms": tot / n}
+                    stages[name] = {"ms_per_step": tot / profiled_steps, "launches": n // profiled_steps,
+                                    "avg_ms": tot / n}
         return ms, wall / steps * 1e3, stages
 
     K0 = args.K
-    print(f"[bench] {workload_name(cfg)}", file=sys.stderr, flush=True)
-    head_bit = 1 << tadm.STAGES.index("head")
-    ms, wall_ms, head_only = timed(K0, args.steps, args.warmup, profile=head_bit)
     tokens = B * G
+    print(f"[bench] {workload_name(cfg)}", file=sys.stderr, flush=True)
+    # 1. per-stage breakdown (HIP events around every stage, so a pass of its own)
+    _, _, stages = timed(K0, max(1, args.steps // 2), args.warmup, profile=-1)
+    kernels = kernel_table(cfg, B, K0, stages)
+    for k in kernels:
+        print(f"[bench]   {k['ms_per_step']:8.3f} ms  {k['achieved']:8.1f} {k['unit']:7s} ({100 * k['frac']:.1f}% "
+              f"of peak)  {k['launches']} launches  {k['kernel']}", file=sys.stderr, flush=True)
+    # 2. headline; the dominant kernel's launches of the last generation carry timers
+    dom = kernels[0] if kernels else None
+    mask = sum(1 << tadm.STAGES.index(n) for n in dom["stages"]) if dom else 0
+    ms, wall_ms, dom_stages = timed(K0, args.steps, 1, profile=mask, profiled_steps=1)
     value = tokens / (ms / 1e3)
     print(f"[bench] K={K0}: {ms:.3f} ms/generation ({wall_ms:.3f} wall) -> {value:.1f} tokens/s",
           file=sys.stderr, flush=True)
-    # stage breakdown from a separate pass (events around every stage perturb timing)
-    _, _, stages = timed(K0, max(1, args.steps // 2), 0, profile=-1)
     sweep = {}
     if not args.no_sweep:
         for K in cfg["Ks"]:
@@ -175,15 +421,17 @@ def main():
             sweep[f"K={K}"] = {"tokens_per_s": tokens / (kms / 1e3), "ms_per_step": kms}
             print(f"[bench] K={K}: {kms:.3f} ms -> {tokens / (kms / 1e3):.1f} tokens/s", file=sys.stderr,
                   flush=True)
-    head = head_only.get("head")
     roof = None
-    if head:
-        flops = head_flops(cfg, B)
-        achieved = flops / (head["avg_ms"] / 1e3) / 1e12
-        roof = {"kernel": "vocabulary projection GEMM (bf16 MFMA, fp32 logits)", "bound": "mfma",
-                "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
-                "avg_launch_ms": head["avg_ms"], "flops_per_launch": flops}
+    if dom:
+        live = kernel_table(cfg, B, K0, dom_stages)[0]
+        source = next(k[4] for k in KERNELS if k[0] == dom["kernel"])
+        traffic = stored_traffic(args.config, K0, dom["stages"][0], source)
+        avg_ms = live["ms_per_step"] / live["launches"]
+        roof = {"kernel": live["kernel"], "bound": live["bound"], "achieved": live["achieved"],
+                "peak": live["peak"], "unit": live["unit"], "frac": live["frac"], "traffic": traffic,
+                "avg_launch_ms": avg_ms, "launches_per_step": live["launches"],
+                "timed_in": "the last generation of the headline timed region",
+                ("flops_per_launch" if live["bound"] == "mfma" else "bytes_per_launch"): live["work_per_launch"]}
     cpu = None
     if not args.no_cpu:
         try:
@@ -200,6 +448,7 @@ def main():
                    "parallelism": "none (1 GPU)"},
         "k_sweep": sweep,
         "stages_ms_per_step": {k: v["ms_per_step"] for k, v in stages.items()},
+        "kernels": [{k: v for k, v in r.items() if k != "stages"} for r in kernels],
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -176,14 +176,22 @@ enum { TADM_TAP_EMBED = 0, TADM_TAP_FUSED = 1, TADM_TAP_FINAL = 2 };
 tadm_status tadm_debug_taps(tadm_model* m, int32_t enable);
 tadm_status tadm_debug_read(tadm_model* m, int32_t tap, float* dst_dev, size_t bytes);
 
-/* Per-stage timing with HIP events recorded on the model stream around each
- * stage whose bit is set in stage_mask (bit s = stage s; 0 = off, -1 = all);
- * read synchronises the stream.  TADM_STAGE_HEAD brackets exactly one kernel, the
- * vocabulary projection.  Stage ids: */
+/* Per-stage timing on the model stream for each stage whose bit is set in stage_mask
+ * (bit s = stage s; 0 = off, -1 = all).  Stages nest.  A single-kernel stage (HEAD,
+ * SAMPLE and QKV..FUSION2; with fp32 weights FFN_UP times its GEMM only) hands a pair of
+ * events to its kernel launch (hipExtLaunchKernel), which stamps the kernel's own start
+ * and end and adds nothing to the stream; the other stages record events before and
+ * after their launches.  read synchronises the stream and sums the intervals recorded
+ * since the last reset; reset also drops stages left open by a failed call.  Stage ids: */
 enum {
   TADM_STAGE_EMBED = 0, TADM_STAGE_ANCHOR = 1, TADM_STAGE_FUSION = 2, TADM_STAGE_DENOISE = 3,
   TADM_STAGE_HEAD = 4, TADM_STAGE_SAMPLE = 5, TADM_STAGE_SELECT = 6, TADM_STAGE_CONTEXT = 7,
-  TADM_STAGE_COUNT = 8
+  /* single-kernel stages inside the layers and the gated-MLP fusion (every layer of
+   * every pass): q/k/v projection (with rotary epilogue), attention, output projection,
+   * feed-forward up (gate+up) and down projections, fusion GEMM 1 and 2 */
+  TADM_STAGE_QKV = 8, TADM_STAGE_ATTN = 9, TADM_STAGE_OPROJ = 10, TADM_STAGE_FFN_UP = 11,
+  TADM_STAGE_FFN_DOWN = 12, TADM_STAGE_FUSION1 = 13, TADM_STAGE_FUSION2 = 14,
+  TADM_STAGE_COUNT = 15
 };
 tadm_status tadm_profile_enable(tadm_model* m, int32_t stage_mask);
 tadm_status tadm_profile_read(tadm_model* m, int32_t stage, double* total_ms, int64_t* count);

@@ -25,7 +25,8 @@ FFN = {"gelu": 0, "swiglu": 1, "geglu": 2}
 FUSION = {"gated_mlp": 0, "paired": 1}
 CACHE_H, CACHE_C, CACHE_A = 0, 1, 2
 TAP_EMBED, TAP_FUSED, TAP_FINAL = 0, 1, 2
-STAGES = ["embed", "anchor", "fusion", "denoise", "head", "sample", "select", "context"]
+STAGES = ["embed", "anchor", "fusion", "denoise", "head", "sample", "select", "context",
+          "qkv", "attn", "oproj", "ffn_up", "ffn_down", "fusion1", "fusion2"]
 
 
 class tadm_config(C.Structure):

@@ -262,22 +262,21 @@ hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, voi
     const dim3 grid((Lq + 63) / 64, H, B);
     const float sl2 = 1.4426950408889634f / sqrtf((float)dh);
     if (dh == 64)
-      hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
-                         static_cast<const bf16*>(K), static_cast<const bf16*>(Vt), static_cast<bf16*>(O),
-                         H, Hkv, Lq, Lk, kv_cap, sl2);
+      launch_timed(attn_bf16_kernel<64>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
+                   static_cast<const bf16*>(K), static_cast<const bf16*>(Vt), static_cast<bf16*>(O), H, Hkv, Lq,
+                   Lk, kv_cap, sl2);
     else if (dh == 128)
-      hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
-                         static_cast<const bf16*>(K), static_cast<const bf16*>(Vt), static_cast<bf16*>(O),
-                         H, Hkv, Lq, Lk, kv_cap, sl2);
+      launch_timed(attn_bf16_kernel<128>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
+                   static_cast<const bf16*>(K), static_cast<const bf16*>(Vt), static_cast<bf16*>(O), H, Hkv, Lq,
+                   Lk, kv_cap, sl2);
     else
       return hipErrorInvalidValue;
     return hipGetLastError();
   }
   const dim3 grid((Lq + 3) / 4, H, B);
-  hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(256), 4 * Lk * sizeof(float), s,
-                     static_cast<const float*>(Q), static_cast<const float*>(K),
-                     static_cast<const float*>(Vt), static_cast<float*>(O), H, Hkv, Lq, Lk, kv_cap, dh,
-                     1.f / sqrtf((float)dh));
+  launch_timed(attn_f32_kernel, grid, dim3(256), (uint32_t)(4 * Lk * sizeof(float)), s,
+               static_cast<const float*>(Q), static_cast<const float*>(K), static_cast<const float*>(Vt),
+               static_cast<float*>(O), H, Hkv, Lq, Lk, kv_cap, dh, 1.f / sqrtf((float)dh));
   return hipGetLastError();
 }
 

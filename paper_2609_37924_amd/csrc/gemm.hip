@@ -401,8 +401,8 @@ hipError_t launch_bf16(const GemmProblem& p0, const EpiParams& e, hipStream_t s)
   GemmProblem p = p0;
   const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
   xcd_regions(tiles_m, tiles_n, BM, BN, p.rm, p.rn);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, ST, WGM, WGN, MINB, K>), dim3(tiles_m * tiles_n),
-                     dim3(64 * WGM * WGN), 0, s, p, e);
+  launch_timed(gemm_bf16_kernel<BM, BN, ST, WGM, WGN, MINB, K>, dim3(tiles_m * tiles_n), dim3(64 * WGM * WGN),
+               0, s, p, e);
   return hipGetLastError();
 }
 
@@ -410,7 +410,7 @@ template <EpiKind K>
 hipError_t dispatch(DType dt, const GemmProblem& p, const EpiParams& e, hipStream_t s) {
   if (dt == F32) {
     const int tiles = ((p.M + 63) / 64) * ((p.N + 63) / 64);
-    hipLaunchKernelGGL(gemm_f32_kernel<K>, dim3(tiles), dim3(256), 0, s, p, e);
+    launch_timed(gemm_f32_kernel<K>, dim3(tiles), dim3(256), 0, s, p, e);
     return hipGetLastError();
   }
   // tile choice by how many blocks each shape yields (256 CUs): GEMMs with many rows

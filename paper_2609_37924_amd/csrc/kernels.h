@@ -2,9 +2,28 @@
 // return the launch status; shapes are validated by the caller (runtime.cpp).
 #pragma once
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stdint.h>
 
 namespace tadm {
+
+// Start/stop events for the next timed launch made on this host thread (null: untimed).
+// The events take the dispatch's own begin and end timestamps (hipExtLaunchKernel), so
+// timing a kernel adds no packets to the stream.  The launch consumes them.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern thread_local LaunchEvents next_launch_events;
+
+template <typename F, typename... Args>
+inline void launch_timed(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
+  const LaunchEvents ev = next_launch_events;
+  next_launch_events = LaunchEvents{};
+  if (ev.start)
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, ev.start, ev.stop, 0u, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+}
 
 enum DType { F32 = 0, BF16 = 1 };
 

@@ -19,6 +19,8 @@
 
 using namespace tadm;
 
+thread_local tadm::LaunchEvents tadm::next_launch_events;
+
 // ------------------------------------------------------------------ errors ----
 static thread_local std::string g_err;
 
@@ -241,6 +243,11 @@ struct ProfRec {
   hipEvent_t a, b;
 };
 
+struct OpenStage {
+  int stage;
+  hipEvent_t a, b;  // b is set for a single-kernel stage: both events ride on its launch
+};
+
 struct tadm_model {
   tadm_config cfg;
   DType dt;
@@ -264,8 +271,7 @@ struct tadm_model {
   int32_t prof_mask = 0;  // bit s: record stage s
   std::vector<ProfRec> recs;
   std::vector<hipEvent_t> pool;
-  int cur_stage = -1;
-  hipEvent_t cur_ev = nullptr;
+  std::vector<OpenStage> open;  // stages begun and not yet ended
 
   void* W(int t) const { return arena + lay.tensors[t].off; }
   float* Wf(int t) const { return reinterpret_cast<float*>(arena + lay.tensors[t].off); }
@@ -290,37 +296,55 @@ struct tadm_context {
 };
 
 // ---------------------------------------------------------------- profiling ---
+static tadm_status prof_event(tadm_model* m, hipEvent_t* e) {
+  if (m->pool.empty()) {
+    HIPCHK(hipEventCreate(e));
+  } else {
+    *e = m->pool.back();
+    m->pool.pop_back();
+  }
+  return TADM_OK;
+}
+
+// A single-kernel stage times its first launch with the launch's own timestamps;
+// the other stages bracket their launches with recorded events.
+static bool single_kernel_stage(int stage) {
+  return stage == TADM_STAGE_HEAD || stage == TADM_STAGE_SAMPLE || stage >= TADM_STAGE_QKV;
+}
+
+// Stages nest (a kernel stage inside a layer stage); each end closes the latest begin.
 static tadm_status prof_begin(tadm_model* m, int stage) {
   if (!((m->prof_mask >> stage) & 1)) return TADM_OK;
-  hipEvent_t e;
-  if (m->pool.empty()) {
-    HIPCHK(hipEventCreate(&e));
+  OpenStage o{stage, nullptr, nullptr};
+  TRY(prof_event(m, &o.a));
+  if (single_kernel_stage(stage)) {
+    TRY(prof_event(m, &o.b));
+    next_launch_events = LaunchEvents{o.a, o.b};
   } else {
-    e = m->pool.back();
-    m->pool.pop_back();
+    HIPCHK(hipEventRecord(o.a, m->stream));
   }
-  HIPCHK(hipEventRecord(e, m->stream));
-  m->cur_stage = stage;
-  m->cur_ev = e;
+  m->open.push_back(o);
   return TADM_OK;
 }
 
-static tadm_status prof_end(tadm_model* m) {
-  if (m->cur_stage < 0) return TADM_OK;
-  hipEvent_t e;
-  if (m->pool.empty()) {
-    HIPCHK(hipEventCreate(&e));
+static tadm_status prof_end(tadm_model* m, int stage) {
+  if (!((m->prof_mask >> stage) & 1) || m->open.empty() || m->open.back().stage != stage) return TADM_OK;
+  OpenStage o = m->open.back();
+  m->open.pop_back();
+  if (o.b) {
+    if (next_launch_events.start == o.a) {  // nothing was launched: an empty interval
+      next_launch_events = LaunchEvents{};
+      HIPCHK(hipEventRecord(o.a, m->stream));
+      HIPCHK(hipEventRecord(o.b, m->stream));
+    }
   } else {
-    e = m->pool.back();
-    m->pool.pop_back();
+    TRY(prof_event(m, &o.b));
+    HIPCHK(hipEventRecord(o.b, m->stream));
   }
-  HIPCHK(hipEventRecord(e, m->stream));
-  m->recs.push_back(ProfRec{m->cur_stage, m->cur_ev, e});
-  m->cur_stage = -1;
+  m->recs.push_back(ProfRec{stage, o.a, o.b});
   return TADM_OK;
 }
 
-// ---------------------------------------------------------------- workspace ---
 static tadm_status ws_alloc(tadm_model* m, void** p, size_t bytes) {
   HIPCHK(hipMalloc(p, std::max<size_t>(bytes, 256)));
   m->ws.allocs.push_back(*p);
@@ -410,17 +434,24 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
     e.q = s.q;
     e.k = kv.k;
     e.vt = kv.vt;
+    TRY(prof_begin(m, TADM_STAGE_QKV));
     HIPCHK(gemm(m->dt, p, EPI_QKV_ROPE, e, st));
+    TRY(prof_end(m, TADM_STAGE_QKV));
   }
+  TRY(prof_begin(m, TADM_STAGE_ATTN));
   HIPCHK(attention(m->dt, s.q, kv.k, kv.vt, s.ao, B, H, Hk, L, kv.off + L, kv.cap, dh, st));
+  TRY(prof_end(m, TADM_STAGE_ATTN));
   {
     GemmProblem p{N, d, H * dh, s.ao, H * dh, H * dh, nullptr, 0, m->W(w.wo), H * dh};
     EpiParams e;
     e.resid = x;
     e.ldr = d;
+    TRY(prof_begin(m, TADM_STAGE_OPROJ));
     HIPCHK(gemm(m->dt, p, EPI_RESID, e, st));
+    TRY(prof_end(m, TADM_STAGE_OPROJ));
   }
   HIPCHK(rms_norm(m->dt, x, m->Wf(w.ffn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
+  TRY(prof_begin(m, TADM_STAGE_FFN_UP));
   if (c.ffn_kind == TADM_FFN_GELU) {
     GemmProblem p{N, F, d, s.xn, d, d, nullptr, 0, m->W(w.wup), d};
     EpiParams e;
@@ -441,12 +472,15 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
     HIPCHK(gemm(m->dt, p, EPI_STORE_F32, e, st));
     HIPCHK(glu_f32(s.ffn_pre, N, F, c.ffn_kind == TADM_FFN_SWIGLU, (float*)s.ffn, st));
   }
+  TRY(prof_end(m, TADM_STAGE_FFN_UP));
   {
     GemmProblem p{N, d, F, s.ffn, F, F, nullptr, 0, m->W(w.wdown), F};
     EpiParams e;
     e.resid = x;
     e.ldr = d;
+    TRY(prof_begin(m, TADM_STAGE_FFN_DOWN));
     HIPCHK(gemm(m->dt, p, EPI_RESID, e, st));
+    TRY(prof_end(m, TADM_STAGE_FFN_DOWN));
   }
   return TADM_OK;
 }
@@ -633,7 +667,9 @@ static tadm_status fusion(tadm_model* m, int B, int L, const float* c, const tad
     e.out2 = s.fus_g;
     e.ldo2 = d;
     e.split = 4 * d;
+    TRY(prof_begin(m, TADM_STAGE_FUSION1));
     HIPCHK(gemm(m->dt, p, EPI_FUSION1, e, st));
+    TRY(prof_end(m, TADM_STAGE_FUSION1));
   }
   {
     GemmProblem p{N, d, 4 * d, s.fus_h, 4 * d, 4 * d, nullptr, 0, m->W(Y.w2), 4 * d};
@@ -645,7 +681,9 @@ static tadm_status fusion(tadm_model* m, int B, int L, const float* c, const tad
     e.ld_aux = d;
     e.gate = s.fus_g;
     e.ldg = d;
+    TRY(prof_begin(m, TADM_STAGE_FUSION2));
     HIPCHK(gemm(m->dt, p, EPI_FUSION2, e, st));
+    TRY(prof_end(m, TADM_STAGE_FUSION2));
   }
   HIPCHK(layer_norm(m->dt, s.x, m->Wf(Y.ln_o_w), m->Wf(Y.ln_o_b), cf.ln_eps, N, d, nullptr, s.x, st));
   return TADM_OK;
@@ -805,6 +843,11 @@ tadm_status tadm_model_destroy(tadm_model* m) {
   if (m->arena) (void)hipFree(m->arena);
   if (m->rope_cos) (void)hipFree(m->rope_cos);
   if (m->rope_sin) (void)hipFree(m->rope_sin);
+  next_launch_events = LaunchEvents{};
+  for (auto& o : m->open) {
+    (void)hipEventDestroy(o.a);
+    if (o.b) (void)hipEventDestroy(o.b);
+  }
   for (auto& r : m->recs) {
     (void)hipEventDestroy(r.a);
     (void)hipEventDestroy(r.b);
@@ -958,7 +1001,7 @@ tadm_status tadm_context_append(tadm_model* m, tadm_context* ctx, const int32_t*
   TRY(ensure_scratch(m));
   TRY(prof_begin(m, TADM_STAGE_CONTEXT));
   TRY(context_append_impl(m, ctx, tokens_dev, B, n, m->scratch));
-  return prof_end(m);
+  return prof_end(m, TADM_STAGE_CONTEXT);
 }
 
 // ------------------------------------------------------------------ step ----
@@ -966,10 +1009,10 @@ static tadm_status anchor_impl(tadm_model* m, const tadm_context* ctx, const int
                                int L, int i, tadm_cache* cache) {
   TRY(prof_begin(m, TADM_STAGE_EMBED));
   TRY(shared_net(m, ctx, canvas, B, L, m->ws.c));
-  TRY(prof_end(m));
+  TRY(prof_end(m, TADM_STAGE_EMBED));
   TRY(prof_begin(m, TADM_STAGE_ANCHOR));
   TRY(anchor_net(m, ctx, B, L, m->ws.c, cache));
-  TRY(prof_end(m));
+  TRY(prof_end(m, TADM_STAGE_ANCHOR));
   cache->refresh_i = i;
   return TADM_OK;
 }
@@ -993,10 +1036,10 @@ static tadm_status sample_impl(tadm_model* m, const float* logits, const int32_t
   TRY(prof_begin(m, TADM_STAGE_SAMPLE));
   HIPCHK(sample_tokens(logits, row_map, canvas, B, L, off, m->cfg.vocab, mask, pos0, a->step_id, a->seed,
                        a->inv_temp, choice, conf, m->stream));
-  TRY(prof_end(m));
+  TRY(prof_end(m, TADM_STAGE_SAMPLE));
   TRY(prof_begin(m, TADM_STAGE_SELECT));
   HIPCHK(select_unmask(canvas, choice, conf, B, L, off, mask, a->n_unmask, next, m->stream));
-  TRY(prof_end(m));
+  TRY(prof_end(m, TADM_STAGE_SELECT));
   return TADM_OK;
 }
 
@@ -1011,10 +1054,10 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
   const int pos0 = ctx ? ctx->len : 0, Lc = L - off, d = cf.d_model;
   TRY(prof_begin(m, TADM_STAGE_EMBED));
   TRY(shared_net(m, ctx, canvas, B, L, s.c));
-  TRY(prof_end(m));
+  TRY(prof_end(m, TADM_STAGE_EMBED));
   TRY(prof_begin(m, TADM_STAGE_FUSION));
   TRY(fusion(m, B, L, s.c, cache));
-  TRY(prof_end(m));
+  TRY(prof_end(m, TADM_STAGE_FUSION));
   if (m->taps) HIPCHK(copy_f32(s.x, s.ht, (size_t)B * L * d, m->stream));
   const bool full = logits != nullptr;
   const int rows = full ? B * Lc : std::min(max_masked, B * Lc);
@@ -1027,7 +1070,7 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
     HIPCHK(rms_norm_gather(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, s.cidx, s.count, rows, Lc, L,
                            off, d, s.xn, m->stream));
   }
-  TRY(prof_end(m));
+  TRY(prof_end(m, TADM_STAGE_DENOISE));
   if (!full) {
     TRY(ensure_logits(m, (size_t)B * Lc * cf.vocab));
     logits = s.logits;
@@ -1041,7 +1084,7 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
     e.ldo = cf.vocab;
     HIPCHK(gemm(m->dt, p, EPI_STORE_F32, e, m->stream));
   }
-  TRY(prof_end(m));
+  TRY(prof_end(m, TADM_STAGE_HEAD));
   m->tap_B = B;
   m->tap_L = L;
   m->tap_Lc = Lc;
@@ -1131,7 +1174,7 @@ tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, i
   int32_t* win = m->gwin;
   TRY(prof_begin(m, TADM_STAGE_CONTEXT));
   TRY(context_append_impl(m, ctx, prompt_dev, B, P, m->scratch));
-  TRY(prof_end(m));
+  TRY(prof_end(m, TADM_STAGE_CONTEXT));
   const int nblocks = gen_len / block_len;
   for (int j = 0; j < nblocks; ++j) {
     HIPCHK(fill_i32(win, (size_t)B * block_len, mask, m->stream));
@@ -1148,7 +1191,7 @@ tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, i
     if (j + 1 < nblocks) {
       TRY(prof_begin(m, TADM_STAGE_CONTEXT));
       TRY(context_append_impl(m, ctx, win, B, block_len, m->scratch));
-      TRY(prof_end(m));
+      TRY(prof_end(m, TADM_STAGE_CONTEXT));
     }
   }
   return TADM_OK;
@@ -1201,6 +1244,12 @@ tadm_status tadm_profile_reset(tadm_model* m) {
     m->pool.push_back(r.b);
   }
   m->recs.clear();
+  for (auto& o : m->open) {  // left open by a call that failed mid-stage
+    m->pool.push_back(o.a);
+    if (o.b) m->pool.push_back(o.b);
+  }
+  m->open.clear();
+  next_launch_events = LaunchEvents{};
   return TADM_OK;
 }
 

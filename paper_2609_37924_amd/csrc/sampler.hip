@@ -359,11 +359,11 @@ hipError_t sample_tokens(const float* logits, const int32_t* row_map, const int3
   const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
   const dim3 grid(Lc, B);
   if (V % 4 == 0)
-    hipLaunchKernelGGL(sample_kernel<true>, grid, dim3(256), 0, s, logits, row_map, canvas, L, canvas_off, Lc, V,
-                       mask_id, pos0, step_id, k0, k1, inv_temp, choice, conf);
+    launch_timed(sample_kernel<true>, grid, dim3(256), 0, s, logits, row_map, canvas, L, canvas_off, Lc, V, mask_id,
+                 pos0, step_id, k0, k1, inv_temp, choice, conf);
   else
-    hipLaunchKernelGGL(sample_kernel<false>, grid, dim3(256), 0, s, logits, row_map, canvas, L, canvas_off, Lc,
-                       V, mask_id, pos0, step_id, k0, k1, inv_temp, choice, conf);
+    launch_timed(sample_kernel<false>, grid, dim3(256), 0, s, logits, row_map, canvas, L, canvas_off, Lc, V,
+                 mask_id, pos0, step_id, k0, k1, inv_temp, choice, conf);
   return hipGetLastError();
 }
 

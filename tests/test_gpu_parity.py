@@ -229,6 +229,46 @@ def test_tiny_paired_generation_matches_oracle():
     np.testing.assert_array_equal(got, ref)
 
 
+def test_block_mode_bf16_step_parity():
+    """Block diffusion with GQA at bf16: the prompt is prefilled into the context KV
+    (a fresh pass through every layer), then a refresh and a stale step run on the
+    active block attending to [context | block] (App. C.1 encoder/decoder split)."""
+    cfg = synth.get_config("block", d_model=512, n_heads=8, n_kv_heads=2, head_dim=64, d_ffn=1024,
+                           n_anchor=2, n_denoise=2, vocab=4096, batch=2, prompt_len=70, gen_len=128,
+                           block_len=64)
+    B, P, bl = 2, cfg["prompt_len"], cfg["block_len"]
+    tensors = synth.make_weights(cfg, perturb=True)
+    net = oracle_net(cfg, tensors)
+    m = gpu_model(cfg, tensors, B, P + cfg["gen_len"])
+    try:
+        ctx = tadm.tadm_context_create(m, B, P + cfg["gen_len"])
+        prompt = synth.make_prompt(cfg, batch=B)
+        tadm.tadm_context_append(m, ctx, prompt.to(dev()), B, P)
+        assert tadm.tadm_context_length(ctx) == P
+        g = torch.Generator().manual_seed(3)
+        z0 = torch.full((B, bl), cfg["vocab"], dtype=torch.int32)
+        z1 = torch.randint(0, cfg["vocab"], (B, bl), generator=g, dtype=torch.int32)
+        z1[torch.rand(B, bl, generator=g) < 0.6] = cfg["vocab"]
+        cache = tadm.tadm_cache_create(m, B, bl)
+        tadm.tadm_anchor_forward(m, ctx, z0.to(dev()), B, bl, 8, 8, cache)
+        args = tadm.step_args(6, 8, 5, 2, 4, 1.0)
+        logits = torch.empty(B, bl, cfg["vocab"], device=dev())
+        nxt = torch.empty(B, bl, dtype=torch.int32, device=dev())
+        tadm.tadm_denoise_step(m, ctx, z1.to(dev()), B, bl, 0, cache, args, logits, nxt)
+        sync()
+        pos = np.arange(P, P + bl)
+        for b in range(B):
+            kv = net.fresh_kv(prompt[b].numpy(), np.arange(P))
+            cache_ref = net.anchor_cache(net.shared(z0[b].numpy(), pos, kv), pos, kv)
+            c = net.shared(z1[b].numpy(), pos, kv)
+            xf = net.denoise(net.fuse(c, cache_ref), pos, kv)
+            rows_close(logits[b].cpu().numpy(), net.head(xf), what=f"block logits row {b}", **BF16_TOL)
+        tadm.tadm_cache_destroy(cache)
+        tadm.tadm_context_destroy(ctx)
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
 # -------------------------------------------------------------- generation
 def _generate(cfg, K, block_len=None, B=None):
     B = B or cfg["batch"]
@@ -353,5 +393,39 @@ def test_state_errors():
             tadm.tadm_anchor_forward(m, None, z, 2, 32, 1, 4, cache)
         assert e.value.status == tadm.TADM_ERR_INVALID
         tadm.tadm_cache_destroy(cache)
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
+def test_profile_stages_count_every_launch():
+    """Stage timers: one interval per launch of each single-kernel stage over a whole
+    generation (refresh iff (T - i) mod K == 0), each positive, nested inside its layer
+    stages."""
+    cfg = synth.get_config("tiny", batch=2)
+    K, T = 4, cfg["T"]
+    tensors = synth.make_weights(cfg)
+    P, G = cfg["prompt_len"], cfg["gen_len"]
+    m = gpu_model(cfg, tensors, 2, P + G)
+    try:
+        prompt = synth.make_prompt(cfg, batch=2).to(dev())
+        out = torch.empty(2, P + G, dtype=torch.int32, device=dev())
+        tadm.tadm_profile_reset(m)
+        tadm.tadm_profile_enable(m, -1)
+        tadm.tadm_generate(m, prompt, 2, P, G, T, K, G, 2, 1.0, out)
+        tadm.tadm_profile_enable(m, 0)
+        got = {name: tadm.tadm_profile_read(m, si) for si, name in enumerate(tadm.STAGES)}
+        n_ref = -(-T // K)
+        per_layer = n_ref * (cfg["n_shared"] + cfg["n_anchor"]) + T * (cfg["n_shared"] + cfg["n_denoise"])
+        expect = {"qkv": per_layer, "attn": per_layer, "oproj": per_layer, "ffn_up": per_layer,
+                  "ffn_down": per_layer, "fusion1": T, "fusion2": T, "head": T, "sample": T, "select": T,
+                  "anchor": n_ref, "denoise": T}
+        for name, n in expect.items():
+            tot, cnt = got[name]
+            assert cnt == n, (name, cnt, n)
+            assert tot > 0, name
+        inner = sum(got[n][0] for n in ("qkv", "attn", "oproj", "ffn_up", "ffn_down"))
+        assert inner <= got["anchor"][0] + got["denoise"][0] + 1e-3
+        tadm.tadm_profile_reset(m)
+        assert tadm.tadm_profile_read(m, tadm.STAGES.index("head")) == (0.0, 0)
     finally:
         tadm.tadm_model_destroy(m)
