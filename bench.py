@@ -94,7 +94,9 @@ def schedule_work(cfg, B, K):
         fusion(L)
         rows = B * ((bl * i) // T)
         work["head"] += 2.0 * rows * d * V
-        work["sample"] += 4.0 * rows * V
+        # bf16: the head samples in its epilogue and the sampler stage merges one
+        # 24-byte partial per (row, 64-entry group); fp32: the sampler reads the logits
+        work["sample"] += rows * (24.0 * -(-V // 64) if cfg["dtype"] == "bf16" else 4.0 * V)
         launches["head"] += 1
         launches["sample"] += 1
 
@@ -127,13 +129,14 @@ KERNELS = [
     ("q/k/v GEMM with rotary epilogue (bf16 MFMA)", ("qkv",), "mfma", r"gemm_bf16_kernel<.*EpiKind\)13>",
      "gemm.hip"),
     ("attention (bf16 MFMA)", ("attn",), "mfma", r"attn_bf16_kernel", "attention.hip"),
-    ("vocabulary projection GEMM (bf16 MFMA, fp32 logits)", ("head",), "mfma",
-     r"gemm_bf16_kernel<.*EpiKind\)1>", "gemm.hip"),
+    ("vocabulary projection with the sampling epilogue (bf16 MFMA + Gumbel-max/normaliser partials)", ("head",),
+     "mfma", r"gemm_bf16_kernel<.*EpiKind\)14>", "head_sample.hip"),
     ("fusion GEMM 1 (LN inputs -> hidden + gate, bf16 MFMA)", ("fusion1",), "mfma",
      r"gemm_bf16_kernel<.*EpiKind\)6>", "gemm.hip"),
     ("fusion GEMM 2 (gated residual, bf16 MFMA)", ("fusion2",), "mfma", r"gemm_bf16_kernel<.*EpiKind\)7>",
      "gemm.hip"),
-    ("Gumbel-max sampler + confidence", ("sample",), "hbm", r"sample_kernel", "sampler.hip"),
+    ("sampler finalize: merge of the group partials into token + confidence", ("sample",), "hbm",
+     r"finalize_kernel", "head_sample.hip"),
 ]
 
 
@@ -161,7 +164,7 @@ def source_digest(source):
     while it matches."""
     src = os.path.join(ROOT, "paper_2609_37924_amd", "csrc")
     h = hashlib.sha256()
-    for f in ("common.h", "kernels.h", source):
+    for f in ("common.h", "kernels.h", "gemm_kernel.h", "sampler_math.h", source):
         with open(os.path.join(src, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -52,7 +52,8 @@ enum { TADM_FUSION_GATED_MLP = 0, TADM_FUSION_PAIRED = 1 };
 /* Model shape.  Layers are numbered shared [0, n_shared), anchor, then denoiser.
  * dtype is the storage/operand type of weights and GEMM/attention operands; the
  * residual stream, norm statistics, softmax, logits and the sampler are float32.
- * max_batch x max_seq bounds every call (positions include any context). */
+ * max_batch x max_seq bounds every call (positions include any context).
+ * vocab is at most 262144 (the sampler keeps one partial per 64 entries on chip). */
 typedef struct {
   int32_t vocab, d_model, n_heads, n_kv_heads, head_dim, d_ffn, ffn_kind;
   int32_t n_shared, n_anchor, n_denoise, fusion_kind, fusion_rank, paired_heads;
@@ -143,7 +144,10 @@ tadm_status tadm_denoise_step(tadm_model* m, const tadm_context* ctx, const int3
  * (MDLM zero-masking and carry-over, App. B.1.1, with sigma_t = 0).
  * For every masked position (absolute position pos0 + column): Gumbel-max token
  * from softmax(logits * inv_temp) with Philox4x32-10 noise, and its confidence
- * (log-probability at that temperature, normaliser summed in 2^-40 fixed point).
+ * (log-probability at that temperature; the normaliser is summed in 2^-40 fixed
+ * point per group of 64 vocabulary entries relative to the group maximum, and the
+ * groups' integer sums are rescaled to the row maximum and added as integers, so the
+ * result does not depend on summation order).  Logits must be finite.
  * Per row, the n_unmask masked positions of highest (confidence, then lowest
  * position) take their token; every other entry of canvas_dev is copied.
  * choice_dev / conf_dev ([B, L - canvas_off], nullable) receive the sampled token
@@ -170,8 +174,11 @@ int32_t tadm_unmask_count(int32_t M0, int32_t i, int32_t T);
  *   TADM_TAP_EMBED  c = S(z)          [B, L, d]
  *   TADM_TAP_FUSED  h~ = Phi(c, h')   [B, L, d]
  *   TADM_TAP_FINAL  final-normed D output of the canvas columns [B, L - off, d]
- *                   (only after a step that was given logits_dev) */
-enum { TADM_TAP_EMBED = 0, TADM_TAP_FUSED = 1, TADM_TAP_FINAL = 2 };
+ *                   (only after a step that was given logits_dev)
+ *   TADM_TAP_CHOICE sampled token of every canvas column [B, L - off] (int32 bits;
+ *                   -1 where the entry was not masked)
+ *   TADM_TAP_CONF   its confidence [B, L - off] (float32; -inf where not masked) */
+enum { TADM_TAP_EMBED = 0, TADM_TAP_FUSED = 1, TADM_TAP_FINAL = 2, TADM_TAP_CHOICE = 3, TADM_TAP_CONF = 4 };
 /* Keep a copy of h~ for TADM_TAP_FUSED (one extra [B, L, d] copy per step; off by default). */
 tadm_status tadm_debug_taps(tadm_model* m, int32_t enable);
 tadm_status tadm_debug_read(tadm_model* m, int32_t tap, float* dst_dev, size_t bytes);

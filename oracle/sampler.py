@@ -17,9 +17,15 @@ individually rounded +, -, *, / (no fused multiply-add):
 * Gumbel noise G = -log(-log u); the token is argmax_v (l_v * inv_temp + G_v) with
   ties broken towards the smaller v (Gumbel-max sampling from softmax(l/temp));
 * confidence = log-softmax of the chosen token at temperature temp, with the
-  normaliser summed exactly in 64-bit fixed point:
-  S = sum_v rint(exp(l'_v - m) * 2^40), conf = (l'_x - m) - log(float(S) * 2^-40),
-  where l' = l * inv_temp and m = max l' (terms with l'_v - m < -30 are 0);
+  normaliser summed exactly in 64-bit fixed point over groups of 64 consecutive
+  vocabulary entries (g = v div 64; the last group may be shorter):
+  m_g = max_{v in g} l'_v, S_g = sum_{v in g} rint(exp(l'_v - m_g) * 2^40),
+  S = sum_g rint(float(S_g) * exp(m_g - m)), conf = (l'_x - m) - log(float(S) * 2^-40),
+  where l' = l * inv_temp, m = max l' = max_g m_g, float() rounds to nearest even and
+  exp of an argument below -30 is 0.  Every sum is over integers, so any summation
+  order gives the same bits, and a group only needs its own 64 logits: a kernel
+  that sees the vocabulary one tile at a time (the vocabulary projection's own
+  output tiles) computes the same confidence as one that sees the whole row;
 * ranking key: confidence descending, then position ascending.
 
 ``log32`` and ``exp32`` are this module's own float32 logarithm and exponential:
@@ -125,6 +131,23 @@ def uniforms(V, pos, row, step_id, seed):
     return bits_to_uniform(words)
 
 
+GROUP = 64  # vocabulary entries per normaliser group
+
+
+def normaliser(lp):
+    """(m, S): the row maximum of the scaled logits lp and the two-level fixed-point
+    normaliser, S ~ 2^40 * sum_v exp(lp_v - m)."""
+    m = lp.max()
+    S = 0
+    for g0 in range(0, lp.shape[0], GROUP):
+        seg = lp[g0:g0 + GROUP]
+        mg = seg.max()
+        Sg = int(np.sum(np.rint(exp32(seg - mg) * F32(2.0 ** 40)).astype(np.int64)))
+        term = F32(F32(Sg) * exp32(F32(mg - m)))
+        S += int(np.rint(term))
+    return m, S
+
+
 def sample_position(logits_row, inv_temp, pos, row, step_id, seed):
     """(token, confidence) for one masked position; logits_row is float32 [V]."""
     lg = np.asarray(logits_row, dtype=F32)
@@ -134,9 +157,7 @@ def sample_position(logits_row, inv_temp, pos, row, step_id, seed):
     gumbel = -log32(-log32(u))
     score = lp + gumbel
     tok = int(np.argmax(score))            # first maximum: smallest v on ties
-    m = lp.max()
-    e = exp32(lp - m)
-    S = int(np.sum(np.rint(e * F32(2.0 ** 40)).astype(np.int64)))
+    m, S = normaliser(lp)
     norm = F32(np.int64(S).astype(F32)) * F32(2.0 ** -40)
     conf = F32(lp[tok] - m) - log32(np.array([norm], dtype=F32))[0]
     return tok, F32(conf)

@@ -24,7 +24,7 @@ DTYPE = {"f32": 0, "bf16": 1}
 FFN = {"gelu": 0, "swiglu": 1, "geglu": 2}
 FUSION = {"gated_mlp": 0, "paired": 1}
 CACHE_H, CACHE_C, CACHE_A = 0, 1, 2
-TAP_EMBED, TAP_FUSED, TAP_FINAL = 0, 1, 2
+TAP_EMBED, TAP_FUSED, TAP_FINAL, TAP_CHOICE, TAP_CONF = 0, 1, 2, 3, 4
 STAGES = ["embed", "anchor", "fusion", "denoise", "head", "sample", "select", "context",
           "qkv", "attn", "oproj", "ffn_up", "ffn_down", "fusion1", "fusion2"]
 

@@ -73,11 +73,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, grp = lane >> 4, fr = lane & 15;
-  const int h = blockIdx.y, b = blockIdx.z;
+  // one block per (64-query tile, head, batch row), query tiles fastest: the tiles of a
+  // head, and the heads sharing a K/V head, run on one XCD and read K/V from its L2
+  const int nqt = (Lq + 63) / 64;
+  const int id = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int qt = id % nqt, h = (id / nqt) % H, b = id / (nqt * H);
   const int hk = (h * Hkv) / H;
   const bf16* Kb = K + ((size_t)b * Hkv + hk) * kv_cap * DH;
   const bf16* Vb = Vt + ((size_t)b * Hkv + hk) * DH * kv_cap;
-  const int q = blockIdx.x * 64 + wave * 16 + fr;
+  const int q = qt * 64 + wave * 16 + fr;
   const bf16* Qr = Q + (((size_t)b * H + h) * Lq + min(q, Lq - 1)) * DH;
 
   bf16x8 qf[DH / 32];
@@ -259,7 +263,7 @@ hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, voi
                      int Hkv, int Lq, int Lk, int kv_cap, int dh, hipStream_t s) {
   if (B * Lq == 0) return hipSuccess;
   if (dt == BF16) {
-    const dim3 grid((Lq + 63) / 64, H, B);
+    const dim3 grid(((Lq + 63) / 64) * H * B);
     const float sl2 = 1.4426950408889634f / sqrtf((float)dh);
     if (dh == 64)
       launch_timed(attn_bf16_kernel<64>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),

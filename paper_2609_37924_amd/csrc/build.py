@@ -1,9 +1,10 @@
 """Builds libtadm.so (gfx950) from the HIP sources next to this file.
 
 Usage: python build.py [--jobs N].  Each source compiles to an object with hipcc
-(-O3, --offload-arch=gfx950, packed-fp32 instructions disabled); the sampler is
-compiled without floating-point contraction so that its float32 arithmetic is
-exactly the documented sequence of rounded operations.
+(-O3, --offload-arch=gfx950, packed-fp32 instructions disabled); the sampler and
+the vocabulary projection with the sampling epilogue are compiled without
+floating-point contraction and with correctly rounded division, so that their
+float32 arithmetic is exactly the documented sequence of rounded operations.
 """
 import os
 import subprocess
@@ -13,8 +14,9 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
-SOURCES = ["runtime.hip", "gemm.hip", "attention.hip", "norm.hip", "sampler.hip", "fusion.hip"]
-EXTRA = {"sampler.hip": ["-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt"]}
+SOURCES = ["runtime.hip", "gemm.hip", "attention.hip", "norm.hip", "sampler.hip", "head_sample.hip", "fusion.hip"]
+CONTRACT = ["-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt"]
+EXTRA = {"sampler.hip": CONTRACT, "head_sample.hip": CONTRACT}
 OUT = os.path.join(PKG, "libtadm.so")
 
 

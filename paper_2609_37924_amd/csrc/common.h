@@ -26,6 +26,14 @@ __device__ __forceinline__ void store4(bf16* p, float a, float b, float c, float
   *reinterpret_cast<bf16x4*>(p) = v;
 }
 
+// Workgroups of a launch are dispatched round-robin over the 8 XCDs (id % 8), each with
+// its own L2.  Renumber ids so that XCD x runs one contiguous range of logical ids:
+// neighbouring work items that read the same data then share an L2.
+__device__ __forceinline__ int xcd_contiguous(int id, int n) {
+  const int x = id % 8, local = id / 8, q = n / 8, r = n % 8;
+  return x < r ? x * (q + 1) + local : r * (q + 1) + (x - r) * q + local;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, TADM_WAVE);

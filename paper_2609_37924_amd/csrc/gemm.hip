@@ -1,25 +1,15 @@
 // Dense contractions of the TADM step: C = A W^T with fused epilogues.
 //
-// bf16 path (gfx950): WGM x WGN wave64s per block, block tile BM x BN, K tiles of
-// 64.  Tiles move global -> LDS with global_load_lds_dwordx4 (no register staging) through a STAGES-deep ring of LDS buffers, so that STAGES-1 tiles are in
-// flight while one is multiplied.  LDS rows are 128 B (64 bf16); the 16-byte chunk c
-// of row r is stored in slot c ^ (r & 7), which makes the MFMA fragment reads
-// (16 rows x one chunk) hit distinct banks; the permutation is applied through the
-// global addresses because each lane's 16 bytes land at a fixed LDS slot.
-// Products use v_mfma_f32_16x16x32_bf16 with the weight tile as the "A" operand and
-// the activation tile as "B", so every lane ends with 4 consecutive output features
-// of one row and stores them as one vector.  Blocks are renumbered so that the
-// tiles sharing a weight panel run on the same XCD (each XCD has its own L2).
-// float32 path (small fp32 models): a register-blocked VALU kernel, same epilogues.
-#include "common.h"
-#include "kernels.h"
+// bf16 operands run on the MFMA kernel template of gemm_kernel.h with the epilogues
+// below; the tile shape is picked per call from the number of blocks it yields.
+// float32 operands (small fp32 models) run on a register-blocked VALU kernel with
+// the same epilogues.
+#include "gemm_kernel.h"
 
 namespace tadm {
 namespace {
 
 // ------------------------------------------------------------------ epilogues
-template <EpiKind K, class T>
-struct Epi;
 
 template <class T>
 struct Epi<EPI_STORE, T> {
@@ -170,145 +160,6 @@ struct Epi<EPI_GLU_GELU, T> {
   }
 };
 
-// waitcnt immediate for "at most n vector-memory operations outstanding" (gfx9 encoding)
-constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
-
-typedef __attribute__((address_space(3))) void* lds_ptr;
-typedef const __attribute__((address_space(1))) void* gbl_ptr;
-
-// Block index -> (m tile, n tile).  Workgroups are dealt to the 8 XCDs round-robin,
-// so block b runs on XCD b % 8 as its (b / 8)-th block.  When the tile grid splits
-// into 8 regions of rm x rn tiles, XCD x works through region x (m fastest), so the
-// A rows and W rows it reads (rm*BM + rn*BN rows) stay in its own L2.
-__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int rm, int rn, int& tm, int& tn) {
-  const int b = blockIdx.x;
-  if (rm > 0) {
-    const int x = b % 8, i = b / 8, regions_m = tiles_m / rm;
-    tm = (x % regions_m) * rm + i % rm;
-    tn = (x / regions_m) * rn + i / rm;
-    return;
-  }
-  tm = b % tiles_m;
-  tn = b / tiles_m;
-}
-
-// ------------------------------------------------------------ bf16 MFMA kernel
-template <int BM, int BN, int STAGES, int WGM, int WGN, int MINB, EpiKind KIND>
-__global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmProblem p, EpiParams ep) {
-  using E = Epi<KIND, bf16>;
-  constexpr int NW = WGM * WGN;                 // waves per block
-  constexpr int ROW = 128;                      // bytes per LDS row (64 bf16)
-  constexpr int STAGE_BYTES = (BM + BN) * ROW;
-  constexpr int LA = BM / 8 / NW, LW = BN / 8 / NW;  // load instructions per wave per stage
-  static_assert(LA * 8 * NW == BM && LW * 8 * NW == BN, "tile rows must split evenly over waves");
-  constexpr int LPS = LA + LW;
-  constexpr int WTM = BM / WGM, WTN = BN / WGN; // wave tile
-  constexpr int TM = WTM / 16, TN = WTN / 16;   // 16x16 subtiles per wave
-  static_assert(WTN % 32 == 0, "GLU pairs need 32-row weight blocks per wave");
-  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE_BYTES];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave % WGM, wn = wave / WGM;
-  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
-  int tmi, tni;
-  tile_of(tiles_m, tiles_n, p.rm, p.rn, tmi, tni);
-  const int m0 = tmi * BM, n0 = tni * BN;
-  if (p.M_dev) {  // rows present this call; the grid was sized for p.M
-    p.M = min(*p.M_dev, p.M);
-    if (m0 >= p.M) return;
-  }
-
-  const bf16* A1 = static_cast<const bf16*>(p.A1);
-  const bf16* A2 = static_cast<const bf16*>(p.A2);
-  const bf16* W = static_cast<const bf16*>(p.W);
-
-  // this lane's source row inside an 8-row group and its swizzled chunk
-  const int lrow = lane >> 3, lchunk = (lane & 7) ^ (lane >> 3);
-
-  auto issue = [&](int kt, int buf) {
-    const int k0 = kt * 64;
-    const bf16* Ab = A1;
-    int lda = p.lda1, kk = k0;
-    if (k0 >= p.K1) { Ab = A2; lda = p.lda2; kk = k0 - p.K1; }
-    char* sb = smem + buf * STAGE_BYTES;
-#pragma unroll
-    for (int j = 0; j < LA; ++j) {
-      const int g = wave + NW * j;              // 8-row group
-      const int r = min(m0 + g * 8 + lrow, p.M - 1);
-      const bf16* src = Ab + (size_t)r * lda + kk + lchunk * 8;
-      __builtin_amdgcn_global_load_lds((gbl_ptr)src, (lds_ptr)(sb + g * 1024), 16, 0, 0);
-    }
-#pragma unroll
-    for (int j = 0; j < LW; ++j) {
-      const int g = wave + NW * j;
-      const int r = min(n0 + g * 8 + lrow, p.N - 1);
-      const bf16* src = W + (size_t)r * p.ldw + k0 + lchunk * 8;
-      __builtin_amdgcn_global_load_lds((gbl_ptr)src, (lds_ptr)(sb + BM * ROW + g * 1024), 16, 0, 0);
-    }
-  };
-
-  f32x4 acc[TN][TM];
-#pragma unroll
-  for (int a = 0; a < TN; ++a)
-#pragma unroll
-    for (int b = 0; b < TM; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const int nk = p.K / 64;
-#pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) issue(s, s);
-
-  const int fr = lane & 15, fq = lane >> 4, sw = lane & 7;
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + STAGES - 2 < nk)
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm((STAGES - 2) * LPS));
-    else
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    __syncthreads();
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-    const char* sa = smem + (kt % STAGES) * STAGE_BYTES;
-    const char* swt = sa + BM * ROW;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int slot = ((kk * 4 + fq) ^ sw) * 16;
-      bf16x8 fa[TM], fw[TN];
-#pragma unroll
-      for (int t = 0; t < TM; ++t)
-        fa[t] = *reinterpret_cast<const bf16x8*>(sa + (wm * WTM + t * 16 + fr) * ROW + slot);
-#pragma unroll
-      for (int t = 0; t < TN; ++t)
-        fw[t] = *reinterpret_cast<const bf16x8*>(swt + (wn * WTN + t * 16 + fr) * ROW + slot);
-#pragma unroll
-      for (int a = 0; a < TN; ++a)
-#pragma unroll
-        for (int b = 0; b < TM; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[a], fa[b], acc[a][b], 0, 0, 0);
-    }
-  }
-
-  // lane holds C[n = nb + 4*(lane>>4) + j][m = mb + (lane & 15)]
-  const int mw = m0 + wm * WTM + fr;
-  if constexpr (E::kGlu) {
-#pragma unroll
-    for (int a = 0; a < TN; a += 2)
-#pragma unroll
-      for (int b = 0; b < TM; ++b) {
-        const int m = mw + b * 16;
-        const int ng = n0 + wn * WTN + a * 16;  // multiple of 32: gate rows of a 32-row block
-        if (m < p.M && ng < p.N) E::glu(ep, m, ng / 2 + 4 * fq, acc[a][b], acc[a + 1][b]);
-      }
-  } else {
-    const int nw = n0 + wn * WTN + 4 * fq;
-#pragma unroll
-    for (int a = 0; a < TN; ++a)
-#pragma unroll
-      for (int b = 0; b < TM; ++b) {
-        const int m = mw + b * 16, n = nw + a * 16;
-        if (m < p.M && n < p.N) E::apply(ep, m, n, acc[a][b]);
-      }
-  }
-}
-
 // ------------------------------------------------------------ fp32 VALU kernel
 // Tile 64 (rows) x 64 (features), K step 16; each thread computes 4 x 4 outputs.
 template <EpiKind KIND>
@@ -379,33 +230,6 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmProblem p, EpiParams 
   }
 }
 
-// Per-XCD region rm x rn with (tiles_m / rm) * (tiles_n / rn) = 8 that minimises the
-// rows each XCD reads (rm * BM + rn * BN); 0 when the grid does not split evenly.
-inline void xcd_regions(int tiles_m, int tiles_n, int BM, int BN, int& rm, int& rn) {
-  rm = rn = 0;
-  long best = -1;
-  for (int gm = 1; gm <= 8; gm *= 2) {
-    const int gn = 8 / gm;
-    if (tiles_m % gm || tiles_n % gn) continue;
-    const long cost = (long)(tiles_m / gm) * BM + (long)(tiles_n / gn) * BN;
-    if (best < 0 || cost < best) {
-      best = cost;
-      rm = tiles_m / gm;
-      rn = tiles_n / gn;
-    }
-  }
-}
-
-template <int BM, int BN, int ST, int WGM, int WGN, int MINB, EpiKind K>
-hipError_t launch_bf16(const GemmProblem& p0, const EpiParams& e, hipStream_t s) {
-  GemmProblem p = p0;
-  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
-  xcd_regions(tiles_m, tiles_n, BM, BN, p.rm, p.rn);
-  launch_timed(gemm_bf16_kernel<BM, BN, ST, WGM, WGN, MINB, K>, dim3(tiles_m * tiles_n), dim3(64 * WGM * WGN),
-               0, s, p, e);
-  return hipGetLastError();
-}
-
 template <EpiKind K>
 hipError_t dispatch(DType dt, const GemmProblem& p, const EpiParams& e, hipStream_t s) {
   if (dt == F32) {
@@ -442,6 +266,7 @@ hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e
     case EPI_ADD_SUB: return dispatch<EPI_ADD_SUB>(dt, p, e, s);
     case EPI_PAIRED: return dispatch<EPI_PAIRED>(dt, p, e, s);
     case EPI_QKV_ROPE: return dispatch<EPI_QKV_ROPE>(dt, p, e, s);
+    case EPI_SAMPLE: break;  // head_sample
   }
   return hipErrorInvalidValue;
 }

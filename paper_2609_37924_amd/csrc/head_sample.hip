@@ -1,0 +1,211 @@
+// Vocabulary projection with the reverse step's sampling in its epilogue: the logits
+// of the masked rows stay in registers.  A wave's 64 output columns of a row are one
+// normaliser group of the sampling contract (64 consecutive vocabulary entries), held
+// by the four lanes (lane & 15) + 16 q, q = 0..3.  Per (row, group) the epilogue
+// emits the group maximum m_g, the fixed-point sum S_g and the group's exact best
+// Gumbel score; sample_finalize merges the groups of a row exactly as the standalone
+// sampler merges its own groups, so both paths give the same bits.
+//
+// This file is compiled with -ffp-contract=off and correctly rounded float32 division
+// (the contract arithmetic of sampler_math.h); the MFMA main loop is unaffected.
+#include "gemm_kernel.h"
+#include "sampler_math.h"
+
+namespace tadm {
+namespace {
+
+struct Cand {  // exact score, entry and its scaled logit
+  float score;
+  int v;
+  float lp;
+};
+__device__ __forceinline__ Cand better_cand(Cand a, Cand b) {
+  return (b.score > a.score || (b.score == a.score && b.v < a.v)) ? b : a;
+}
+__device__ __forceinline__ Cand shfl_cand(Cand c, int o) {
+  return Cand{__shfl_xor(c.score, o, 64), __shfl_xor(c.v, o, 64), __shfl_xor(c.lp, o, 64)};
+}
+
+template <class T>
+struct Epi<EPI_SAMPLE, T> {
+  static constexpr bool kTile = true;
+
+  // acc[a][b][jj] = C[n = nb + 16 a + 4 (lane >> 4) + jj][m = mb + 16 b + (lane & 15)]
+  template <int TN, int TM>
+  __device__ __forceinline__ static void tile(const EpiParams& e, const GemmProblem& p, const f32x4 (&acc)[TN][TM],
+                                              int mb,
+                              int nb, int lane) {
+    static_assert(TN * 16 == SAMPLE_GROUP, "one wave column strip must be one normaliser group");
+    const int fr = lane & 15, fq = lane >> 4;
+    const int g = nb / SAMPLE_GROUP;
+#pragma unroll 1
+    for (int b = 0; b < TM; ++b) {
+      // this row subtile's accumulators, picked with static indices (a runtime index
+      // into acc would move the whole tile to scratch)
+      f32x4 cb[TN];
+#pragma unroll
+      for (int a = 0; a < TN; ++a) {
+        cb[a] = acc[a][0];
+#pragma unroll
+        for (int k = 1; k < TM; ++k)
+          if (b == k) cb[a] = acc[a][k];
+      }
+      const int m = mb + 16 * b + fr;
+      const bool row_ok = m < p.M;
+      const int ci = e.rows_idx[row_ok ? m : 0];
+      const uint32_t brow = (uint32_t)(ci / e.Lc), pos = (uint32_t)(e.pos_base + ci % e.Lc);
+      float lp[TN][4];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int a = 0; a < TN; ++a)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int n = nb + 16 * a + 4 * fq + jj;
+          lp[a][jj] = n < p.N ? cb[a][jj] * e.inv_temp : -INFINITY;
+          mx = fmaxf(mx, lp[a][jj]);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      // S_g: each rint(exp(l' - m_g) 2^40) <= 2^40 is split exactly into 20-bit halves
+      uint32_t hi = 0, lo = 0;
+      // screening: this lane's two best scores, with the best entry's l' and u
+      float a1 = -INFINITY, a2 = -INFINITY, lp1 = 0.f, u1 = 0.5f;
+      int v1 = 0x7FFFFFFF;
+#pragma unroll
+      for (int a = 0; a < TN; ++a) {
+        const int n0 = nb + 16 * a + 4 * fq;
+        uint32_t c[4] = {(uint32_t)n0 >> 2, pos, brow, e.step_id};
+        philox4x32_10(c, e.k0, e.k1);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          if (n0 + jj >= p.N) continue;
+          const float q = rintf(own_exp(lp[a][jj] - mx) * 1099511627776.0f);  // * 2^40
+          const float qh = floorf(q * 9.5367431640625e-07f);                      // * 2^-20
+          hi += (uint32_t)qh;
+          lo += (uint32_t)(q - qh * 1048576.0f);
+          const float u = uniform01(c[jj]);
+          const float sc = screen_score(lp[a][jj], u);
+          if (sc > a1) {
+            a2 = a1;
+            a1 = sc;
+            v1 = n0 + jj;
+            lp1 = lp[a][jj];
+            u1 = u;
+          } else if (sc > a2) {
+            a2 = sc;
+          }
+        }
+      }
+      hi += __shfl_xor(hi, 16, 64);
+      hi += __shfl_xor(hi, 32, 64);
+      lo += __shfl_xor(lo, 16, 64);
+      lo += __shfl_xor(lo, 32, 64);
+      float amax = fmaxf(a1, __shfl_xor(a1, 16, 64));
+      amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
+      const float delta = 1e-3f + 2.4e-6f * (fabsf(mx) + 32.f);  // screening error bound, x 100
+      const float wlo = amax - 2.5f * delta;
+      int multi = a2 >= wlo ? 1 : 0;
+      multi |= __shfl_xor(multi, 16, 64);
+      multi |= __shfl_xor(multi, 32, 64);
+      Cand best{-INFINITY, 0x7FFFFFFF, 0.f};
+      if (multi) {  // a second entry of some lane is in the window: score the group exactly
+#pragma unroll
+        for (int a = 0; a < TN; ++a) {
+          const int n0 = nb + 16 * a + 4 * fq;
+          uint32_t c[4] = {(uint32_t)n0 >> 2, pos, brow, e.step_id};
+          philox4x32_10(c, e.k0, e.k1);
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+            if (n0 + jj < p.N)
+              best = better_cand(best, Cand{exact_score_of(lp[a][jj], uniform01(c[jj])), n0 + jj, lp[a][jj]});
+        }
+      } else if (a1 >= wlo && v1 < p.N) {
+        best = Cand{exact_score_of(lp1, u1), v1, lp1};
+      }
+      best = better_cand(best, shfl_cand(best, 16));
+      best = better_cand(best, shfl_cand(best, 32));
+      if (fq == 0 && row_ok && nb < p.N) {
+        SamplePart r;
+        r.m = mx;
+        r.score = best.score;
+        r.lp = best.lp;
+        r.v = best.v;
+        r.S = ((long long)hi << 20) + (long long)lo;
+        static_cast<SamplePart*>(e.part)[(size_t)m * e.n_groups + g] = r;
+      }
+    }
+  }
+};
+
+// grid (Lc, B), 256 threads: one workgroup per canvas position.
+__global__ __launch_bounds__(256) void finalize_kernel(const SamplePart* part, int n_groups, int V,
+                                                       const int32_t* row_map, const int32_t* canvas, int L,
+                                                       int off, int Lc, int mask_id, int32_t* choice,
+                                                       float* conf) {
+  __shared__ float s_m[4];
+  __shared__ Cand s_c[4];
+  __shared__ long long s_S[4];
+  const int j = blockIdx.x, b = blockIdx.y, row = b * Lc + j;
+  if (canvas[(size_t)b * L + off + j] != mask_id) {
+    if (threadIdx.x == 0) {
+      choice[row] = -1;
+      conf[row] = -INFINITY;
+    }
+    return;
+  }
+  const SamplePart* P = part + (size_t)row_map[row] * n_groups;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  float mx = -INFINITY;
+  Cand best{-INFINITY, 0x7FFFFFFF, 0.f};
+  for (int g = tid; g < n_groups; g += 256) {
+    mx = fmaxf(mx, P[g].m);
+    best = better_cand(best, Cand{P[g].score, P[g].v, P[g].lp});
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    best = better_cand(best, shfl_cand(best, o));
+  }
+  if (lane == 0) {
+    s_m[wave] = mx;
+    s_c[wave] = best;
+  }
+  __syncthreads();
+  mx = fmaxf(fmaxf(s_m[0], s_m[1]), fmaxf(s_m[2], s_m[3]));
+  long long S = 0;
+  for (int g = tid; g < n_groups; g += 256) S += (long long)rintf((float)P[g].S * own_exp(P[g].m - mx));
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) S += __shfl_xor(S, o, 64);
+  if (lane == 0) s_S[wave] = S;
+  __syncthreads();
+  if (tid == 0) {
+    best = s_c[0];
+    for (int k = 1; k < 4; ++k) best = better_cand(best, s_c[k]);
+    S = s_S[0] + s_S[1] + s_S[2] + s_S[3];
+    if (best.v >= V) best = Cand{0.f, 0, 0.f};  // only reachable with non-finite logits
+    const float norm = (float)S * 9.094947017729282379150390625e-13f;  // * 2^-40, exact
+    choice[row] = best.v;
+    conf[row] = (best.lp - mx) - own_log(norm);
+  }
+}
+
+}  // namespace
+
+hipError_t head_sample(const GemmProblem& p, const EpiParams& e, hipStream_t s) {
+  if (p.M <= 0 || p.N <= 0) return hipSuccess;
+  // 128 x 128 tiles on 2 x 2 waves (64-column wave strips), two blocks per CU: one
+  // block's VALU-heavy epilogue overlaps the other's MFMA main loop
+  return launch_bf16<128, 128, 2, 2, 2, 2, EPI_SAMPLE>(p, e, s);
+}
+
+hipError_t sample_finalize(const SamplePart* part, int n_groups, int V, const int32_t* row_map,
+                           const int32_t* canvas, int B, int L, int canvas_off, int mask_id, int32_t* choice,
+                           float* conf, hipStream_t s) {
+  const int Lc = L - canvas_off;
+  if (B * Lc == 0) return hipSuccess;
+  launch_timed(finalize_kernel, dim3(Lc, B), dim3(256), 0, s, part, n_groups, V, row_map, canvas, L, canvas_off, Lc,
+               mask_id, choice, conf);
+  return hipGetLastError();
+}
+
+}  // namespace tadm

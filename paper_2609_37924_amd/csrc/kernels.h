@@ -55,6 +55,8 @@ enum EpiKind {
   EPI_PAIRED,         // out(float)[m, n] = aux[m, n] + row1[m] * row2[m] * acc
   EPI_QKV_ROPE,       // q/k/v projection: rotary embedding on q, k (pair-interleaved
                       // weight rows) and scatter into the attention layouts (see EpiParams)
+  EPI_SAMPLE,         // vocabulary projection: sampling partials per (row, 64-column
+                      // group) instead of logits (head_sample only; see EpiParams)
 };
 
 struct EpiParams {
@@ -80,6 +82,23 @@ struct EpiParams {
   void* q = nullptr;
   void* k = nullptr;
   void* vt = nullptr;
+  // EPI_SAMPLE: row m is canvas entry rows_idx[m] = b * Lc + j at absolute position
+  // pos_base + j; the sampling contract's Philox key (k0, k1), step id and 1/temp;
+  // part receives n_groups SamplePart records per row.
+  const int32_t* rows_idx = nullptr;
+  int Lc = 0, pos_base = 0, n_groups = 0;
+  uint32_t step_id = 0, k0 = 0, k1 = 0;
+  float inv_temp = 1.f;
+  void* part = nullptr;
+};
+
+// Sampling partial of one (row, 64-entry vocabulary group): the group maximum m_g of
+// the scaled logits, its fixed-point sum S_g, and its exact best Gumbel score with the
+// entry's id and scaled logit.
+struct SamplePart {
+  float m, score, lp;
+  int v;
+  long long S;
 };
 
 hipError_t gemm(DType dt, const GemmProblem& p, EpiKind epi, const EpiParams& e, hipStream_t s);
@@ -138,6 +157,18 @@ hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, voi
 // (row-major order), row_map[b * Lc + j] = r or -1, *count = number of entries.
 hipError_t compact_masked(const int32_t* canvas, int B, int L, int canvas_off, int mask_id,
                           int32_t* idx, int32_t* row_map, int* count, hipStream_t s);
+// Vocabulary projection of the masked rows with the sampler in the epilogue (bf16):
+// p is the head GEMM (M = compacted masked rows, M_dev their device count, N = V);
+// e carries the EPI_SAMPLE fields.  Writes p.M x ceil(V / 64) partials to e.part.
+hipError_t head_sample(const GemmProblem& p, const EpiParams& e, hipStream_t s);
+// Merges the partials of every masked canvas position into its token and confidence
+// (row_map: canvas entry -> partial row); other positions get -1 / -inf.
+hipError_t sample_finalize(const SamplePart* part, int n_groups, int V, const int32_t* row_map,
+                           const int32_t* canvas, int B, int L, int canvas_off, int mask_id, int32_t* choice,
+                           float* conf, hipStream_t s);
+// Largest vocabulary the sampler handles: its per-group partials (64 entries per
+// group, 12 bytes each) live in 48 KB of LDS.
+constexpr int SAMPLE_MAX_VOCAB = 4096 * 64;
 // For every masked canvas position: Gumbel-max token and fixed-point confidence.
 // Logits row of position (b, j) is row_map[b * Lc + j] if row_map is set, else b * Lc + j.
 hipError_t sample_tokens(const float* logits, const int32_t* row_map, const int32_t* canvas, int B,

@@ -200,6 +200,7 @@ bool valid_config(const tadm_config* c, std::string& why) {
   if (c->vocab < 1 || c->d_model < 4 || c->n_heads < 1 || c->n_kv_heads < 1 || c->head_dim < 2 ||
       c->d_ffn < 16 || c->max_batch < 1 || c->max_seq < 1) { why = "non-positive size"; return false; }
   if (c->n_shared < 0 || c->n_anchor < 0 || c->n_denoise < 0) { why = "layer counts"; return false; }
+  if (c->vocab > SAMPLE_MAX_VOCAB) { why = "vocab above the sampler's 262144 entries"; return false; }
   if (c->n_heads % c->n_kv_heads) { why = "n_heads must be a multiple of n_kv_heads"; return false; }
   if (c->head_dim % 2) { why = "odd head_dim"; return false; }
   if (c->ffn_kind < 0 || c->ffn_kind > 2) { why = "ffn_kind"; return false; }
@@ -1071,8 +1072,16 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
                            off, d, s.xn, m->stream));
   }
   TRY(prof_end(m, TADM_STAGE_DENOISE));
+  m->tap_B = B;
+  m->tap_L = L;
+  m->tap_Lc = Lc;
+  m->tap_final = full;
+  // bf16 masked-only head: the sampler runs in the projection's epilogue and only
+  // per-(row, 64-entry group) partials reach memory
+  const bool fused = !full && m->dt == BF16;
+  const int ng = (cf.vocab + 63) / 64;
   if (!full) {
-    TRY(ensure_logits(m, (size_t)B * Lc * cf.vocab));
+    TRY(ensure_logits(m, fused ? (size_t)B * Lc * ng * (sizeof(SamplePart) / 4) : (size_t)B * Lc * cf.vocab));
     logits = s.logits;
   }
   TRY(prof_begin(m, TADM_STAGE_HEAD));
@@ -1080,17 +1089,35 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
     GemmProblem p{rows, cf.vocab, d, s.xn, d, d, nullptr, 0, m->W(m->lay.w_out), d};
     if (!full) p.M_dev = s.count;
     EpiParams e;
-    e.out = logits;
-    e.ldo = cf.vocab;
-    HIPCHK(gemm(m->dt, p, EPI_STORE_F32, e, m->stream));
+    if (fused) {
+      e.rows_idx = s.cidx;
+      e.Lc = Lc;
+      e.pos_base = pos0 + off;
+      e.n_groups = ng;
+      e.step_id = a->step_id;
+      e.k0 = (uint32_t)(a->seed & 0xFFFFFFFFu);
+      e.k1 = (uint32_t)(a->seed >> 32);
+      e.inv_temp = a->inv_temp;
+      e.part = s.logits;
+      HIPCHK(head_sample(p, e, m->stream));
+    } else {
+      e.out = logits;
+      e.ldo = cf.vocab;
+      HIPCHK(gemm(m->dt, p, EPI_STORE_F32, e, m->stream));
+    }
   }
   TRY(prof_end(m, TADM_STAGE_HEAD));
-  m->tap_B = B;
-  m->tap_L = L;
-  m->tap_Lc = Lc;
-  m->tap_final = full;
-  return sample_impl(m, logits, full ? nullptr : s.row_map, canvas, B, L, off, pos0, a, next, s.choice,
-                     s.conf);
+  if (!fused)
+    return sample_impl(m, logits, full ? nullptr : s.row_map, canvas, B, L, off, pos0, a, next, s.choice,
+                       s.conf);
+  TRY(prof_begin(m, TADM_STAGE_SAMPLE));
+  HIPCHK(sample_finalize(reinterpret_cast<const SamplePart*>(s.logits), ng, cf.vocab, s.row_map, canvas, B, L, off,
+                         cf.vocab, s.choice, s.conf, m->stream));
+  TRY(prof_end(m, TADM_STAGE_SAMPLE));
+  TRY(prof_begin(m, TADM_STAGE_SELECT));
+  HIPCHK(select_unmask(canvas, s.choice, s.conf, B, L, off, cf.vocab, a->n_unmask, next, m->stream));
+  TRY(prof_end(m, TADM_STAGE_SELECT));
+  return TADM_OK;
 }
 
 tadm_status tadm_denoise_step(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev, int32_t B,
@@ -1217,6 +1244,14 @@ tadm_status tadm_debug_read(tadm_model* m, int32_t tap, float* dst_dev, size_t b
       const size_t n = (size_t)m->tap_B * m->tap_Lc * d;
       if (bytes != n * 4) return fail(TADM_ERR_INVALID, "tap %d has %zu bytes", tap, n * 4);
       HIPCHK(to_f32(m->dt, m->ws.xn, dst_dev, n, m->stream));
+      return TADM_OK;
+    }
+    case TADM_TAP_CHOICE:
+    case TADM_TAP_CONF: {
+      const size_t n = (size_t)m->tap_B * m->tap_Lc;
+      if (bytes != n * 4) return fail(TADM_ERR_INVALID, "tap %d has %zu bytes", tap, n * 4);
+      HIPCHK(hipMemcpyAsync(dst_dev, tap == TADM_TAP_CHOICE ? (const void*)m->ws.choice : (const void*)m->ws.conf,
+                            bytes, hipMemcpyDeviceToDevice, m->stream));
       return TADM_OK;
     }
     default:

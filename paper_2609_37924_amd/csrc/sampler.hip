@@ -5,153 +5,52 @@
 // by any IEEE float32 implementation of the same operations):
 //  * Philox4x32-10 (Salmon et al., SC'11): counter (v/4, position, row, step id),
 //    key (seed low word, seed high word); word v%4 -> u = (2*(x>>9)+1) * 2^-24.
-//  * Own float32 log / exp built only from individually rounded +,-,*,/:
-//    log: x = 2^e m, m in [sqrt(1/2), sqrt(2)], log m = 2 atanh(s), s = (m-1)/(m+1),
-//         series in z = s^2 up to z^5, ln 2 split in a 15-bit head and a tail;
-//    exp: Cody-Waite reduction k = rint(y/ln2), degree-7 Taylor polynomial, 2^k from
-//         the exponent bits; 0 below -30.
-//    This file is compiled with -ffp-contract=off so that no multiply-add is fused,
-//    and with correctly rounded float32 division.
+//  * Own float32 log / exp (sampler_math.h) built only from individually rounded
+//    +,-,*,/; this file is compiled with -ffp-contract=off and correctly rounded
+//    float32 division.
 //  * token = argmax_v (l_v * inv_temp + G_v), G = -log(-log u), ties to smaller v;
-//    confidence = (l'_x - m) - log(float(S) * 2^-40), S = sum_v rint(exp(l'_v - m) 2^40)
-//    accumulated in int64, so any reduction order gives the same bits.
+//  * confidence = (l'_x - m) - log(float(S) * 2^-40) with the normaliser in 2^-40 fixed
+//    point over groups of 64 entries: m_g = max of group g, S_g = sum_{v in g}
+//    rint(exp(l'_v - m_g) 2^40), S = sum_g rint(float(S_g) exp(m_g - m)); every sum is
+//    over integers, so any reduction order (and any tiling) gives the same bits.
 //  * ranking: confidence descending, then position ascending.
 #include "common.h"
 #include "kernels.h"
+#include "sampler_math.h"
 
 #pragma clang fp contract(off)
 
 namespace tadm {
 namespace {
 
-__device__ __forceinline__ float bits_f(uint32_t b) { return __uint_as_float(b); }
-
-__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
-#pragma unroll
-  for (int r = 0; r < 10; ++r) {
-    if (r) {
-      k0 += 0x9E3779B9u;
-      k1 += 0xBB67AE85u;
-    }
-    const uint32_t lo0 = 0xD2511F53u * c[0], hi0 = __umulhi(0xD2511F53u, c[0]);
-    const uint32_t lo1 = 0xCD9E8D57u * c[2], hi1 = __umulhi(0xCD9E8D57u, c[2]);
-    const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
-    c[0] = n0;
-    c[1] = lo1;
-    c[2] = n2;
-    c[3] = lo0;
-  }
-}
-
-__device__ __forceinline__ float uniform01(uint32_t x) {
-  return (float)((x >> 9) * 2u + 1u) * 5.9604644775390625e-8f;  // * 2^-24, exact
-}
-
-__device__ __forceinline__ float own_log(float x) {
-  const float LN2_HI = bits_f(0x3F317200u), LN2_LO = bits_f(0x35BFBE8Eu);
-  const uint32_t bits = __float_as_uint(x);
-  int e = (int)(bits >> 23) - 127;
-  uint32_t mb = (bits & 0x007FFFFFu) | 0x3F800000u;
-  if (mb > 0x3FB504F3u) {  // m above sqrt(2): halve it
-    mb -= 0x00800000u;
-    e += 1;
-  }
-  const float m = __uint_as_float(mb);
-  const float f = m - 1.0f;
-  const float s = f / (2.0f + f);
-  const float z = s * s;
-  float p = bits_f(0x3E3A2E8Cu);       // 2/11
-  p = p * z + bits_f(0x3E638E39u);     // 2/9
-  p = p * z + bits_f(0x3E924925u);     // 2/7
-  p = p * z + bits_f(0x3ECCCCCDu);     // 2/5
-  p = p * z + bits_f(0x3F2AAAABu);     // 2/3
-  p = p * z + 2.0f;
-  const float t = s * p;
-  const float ef = (float)e;
-  return ef * LN2_HI + (ef * LN2_LO + t);
-}
-
-__device__ __forceinline__ float own_exp(float y) {
-  if (y < -30.0f) return 0.0f;
-  const float LN2_HI = bits_f(0x3F317200u), LN2_LO = bits_f(0x35BFBE8Eu);
-  const float k = rintf(y * bits_f(0x3FB8AA3Bu));
-  const float r = (y - k * LN2_HI) - k * LN2_LO;
-  float p = bits_f(0x39500D01u);       // 1/5040
-  p = p * r + bits_f(0x3AB60B61u);     // 1/720
-  p = p * r + bits_f(0x3C088889u);     // 1/120
-  p = p * r + bits_f(0x3D2AAAABu);     // 1/24
-  p = p * r + bits_f(0x3E2AAAABu);     // 1/6
-  p = p * r + 0.5f;
-  p = p * r + 1.0f;
-  p = p * r + 1.0f;
-  const float scale = __uint_as_float((uint32_t)((int)k + 127) << 23);
-  return p * scale;
-}
-
-struct Best {
-  float score;
-  int v;
-};
-__device__ __forceinline__ Best better(Best a, Best b) {
-  return (b.score > a.score || (b.score == a.score && b.v < a.v)) ? b : a;
-}
-
-// Screening logarithm: the same exponent/mantissa split and atanh series as own_log,
-// with an approximate reciprocal and a shorter series.  Relative error below 1e-6 on
-// the sampler's arguments; it only ranks entries and never decides a token.
-__device__ __forceinline__ float screen_log(float x) {
-  const float LN2 = bits_f(0x3F317218u);
-  const uint32_t bits = __float_as_uint(x);
-  int e = (int)(bits >> 23) - 127;
-  uint32_t mb = (bits & 0x007FFFFFu) | 0x3F800000u;
-  if (mb > 0x3FB504F3u) {
-    mb -= 0x00800000u;
-    e += 1;
-  }
-  const float f = __uint_as_float(mb) - 1.0f;
-  const float s = f * __builtin_amdgcn_rcpf(2.0f + f);
-  const float z = s * s;
-  const float p = fmaf(z, fmaf(z, fmaf(z, 0.2857142857f, 0.4f), 0.6666666667f), 2.0f);
-  return fmaf((float)e, LN2, s * p);
-}
-
-// Exact contract score of entry v: l'_v + G_v with G = -log(-log u), u from Philox.
+// Exact contract score of entry v of a logits row.
 __device__ __forceinline__ float exact_score(const float* lg, int v, uint32_t pos, uint32_t b,
                                              uint32_t step_id, uint32_t k0, uint32_t k1, float inv_temp) {
   uint32_t c[4] = {(uint32_t)(v >> 2), pos, b, step_id};
   philox4x32_10(c, k0, k1);
-  const float E = -own_log(uniform01(c[v & 3]));
-  const float G = -own_log(E);
-  return lg[v] * inv_temp + G;
+  return exact_score_of(lg[v] * inv_temp, uniform01(c[v & 3]));
 }
 
-template <bool VEC4>
-__device__ __forceinline__ void load4(const float* lg, int g, int V, float l4[4]) {
-  if (VEC4) {
-    const float4 v4 = *reinterpret_cast<const float4*>(lg + 4 * g);
-    l4[0] = v4.x; l4[1] = v4.y; l4[2] = v4.z; l4[3] = v4.w;
-  } else {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) l4[e] = 4 * g + e < V ? lg[4 * g + e] : 0.f;
-  }
-}
+constexpr int GROUP = SAMPLE_GROUP;  // one normaliser group: 16 lanes x 4 entries
+constexpr int CHUNK = 1024;     // entries per block pass: 256 threads x 4
+constexpr int UNROLL = 4;       // chunks whose loads are in flight together
 
-// grid (Lc, B); one workgroup per canvas position; only masked positions work.
-//
-// Pass 1: m = max_v l'_v.  Pass 2: the fixed-point normaliser S (exact, every entry)
-// and a screening value r_v = exp(l'_v - m) / E_v with E_v = -log u_v from the
-// screening log, so log r_v approximates the contract score minus m to within
-// ~2e-5 (|logits| < 1e3).  Only entries with r_v >= w * max r (a window of 1e-3 plus
-// the rounding of large scores, in log space) can hold the contract argmax; when each
-// thread has at most one such entry they are evaluated exactly and compared as
-// (score, smaller v); otherwise the row falls back to the exact scan of every entry.
-template <bool VEC4>
+// grid (Lc, B), 256 threads; one workgroup per canvas position, only masked positions
+// work.  One pass over the row's logits: lanes 16k..16k+15 of a wave hold the 64
+// entries of one group, reduce its maximum m_g and its fixed-point sum S_g (int64,
+// exact) with lane shuffles and park them in LDS; each thread also keeps its two best
+// screening scores.  Afterwards m = max m_g, S = sum_g rint(float(S_g) exp(m_g - m))
+// (exact integer sum).  The contract argmax is within 2.5 delta of the best screening
+// score (delta bounds the screening error, with a wide margin); when no thread has
+// a second entry in that window the threads' best entries are the only candidates and
+// are scored exactly, otherwise every entry is scored exactly in a second pass.
+// Dynamic LDS: ceil(V / 64) x (float + int64).
 __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const int32_t* row_map,
-                                                     const int32_t* canvas,
-                                                     int L, int off, int Lc, int V, int mask_id,
-                                                     int pos0, uint32_t step_id, uint32_t k0,
+                                                     const int32_t* canvas, int L, int off, int Lc, int V,
+                                                     int mask_id, int pos0, uint32_t step_id, uint32_t k0,
                                                      uint32_t k1, float inv_temp, int32_t* choice,
                                                      float* conf) {
+  extern __shared__ long long s_dyn[];
   __shared__ float s_f[4];
   __shared__ float s_score[4];
   __shared__ int s_v[4];
@@ -166,87 +65,107 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
     }
     return;
   }
+  const int ng = (V + GROUP - 1) / GROUP;
+  long long* s_S = s_dyn;
+  float* s_m = reinterpret_cast<float*>(s_dyn + ng);
   const float* lg = logits + (size_t)(row_map ? row_map[row] : row) * V;
   const uint32_t pos = (uint32_t)(pos0 + off + j);
-  const int ngroups = (V + 3) / 4;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const bool vec = (V & 3) == 0;
+  const int nchunk = (V + CHUNK - 1) / CHUNK;
 
-  // ---- pass 1: max scaled logit
-  float mx = -INFINITY;
-  for (int g = threadIdx.x; g < ngroups; g += 256) {
-    float l4[4];
-    load4<VEC4>(lg, g, V, l4);
+  Top2 top;
+  for (int c0 = 0; c0 < nchunk; c0 += UNROLL) {
+    float l[UNROLL][4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (VEC4 || 4 * g + e < V) mx = fmaxf(mx, l4[e] * inv_temp);
-  }
+    for (int u = 0; u < UNROLL; ++u) {  // issue every load first
+      const int v0 = (c0 + u) * CHUNK + 4 * tid;
+      if (vec && v0 + 3 < V) {
+        const float4 x = *reinterpret_cast<const float4*>(lg + v0);
+        l[u][0] = x.x; l[u][1] = x.y; l[u][2] = x.z; l[u][3] = x.w;
+      } else {
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-  if (lane == 0) s_f[wave] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(s_f[0], s_f[1]), fmaxf(s_f[2], s_f[3]));
-  __syncthreads();
-
-  // ---- pass 2: exact normaliser, screening values (top two per thread)
-  long long S = 0;
-  float r1 = 0.f, r2 = 0.f;
-  int v1 = 0x7FFFFFFF;
-  for (int g = threadIdx.x; g < ngroups; g += 256) {
-    float l4[4];
-    load4<VEC4>(lg, g, V, l4);
-    uint32_t c[4] = {(uint32_t)g, pos, (uint32_t)b, step_id};
-    philox4x32_10(c, k0, k1);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int v = 4 * g + e;
-      if (!VEC4 && v >= V) break;
-      const float ev = own_exp(l4[e] * inv_temp - mx);
-      S += (long long)rintf(ev * 1099511627776.0f);  // * 2^40, exact
-      const float r = ev * __builtin_amdgcn_rcpf(-screen_log(uniform01(c[e])));
-      if (r > r1) {
-        r2 = r1;
-        r1 = r;
-        v1 = v;
-      } else if (r > r2) {
-        r2 = r;
+        for (int e = 0; e < 4; ++e) l[u][e] = v0 + e < V ? lg[v0 + e] : 0.f;
       }
     }
-  }
-  float rmax = r1;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    S += __shfl_xor(S, o, 64);
-    rmax = fmaxf(rmax, __shfl_xor(rmax, o, 64));
-  }
-  if (lane == 0) {
-    s_sum[wave] = S;
-    s_f[wave] = rmax;
+    for (int u = 0; u < UNROLL; ++u) {
+      const int c = c0 + u;
+      if (c >= nchunk) break;  // uniform over the block
+      const int q = c * (CHUNK / 4) + tid;  // float4 index = Philox counter word 0
+      const int g = q / (GROUP / 4);
+      float lp[4];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        lp[e] = 4 * q + e < V ? l[u][e] * inv_temp : -INFINITY;
+        mx = fmaxf(mx, lp[e]);
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+      long long sg = 0;
+      if (g < ng) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sg += (long long)rintf(own_exp(lp[e] - mx) * 1099511627776.0f);  // * 2^40
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) sg += __shfl_xor(sg, o, 64);
+      if ((lane & 15) == 0 && g < ng) {
+        s_S[g] = sg;
+        s_m[g] = mx;
+      }
+      uint32_t ctr[4] = {(uint32_t)q, pos, (uint32_t)b, step_id};
+      philox4x32_10(ctr, k0, k1);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (4 * q + e < V) top.add(screen_score(lp[e], uniform01(ctr[e])), 4 * q + e);
+    }
   }
   __syncthreads();
-  rmax = fmaxf(fmaxf(s_f[0], s_f[1]), fmaxf(s_f[2], s_f[3]));
-  const float delta = 1e-3f + 2.4e-6f * (fabsf(mx) + 32.f);   // bound on |log r - (score - m)|, x 100
-  const float w = 1.f - 2.5f * delta;                           // below exp(-2 delta)
-  const bool cand = r1 >= w * rmax;
-  // ---- exact decision among candidates (or all entries if a thread has two)
-  const int multi = __any(r2 >= w * rmax) ? 1 : 0;
-  if (lane == 0) s_flag[wave] = multi;
+
+  // m = max_g m_g; S = sum_g rint(float(S_g) * exp(m_g - m))
+  float mx = -INFINITY;
+  for (int g = tid; g < ng; g += 256) mx = fmaxf(mx, s_m[g]);
+  float amax = top.a1;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+  }
+  if (lane == 0) {
+    s_f[wave] = mx;
+    s_score[wave] = amax;
+  }
+  __syncthreads();
+  mx = fmaxf(fmaxf(s_f[0], s_f[1]), fmaxf(s_f[2], s_f[3]));
+  amax = fmaxf(fmaxf(s_score[0], s_score[1]), fmaxf(s_score[2], s_score[3]));
+  long long S = 0;
+  for (int g = tid; g < ng; g += 256)
+    S += (long long)rintf((float)s_S[g] * own_exp(s_m[g] - mx));
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) S += __shfl_xor(S, o, 64);
+  const float delta = 1e-3f + 2.4e-6f * (fabsf(mx) + 32.f);  // screening error bound, x 100
+  const float lo = amax - 2.5f * delta;
+  const int multi = __any(top.a2 >= lo) ? 1 : 0;
+  __syncthreads();  // every wave has read s_f / s_score
+  if (lane == 0) {
+    s_sum[wave] = S;
+    s_flag[wave] = multi;
+  }
   __syncthreads();
   const bool slow = s_flag[0] | s_flag[1] | s_flag[2] | s_flag[3];
   Best best{-INFINITY, 0x7FFFFFFF};
   if (!slow) {
-    if (cand) best = Best{exact_score(lg, v1, pos, (uint32_t)b, step_id, k0, k1, inv_temp), v1};
+    if (top.a1 >= lo && top.v1 < V) best = Best{exact_score(lg, top.v1, pos, (uint32_t)b, step_id, k0, k1, inv_temp), top.v1};
   } else {
-    for (int g = threadIdx.x; g < ngroups; g += 256) {
-      float l4[4];
-      load4<VEC4>(lg, g, V, l4);
-      uint32_t c[4] = {(uint32_t)g, pos, (uint32_t)b, step_id};
-      philox4x32_10(c, k0, k1);
+    for (int q = tid; 4 * q < V; q += 256) {
+      uint32_t ctr[4] = {(uint32_t)q, pos, (uint32_t)b, step_id};
+      philox4x32_10(ctr, k0, k1);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int v = 4 * g + e;
-        if (!VEC4 && v >= V) break;
-        const float E = -own_log(uniform01(c[e]));
-        const float sc = l4[e] * inv_temp + (-own_log(E));
+        const int v = 4 * q + e;
+        if (v >= V) break;
+        const float sc = exact_score_of(lg[v] * inv_temp, uniform01(ctr[e]));
         if (sc > best.score) best = Best{sc, v};
       }
     }
@@ -256,12 +175,13 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
     const Best other{__shfl_xor(best.score, o, 64), __shfl_xor(best.v, o, 64)};
     best = better(best, other);
   }
+  __syncthreads();
   if (lane == 0) {
     s_score[wave] = best.score;
     s_v[wave] = best.v;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     best = Best{s_score[0], s_v[0]};
     for (int k = 1; k < 4; ++k) best = better(best, Best{s_score[k], s_v[k]});
     S = s_sum[0] + s_sum[1] + s_sum[2] + s_sum[3];
@@ -356,14 +276,11 @@ hipError_t sample_tokens(const float* logits, const int32_t* row_map, const int3
                          uint64_t seed, float inv_temp, int32_t* choice, float* conf, hipStream_t s) {
   const int Lc = L - canvas_off;
   if (B * Lc == 0) return hipSuccess;
+  if (V > SAMPLE_MAX_VOCAB) return hipErrorInvalidValue;
   const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
-  const dim3 grid(Lc, B);
-  if (V % 4 == 0)
-    launch_timed(sample_kernel<true>, grid, dim3(256), 0, s, logits, row_map, canvas, L, canvas_off, Lc, V, mask_id,
-                 pos0, step_id, k0, k1, inv_temp, choice, conf);
-  else
-    launch_timed(sample_kernel<false>, grid, dim3(256), 0, s, logits, row_map, canvas, L, canvas_off, Lc, V,
-                 mask_id, pos0, step_id, k0, k1, inv_temp, choice, conf);
+  const uint32_t lds = (uint32_t)(((V + GROUP - 1) / GROUP) * (sizeof(long long) + sizeof(float)));
+  launch_timed(sample_kernel, dim3(Lc, B), dim3(256), lds, s, logits, row_map, canvas, L, canvas_off, Lc, V, mask_id,
+               pos0, step_id, k0, k1, inv_temp, choice, conf);
   return hipGetLastError();
 }
 

@@ -57,6 +57,10 @@ def test_invalid_arguments_fail_before_device_work():
     bad = tadm.make_config(cfg)
     bad.dtype = 7
     assert tadm.lib.tadm_model_create(C.byref(bad), C.byref(m)) == tadm.TADM_ERR_INVALID
+    bad = tadm.make_config(cfg)
+    bad.vocab = 262144 + 4  # past the sampler's on-chip group partials
+    assert tadm.lib.tadm_model_create(C.byref(bad), C.byref(m)) == tadm.TADM_ERR_INVALID
+    assert "vocab" in tadm.last_error()
     good = tadm.make_config(cfg)
     r, k = C.c_int64(), C.c_int64()
     assert tadm.lib.tadm_weight_info(C.byref(good), 10_000, C.byref(r), C.byref(k)) == tadm.TADM_ERR_INVALID

@@ -39,6 +39,9 @@ def sync():
     (8, 32, 1024, 0, 1.0, False, 1e-3),   # near-equal scores: many rows take the exact fallback
     (4, 16, 256, 0, 1.0, False, 0.0),     # all logits equal: the Gumbel noise alone decides
     (50304, 1, 6, 2, 1.3, False, 30.0),   # wide, peaked distribution
+    (65, 2, 16, 0, 1.0, False, 2.0),      # one normaliser group and one entry
+    (1025, 2, 8, 0, 0.9, False, 4.0),     # one 1024-entry chunk and one entry
+    (262144, 1, 3, 0, 1.0, False, 3.0),   # largest vocabulary: 4096 groups
 ])
 def test_sampler_bit_exact(V, B, L, off, temp, ties, std):
     cfg = synth.get_config("tiny", vocab=V)
@@ -370,6 +373,55 @@ def test_masked_only_head_equals_full_head():
             tadm.tadm_denoise_step(m, None, z, B, L, P, cache, args, None, part)
             sync()
             assert torch.equal(full, part), n_masked
+        tadm.tadm_cache_destroy(cache)
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
+@pytest.mark.parametrize("vocab,d,masked", [
+    (1000, 256, (37, 1)),      # 128 x 128 head tiles; last normaliser group has 40 entries
+    (32768, 768, (50, 9)),     # the small workload's head
+    (262144, 256, (20, 3)),    # largest vocabulary: 256 x 256 head tiles, 4096 groups
+])
+def test_fused_head_sampler_matches_unfused(vocab, d, masked):
+    """The masked-only bf16 head samples in its epilogue.  Token and confidence of every
+    masked position must equal, bit for bit, the standalone sampler on the full logits
+    of the same step, and the oracle's sampling contract applied to those logits."""
+    H = d // 64
+    cfg = synth.get_config("small", n_anchor=1, n_denoise=1, prompt_len=24, gen_len=50, vocab=vocab,
+                           d_model=d, n_heads=H, n_kv_heads=H, d_ffn=2 * d)
+    B, P, G = 3, 24, 50
+    L = P + G
+    tensors = synth.make_weights(cfg, perturb=True)
+    m = gpu_model(cfg, tensors, B, L)
+    try:
+        cache = tadm.tadm_cache_create(m, B, L)
+        z0 = synth.make_teacher_canvas(cfg, G, batch=B, seed=3).to(dev())
+        tadm.tadm_anchor_forward(m, None, z0, B, L, 8, 8, cache)
+        for n_masked in masked:
+            z = synth.make_teacher_canvas(cfg, n_masked, batch=B, seed=n_masked).to(dev())
+            args = tadm.step_args(5, 8, 4, 11, 0xDEAD_BEEF_0042, float(np.float32(1 / 0.9)))
+            got = {}
+            logits = torch.empty(B, G, vocab, device=dev())
+            for name, lg in (("unfused", logits), ("fused", None)):
+                nxt = torch.empty_like(z)
+                ch = torch.empty(B, G, dtype=torch.int32, device=dev())
+                cf = torch.empty(B, G, dtype=torch.float32, device=dev())
+                tadm.tadm_denoise_step(m, None, z, B, L, P, cache, args, lg, nxt)
+                tadm.tadm_debug_read(m, tadm.TAP_CHOICE, ch)
+                tadm.tadm_debug_read(m, tadm.TAP_CONF, cf)
+                sync()
+                got[name] = (nxt.cpu().numpy(), ch.cpu().numpy(), cf.cpu().numpy())
+            msk = z[:, P:].cpu().numpy() == vocab
+            assert msk.sum() == B * n_masked
+            for k in range(3):
+                a, b = got["unfused"][k], got["fused"][k]
+                assert np.array_equal(a.view(np.int32), b.view(np.int32)), (n_masked, k)
+            r_next, r_choice, r_conf = oracle_sample_rows(logits.cpu().numpy(), z.cpu().numpy().astype(np.int64),
+                                                          vocab, 4, 0, P, 11, 0xDEAD_BEEF_0042, args.inv_temp)
+            np.testing.assert_array_equal(got["fused"][1][msk], r_choice[msk])
+            np.testing.assert_array_equal(got["fused"][2].view(np.int32)[msk], r_conf.view(np.int32)[msk])
+            np.testing.assert_array_equal(got["fused"][0], r_next)
         tadm.tadm_cache_destroy(cache)
     finally:
         tadm.tadm_model_destroy(m)

@@ -101,6 +101,38 @@ def test_sample_matches_float64_on_tiny_vocab():
     assert checked > 250
 
 
+@pytest.mark.parametrize("V,std", [(63, 1.0), (64, 1.0), (65, 3.0), (1000, 5.0), (4099, 30.0), (130, 0.0)])
+def test_grouped_normaliser_matches_float64(V, std):
+    """S * 2^-40 approximates sum_v exp(l'_v - m) to float32 accuracy for any number of
+    64-entry groups (partial last group, spreads that hit the -30 cut-off), and the
+    confidence is the float64 log-softmax of the chosen token within that bound."""
+    lg = (rng.normal(size=V) * std).astype(np.float32)
+    m, Sx = S.normaliser(lg)
+    l64 = lg.astype(np.float64)
+    ref = np.exp(l64 - l64.max()).sum()
+    assert m == lg.max()
+    assert abs(Sx * 2.0 ** -40 - ref) <= 4e-7 * ref
+    tok, conf = S.sample_position(lg, 1.0, pos=V, row=1, step_id=2, seed=5)
+    lsm = l64[tok] - l64.max() - math.log(ref)
+    assert abs(conf - lsm) < 2e-6 * (1 + abs(lsm))
+
+
+def test_grouped_normaliser_worked_example():
+    """Hand-worked: 64 equal logits and one more, 1 lower, in a second group.  Group 0
+    sums to 64 * 2^40 exactly; group 1 is 2^40 at its own maximum and is scaled by
+    exp(-1) (a power-of-two multiple of a float32, so already an integer)."""
+    lg = np.zeros(65, np.float32)
+    lg[64] = -1.0
+    m, Sx = S.normaliser(lg)
+    e1 = S.exp32(np.float32(-1.0))
+    assert m == 0.0 and Sx == 64 * 2 ** 40 + int(e1 * np.float32(2.0 ** 40))
+    # equal logits: the normaliser is exactly V and the confidence exactly -log V
+    for V in (1, 64, 130):
+        m, Sx = S.normaliser(np.full(V, 2.5, np.float32))
+        assert Sx == V * 2 ** 40
+        assert S.sample_position(np.full(V, 2.5, np.float32), 1.0, 0, 0, 0, 1)[1] == -S.log32(np.float32(V))
+
+
 def test_gumbel_max_frequencies_match_softmax():
     """Gumbel-max draws follow softmax(l / temp): chi-square over 40000 step ids."""
     lg = np.array([0.3, -1.0, 1.2, 0.0, 2.0, -0.5], dtype=np.float32)
