@@ -47,9 +47,9 @@ def parse():
     ap.add_argument("--out", default=None, help="also write the JSON line to this file")
     ap.add_argument("--render-stats", metavar="DIR", default=None,
                     help="print a markdown summary of the rocprofv3 --stats output under DIR and exit")
-    ap.add_argument("--render-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None,
-                    help="print per-kernel HBM traffic from two rocprofv3 --pmc runs "
-                         "(FETCH_SIZE, then WRITE_SIZE) and exit")
+    ap.add_argument("--render-counters", nargs="+", metavar="DIR", default=None,
+                    help="print per-kernel HBM traffic from two rocprofv3 --pmc runs (FETCH_SIZE, then "
+                         "WRITE_SIZE) and, given a third run with MfmaUtil, the MFMA busy share; then exit")
     ap.add_argument("--command", default="", help="command line quoted in a rendered summary")
     return ap.parse_args()
 
@@ -221,7 +221,7 @@ def counter_rows(d, counter):
     return [r for r in csv.DictReader(open(files[0])) if r["Counter_Name"] == counter]
 
 
-def render_counter_summary(fetch_dir, write_dir, command):
+def render_counter_summary(fetch_dir, write_dir, mfma_dir=None, command=""):
     """HBM traffic per dispatch from FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
     scaled by the ratio of known bytes to the same counter on copy_kernel (one thread per
     16 bytes, grid = bytes / 16 on these shapes) in the same run."""
@@ -248,11 +248,20 @@ def render_counter_summary(fetch_dir, write_dir, command):
           f"(FETCH x{sf:.4f} over {ncf} copies, WRITE x{sw:.4f} over {ncw} copies).  Commands, from the "
           "repository root on one MI355X:\n")
     print(f"```\n{command}\n```\n")
-    print("| kernel | dispatches | read MB | written MB | total MB per dispatch |\n|---|---|---|---|---|")
+    util = defaultdict(list)
+    if mfma_dir:
+        for r in counter_rows(mfma_dir, "MfmaUtil"):
+            util[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+    print("| kernel | dispatches | read MB | written MB | total MB per dispatch | MFMA busy % |\n"
+          "|---|---|---|---|---|---|")
     order = sorted(per.items(), key=lambda kv: -(kv[1][1] + kv[1][3]))
     for name, (nf, bf, nw, bw) in order[:16]:
         rd, wr = bf / max(nf, 1) / 1e6, bw / max(nw, 1) / 1e6
-        print(f"| `{short_name(name)}` | {nf} | {rd:.3f} | {wr:.3f} | {rd + wr:.3f} |")
+        u = f"{sum(util[name]) / len(util[name]):.1f}" if util.get(name) else "-"
+        print(f"| `{short_name(name)}` | {nf} | {rd:.3f} | {wr:.3f} | {rd + wr:.3f} | {u} |")
+    if mfma_dir:
+        print("\nMFMA busy %: rocprofv3's derived MfmaUtil per dispatch (MFMA-busy SIMD cycles over active GPU "
+              "cycles x SIMDs), averaged over the kernel's dispatches in a third run.")
     print("\nPer kernel group (the lines bench.py reads; `sources` hashes the group's kernel sources):\n")
     for desc, names, _, pat, source in KERNELS:
         rx = re.compile(pat)
@@ -272,6 +281,17 @@ def workload_name(cfg):
             f"{cfg['n_anchor']} anchor + {cfg['n_denoise']} denoiser layers, {cfg['fusion_kind']} fusion, "
             f"B={cfg['batch']}, prompt {cfg['prompt_len']} + {cfg['gen_len']} generated "
             f"(block {cfg['block_len']}), T={cfg['T']}")
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def cpu_baseline(cfg, K, budget_s=10.0):
@@ -327,6 +347,7 @@ def cpu_baseline(cfg, K, budget_s=10.0):
     job_s = B * (G // bl) * (n_ref * tr + (T - n_ref) * ts)
     threads = max([t.get("num_threads", 1) for t in threadpool_info()] + [1])
     return {"value": B * G / job_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "host_cpus_available": len(os.sched_getaffinity(0)),
             "sample": f"{rows} of {B} rows, first block, one refresh cycle each (1 refresh step, mean "
                       f"{tr:.2f} s; {min(K, T) - 1} stale steps, mean {ts:.2f} s) at the full shape, "
                       f"{time.perf_counter() - t_start:.1f} s in all; scaled to rows x blocks x ({n_ref} refresh + "
@@ -339,7 +360,7 @@ def main():
         render_stats(args.render_stats, args.command)
         return
     if args.render_counters:
-        render_counter_summary(*args.render_counters, args.command)
+        render_counter_summary(*args.render_counters[:3], command=args.command)
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build runs the path on a single MI355X "

@@ -74,6 +74,8 @@ typedef struct {
   uint32_t step_id;    /* Philox counter word: block * T + (T - i) in tadm_generate  */
   uint64_t seed;       /* Philox key                                                 */
   float inv_temp;      /* 1 / temperature, > 0                                       */
+  const int32_t* n_unmask_rows;  /* nullable device [B]: per-row counts (each >= 0, clamped
+                                    to the row's masked count) used instead of n_unmask  */
 } tadm_step_args;
 
 /* ---------------------------------------------------------------- model ---- */
@@ -148,8 +150,9 @@ tadm_status tadm_denoise_step(tadm_model* m, const tadm_context* ctx, const int3
  * point per group of 64 vocabulary entries relative to the group maximum, and the
  * groups' integer sums are rescaled to the row maximum and added as integers, so the
  * result does not depend on summation order).  Logits must be finite.
- * Per row, the n_unmask masked positions of highest (confidence, then lowest
- * position) take their token; every other entry of canvas_dev is copied.
+ * Per row, the n_unmask (or n_unmask_rows[b]) masked positions of highest
+ * (confidence, then lowest position) take their token; every other entry of
+ * canvas_dev is copied.
  * choice_dev / conf_dev ([B, L - canvas_off], nullable) receive the sampled token
  * and confidence (-1 / -inf where not masked). */
 tadm_status tadm_sample(tadm_model* m, const float* logits_dev, const int32_t* canvas_dev,

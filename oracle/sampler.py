@@ -136,16 +136,18 @@ GROUP = 64  # vocabulary entries per normaliser group
 
 def normaliser(lp):
     """(m, S): the row maximum of the scaled logits lp and the two-level fixed-point
-    normaliser, S ~ 2^40 * sum_v exp(lp_v - m)."""
-    m = lp.max()
-    S = 0
-    for g0 in range(0, lp.shape[0], GROUP):
-        seg = lp[g0:g0 + GROUP]
-        mg = seg.max()
-        Sg = int(np.sum(np.rint(exp32(seg - mg) * F32(2.0 ** 40)).astype(np.int64)))
-        term = F32(F32(Sg) * exp32(F32(mg - m)))
-        S += int(np.rint(term))
-    return m, S
+    normaliser, S ~ 2^40 * sum_v exp(lp_v - m).  The row is padded with -inf to whole
+    groups (exp of -inf - m_g is 0); every group holds at least one real entry."""
+    V = lp.shape[0]
+    ng = -(-V // GROUP)
+    padded = np.full(ng * GROUP, -np.inf, dtype=F32)
+    padded[:V] = lp
+    seg = padded.reshape(ng, GROUP)
+    mg = seg.max(axis=1)                                                     # m_g
+    Sg = np.rint(exp32(seg - mg[:, None]) * F32(2.0 ** 40)).astype(np.int64).sum(axis=1)
+    m = mg.max()
+    terms = np.rint((Sg.astype(F32) * exp32((mg - m).astype(F32))).astype(F32)).astype(np.int64)
+    return m, int(terms.sum())
 
 
 def sample_position(logits_row, inv_temp, pos, row, step_id, seed):

@@ -39,7 +39,8 @@ class tadm_config(C.Structure):
 
 class tadm_step_args(C.Structure):
     _fields_ = [("i", C.c_int32), ("T", C.c_int32), ("n_unmask", C.c_int32),
-                ("step_id", C.c_uint32), ("seed", C.c_uint64), ("inv_temp", C.c_float)]
+                ("step_id", C.c_uint32), ("seed", C.c_uint64), ("inv_temp", C.c_float),
+                ("n_unmask_rows", C.c_void_p)]
 
 
 class TadmError(RuntimeError):
@@ -190,9 +191,11 @@ def tadm_anchor_forward(m, ctx, canvas, B, L, i, T, cache):
     check(lib.tadm_anchor_forward(m, ctx, ptr(canvas), B, L, i, T, cache))
 
 
-def step_args(i, T, n_unmask, step_id, seed, inv_temp):
+def step_args(i, T, n_unmask, step_id, seed, inv_temp, n_unmask_rows=None):
+    """n_unmask_rows: optional device int32 tensor [B] of per-row counts (kept alive by
+    the caller until the step has run)."""
     return tadm_step_args(i=i, T=T, n_unmask=n_unmask, step_id=step_id, seed=seed,
-                          inv_temp=inv_temp)
+                          inv_temp=inv_temp, n_unmask_rows=ptr(n_unmask_rows))
 
 
 def tadm_denoise_step(m, ctx, canvas, B, L, canvas_off, cache, args, logits, next_canvas):

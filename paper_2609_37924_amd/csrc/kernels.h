@@ -174,9 +174,10 @@ constexpr int SAMPLE_MAX_VOCAB = 4096 * 64;
 hipError_t sample_tokens(const float* logits, const int32_t* row_map, const int32_t* canvas, int B,
                          int L, int canvas_off, int V, int mask_id, int pos0, uint32_t step_id,
                          uint64_t seed, float inv_temp, int32_t* choice, float* conf, hipStream_t s);
-// Per row: reveal the n_unmask most confident masked positions; copy the rest.
+// Per row: reveal the n most confident masked positions (n = n_rows[b] if n_rows is
+// set, else n_unmask; clamped to the row's masked count); copy the rest.
 hipError_t select_unmask(const int32_t* canvas, const int32_t* choice, const float* conf, int B,
-                         int L, int canvas_off, int mask_id, int n_unmask, int32_t* next,
+                         int L, int canvas_off, int mask_id, int n_unmask, const int32_t* n_rows, int32_t* next,
                          hipStream_t s);
 
 }  // namespace tadm

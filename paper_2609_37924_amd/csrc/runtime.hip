@@ -1039,7 +1039,7 @@ static tadm_status sample_impl(tadm_model* m, const float* logits, const int32_t
                        a->inv_temp, choice, conf, m->stream));
   TRY(prof_end(m, TADM_STAGE_SAMPLE));
   TRY(prof_begin(m, TADM_STAGE_SELECT));
-  HIPCHK(select_unmask(canvas, choice, conf, B, L, off, mask, a->n_unmask, next, m->stream));
+  HIPCHK(select_unmask(canvas, choice, conf, B, L, off, mask, a->n_unmask, a->n_unmask_rows, next, m->stream));
   TRY(prof_end(m, TADM_STAGE_SELECT));
   return TADM_OK;
 }
@@ -1115,7 +1115,8 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
                          cf.vocab, s.choice, s.conf, m->stream));
   TRY(prof_end(m, TADM_STAGE_SAMPLE));
   TRY(prof_begin(m, TADM_STAGE_SELECT));
-  HIPCHK(select_unmask(canvas, s.choice, s.conf, B, L, off, cf.vocab, a->n_unmask, next, m->stream));
+  HIPCHK(select_unmask(canvas, s.choice, s.conf, B, L, off, cf.vocab, a->n_unmask, a->n_unmask_rows, next,
+                       m->stream));
   TRY(prof_end(m, TADM_STAGE_SELECT));
   return TADM_OK;
 }

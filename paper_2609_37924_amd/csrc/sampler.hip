@@ -229,36 +229,48 @@ __global__ __launch_bounds__(1024) void compact_kernel(const int32_t* canvas, in
   if (threadIdx.x == 0) *count = base;
 }
 
-// one workgroup per row; rank by (conf desc, position asc) among masked positions.
-__global__ __launch_bounds__(256) void select_kernel(const int32_t* canvas, const int32_t* choice,
-                                                     const float* conf, int L, int off, int Lc,
-                                                     int mask_id, int n_unmask, int32_t* next) {
-  extern __shared__ float smem[];
-  float* sc = smem;
-  int* cand = reinterpret_cast<int*>(smem + Lc);
-  __shared__ float red[4];
-  const int b = blockIdx.x;
+// One workgroup of 1024 threads per row; rank by (conf desc, position asc) among the
+// masked positions.  The row's confidences go to LDS with -inf for entries that are not
+// masked (a finite confidence never ranks below them); four threads share a position,
+// each counting the better entries in a quarter of the row with float4 reads, and
+// lanes 4k..4k+3 add their counts.  One workgroup per row keeps the update in place:
+// every canvas read of the row happens before the barrier, and each position is written
+// only by its own threads.
+constexpr int SELECT_THREADS = 1024;
+__global__ __launch_bounds__(SELECT_THREADS) void select_kernel(const int32_t* canvas, const int32_t* choice,
+                                                                const float* conf, int L, int off, int Lc,
+                                                                int mask_id, int n_unmask,
+                                                                const int32_t* n_rows, int32_t* next) {
+  extern __shared__ float sc[];  // Lc rounded up to a multiple of 16, padded with -inf
+  __shared__ float red[SELECT_THREADS / 64];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int Lc16 = (Lc + 15) & ~15, quarter = Lc16 / 4;  // each quarter: whole float4s
   float cnt = 0.f;
-  for (int p = threadIdx.x; p < Lc; p += blockDim.x) {
-    const int m = canvas[(size_t)b * L + off + p] == mask_id;
-    cand[p] = m;
-    sc[p] = conf[(size_t)b * Lc + p];
-    cnt += (float)m;
+  for (int p = tid; p < Lc16; p += SELECT_THREADS) {
+    const bool m = p < Lc && canvas[(size_t)b * L + off + p] == mask_id;
+    sc[p] = m ? conf[(size_t)b * Lc + p] : -INFINITY;
+    cnt += m ? 1.f : 0.f;
   }
-  const int n_masked = (int)block_sum(cnt, red);  // exact: counts < 2^24
-  const int n = min(n_unmask, n_masked);
-  __syncthreads();
-  for (int l = threadIdx.x; l < L; l += blockDim.x) {
-    int t = canvas[(size_t)b * L + l];
-    const int p = l - off;
-    if (p >= 0 && p < Lc && cand[p] && n > 0) {
-      const float cp = sc[p];
-      int rank = 0;
-      for (int q = 0; q < Lc; ++q)
-        rank += (cand[q] && (sc[q] > cp || (sc[q] == cp && q < p))) ? 1 : 0;
-      if (rank < n) t = choice[(size_t)b * Lc + p];
+  const int n_masked = (int)block_sum(cnt, red);  // exact: counts < 2^24; ends with a barrier
+  const int n = min(n_rows ? max(n_rows[b], 0) : n_unmask, n_masked);
+  const int sub = tid & 3;
+  for (int l0 = 0; l0 < L; l0 += SELECT_THREADS / 4) {
+    const int l = l0 + (tid >> 2), p = l - off;
+    const bool mine = l < L;
+    const int t = mine ? canvas[(size_t)b * L + l] : 0;
+    const bool cand = mine && p >= 0 && p < Lc && t == mask_id && n > 0;
+    int rank = 0;
+    if (__any(cand)) {
+      const float cp = cand ? sc[p] : 0.f;
+      for (int q = sub * quarter; q < (sub + 1) * quarter; q += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(sc + q);
+        rank += (v.x > cp || (v.x == cp && q < p)) + (v.y > cp || (v.y == cp && q + 1 < p)) +
+                (v.z > cp || (v.z == cp && q + 2 < p)) + (v.w > cp || (v.w == cp && q + 3 < p));
+      }
+      rank += __shfl_xor(rank, 1, 64);
+      rank += __shfl_xor(rank, 2, 64);
     }
-    next[(size_t)b * L + l] = t;
+    if (mine && sub == 0) next[(size_t)b * L + l] = (cand && rank < n) ? choice[(size_t)b * Lc + p] : t;
   }
 }
 
@@ -285,11 +297,12 @@ hipError_t sample_tokens(const float* logits, const int32_t* row_map, const int3
 }
 
 hipError_t select_unmask(const int32_t* canvas, const int32_t* choice, const float* conf, int B, int L,
-                         int canvas_off, int mask_id, int n_unmask, int32_t* next, hipStream_t s) {
+                         int canvas_off, int mask_id, int n_unmask, const int32_t* n_rows, int32_t* next,
+                         hipStream_t s) {
   const int Lc = L - canvas_off;
   if (B == 0) return hipSuccess;
-  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(256), (size_t)Lc * 8, s, canvas, choice, conf, L,
-                     canvas_off, Lc, mask_id, n_unmask, next);
+  hipLaunchKernelGGL(select_kernel, dim3(B), dim3(SELECT_THREADS), (size_t)((Lc + 15) & ~15) * 4, s, canvas, choice,
+                     conf, L, canvas_off, Lc, mask_id, n_unmask, n_rows, next);
   return hipGetLastError();
 }
 

@@ -11,6 +11,7 @@ import torch
 import synth
 from helpers import dev, gpu_model, oracle_net, oracle_sample_rows, oracle_step, rows_close
 from oracle import loop
+from oracle import sampler as S
 
 pytestmark = pytest.mark.gpu
 
@@ -128,6 +129,36 @@ def _teacher_step_parity(cfg, B, tol, rows=None, seed=0, n_masked=(None, None), 
         for b in rows:
             np.testing.assert_array_equal(nxt2[b].cpu().numpy(), r_next[b])
         tadm.tadm_cache_destroy(cache)
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
+def test_sampler_per_row_counts():
+    """Per-row unmask counts from a device array (clamped to each row's masked count,
+    negative counts reveal nothing) against the oracle step with each row's own n."""
+    V, B, L, off = 512, 5, 48, 6
+    cfg = synth.get_config("tiny", vocab=V)
+    m = tadm.tadm_model_create(tadm.make_config(cfg, max_batch=B, max_seq=L))
+    tadm.tadm_set_stream(m, torch.cuda.current_stream().cuda_stream)
+    try:
+        g = torch.Generator().manual_seed(7)
+        canvas = torch.randint(0, V, (B, L), generator=g, dtype=torch.int32)
+        canvas[:, off:][torch.rand(B, L - off, generator=g) < 0.6] = V
+        logits = synth.make_logits(B * (L - off), V, seed=3, std=2.0).view(B, L - off, V)
+        counts = torch.tensor([0, 3, 1000, -2, 7], dtype=torch.int32)
+        d_counts = counts.to(dev())
+        args = tadm.step_args(3, 8, 99, 4, 77, 1.0, n_unmask_rows=d_counts)
+        d_can = canvas.to(dev())
+        nxt = torch.empty_like(d_can)
+        tadm.tadm_sample(m, logits.to(dev()), d_can, B, L, off, 5, args, nxt)
+        sync()
+        got = nxt.cpu().numpy()
+        for b in range(B):
+            n = max(int(counts[b]), 0)
+            ref_b = S.reverse_step(logits[b].numpy(), canvas[b, off:].numpy().astype(np.int64), V, n, 5 + off, b, 4,
+                                   77, np.float32(1.0))[0]
+            assert np.array_equal(got[b, off:], ref_b), b
+            assert np.array_equal(got[b, :off], canvas[b, :off].numpy())
     finally:
         tadm.tadm_model_destroy(m)
 
