@@ -29,6 +29,21 @@ def unmask_count(M0, i, T):
     return (M0 * i) // T - (M0 * (i - 1)) // T
 
 
+def remask_probs(i, T, eta):
+    """(sigma, p_unmask) of reverse step i under the linear schedule alpha_t = 1 - t,
+    t = i/T, s = (i-1)/T, with the capped remasking probability
+    sigma = min(eta, (1 - alpha_s) / alpha_t): the largest sigma for which the posterior
+    of eq. inf-post-TADM keeps a non-negative mask probability 1 - alpha_s - sigma alpha_t.
+    p_unmask = (alpha_s - (1 - sigma) alpha_t) / (1 - alpha_t).  Computed in float64
+    and returned rounded to float32 (the kernels receive the same two numbers)."""
+    a_t = 1.0 - i / T
+    a_s = 1.0 - (i - 1) / T
+    cap = (1.0 - a_s) / a_t if a_t > 0.0 else float("inf")
+    sigma = min(float(np.float32(eta)), cap)  # eta is a float32 parameter
+    p = (a_s - (1.0 - sigma) * a_t) / (1.0 - a_t)
+    return np.float32(sigma), np.float32(p)
+
+
 def is_refresh(i, T, K):
     return (T - i) % K == 0
 
@@ -41,11 +56,13 @@ class Counts:
 
 
 def generate(net, prompt, gen_len, T, K, block_len, seed, temperature, mask_id,
-             counts=None, trace=None, sample_fn=None):
+             counts=None, trace=None, sample_fn=None, remask_eta=None):
     """Run Algorithm 1 on every row of ``prompt`` [B, P]; returns tokens [B, P+gen_len].
 
-    ``trace`` (list) receives per-step dicts (i, step_id, refresh, canvas before the
-    step) for tests; ``sample_fn`` replaces the reverse step (used by counting tests).
+    ``remask_eta`` selects the remasking posterior with sigma = min(eta, cap) instead of
+    confidence-ranked unmasking.  ``trace`` (list) receives per-step dicts (i, step_id,
+    refresh, canvas before the step) for tests; ``sample_fn`` replaces the reverse step
+    (used by counting tests).
     """
     cfg = net.cfg
     prompt = np.asarray(prompt, dtype=np.int64)
@@ -88,8 +105,13 @@ def generate(net, prompt, gen_len, T, K, block_len, seed, temperature, mask_id,
                 ht = net.fuse(c, caches[b])
                 xf = net.denoise(ht, pos, ctx[b])
                 logits = net.head(xf[c0 - w0:]).astype(np.float32)
-                nxt, _, _ = sample(logits, seq[b, c0:w1], mask_id, n, c0, b, step_id,
-                                   seed, inv_temp)
+                if remask_eta is None:
+                    nxt, _, _ = sample(logits, seq[b, c0:w1], mask_id, n, c0, b, step_id,
+                                       seed, inv_temp)
+                else:
+                    sigma, p_unmask = remask_probs(i, T, remask_eta)
+                    nxt, _ = smp.remask_step(logits, seq[b, c0:w1], mask_id, p_unmask, sigma, c0, b,
+                                             step_id, seed, inv_temp)
                 seq[b, c0:w1] = nxt
         if not single:
             for b in range(B):

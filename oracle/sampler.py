@@ -28,6 +28,15 @@ individually rounded +, -, *, / (no fused multiply-add):
   output tiles) computes the same confidence as one that sees the whole row;
 * ranking key: confidence descending, then position ascending.
 
+Remasking posterior (eq. inf-post-TADM, the ReMDM form with sigma_t > 0), an
+alternative reverse step: each position of the active canvas decides on its own
+with one more uniform, word 0 of Philox4x32-10 at counter (2^31, l, b, step_id) --
+word 0 of the counter never reaches 2^31 for the vocabulary draws.  A decoded
+position becomes the mask with probability sigma_t; a masked position takes its
+Gumbel-max token with probability (alpha_s - (1 - sigma_t) alpha_t) / (1 - alpha_t)
+and stays masked otherwise.  Both probabilities are float32 numbers that the caller
+computes once per step (``loop.remask_probs``); a position moves iff u < probability.
+
 ``log32`` and ``exp32`` are this module's own float32 logarithm and exponential:
 exponent/mantissa split with the mantissa in [sqrt(1/2), sqrt(2)] and the series
 log m = 2 atanh(s), s = (m-1)/(m+1); exponential by Cody-Waite reduction with
@@ -191,3 +200,36 @@ def reverse_step(logits, canvas, mask_id, n_unmask, pos0, row, step_id, seed, in
     nxt = canvas.copy()
     nxt[sel] = choice[sel]
     return nxt, choice, conf
+
+
+DECISION_WORD0 = 0x80000000  # Philox counter word 0 of the per-position decision uniform
+
+
+def decision_uniforms(pos, row, step_id, seed):
+    """One uniform per absolute position in ``pos`` (array) for row ``row`` at a step."""
+    pos = np.asarray(pos, dtype=U32)
+    w = philox4x32_10(np.full(pos.shape, DECISION_WORD0, dtype=U32), pos, U32(row), U32(step_id),
+                      U32(seed & 0xFFFFFFFF), U32((seed >> 32) & 0xFFFFFFFF))
+    return bits_to_uniform(w[0])
+
+
+def remask_step(logits, canvas, mask_id, p_unmask, sigma, pos0, row, step_id, seed, inv_temp):
+    """One reverse step of the remasking posterior for one row of the active canvas.
+
+    logits [Lc, V] float32, canvas [Lc], pos0 = absolute position of canvas entry 0,
+    p_unmask / sigma float32.  Returns (next canvas, choice) with choice -1 where the
+    entry was not masked.
+    """
+    canvas = np.asarray(canvas)
+    Lc = canvas.shape[0]
+    u = decision_uniforms(pos0 + np.arange(Lc), row, step_id, seed)
+    nxt = canvas.copy()
+    choice = np.full(Lc, -1, dtype=np.int64)
+    for j in range(Lc):
+        if canvas[j] == mask_id:
+            choice[j] = sample_position(logits[j], inv_temp, pos0 + j, row, step_id, seed)[0]
+            if u[j] < F32(p_unmask):
+                nxt[j] = choice[j]
+        elif u[j] < F32(sigma):
+            nxt[j] = mask_id
+    return nxt, choice
