@@ -388,8 +388,11 @@ def main():
     prompt = synth.make_prompt(cfg, device=dev) if P else None
     out = torch.empty(B, P + G, dtype=torch.int32, device=dev)
 
+    sampler = [None]  # None: confidence-ranked (the headline); else a tadm_sampler
+
     def gen(K):
-        tadm.tadm_generate(m, prompt, B, P, G, T, K, bl, cfg["sampler_seed"], cfg["temperature"], out)
+        tadm.tadm_generate_sampler(m, prompt, B, P, G, T, K, bl, cfg["sampler_seed"], cfg["temperature"],
+                                   sampler[0], out)
 
     def timed(K, steps, warmup, profile=0, profiled_steps=None):
         """Time `steps` generations.  profile: stage bit mask timed during the last
@@ -445,6 +448,15 @@ def main():
             sweep[f"K={K}"] = {"tokens_per_s": tokens / (kms / 1e3), "ms_per_step": kms}
             print(f"[bench] K={K}: {kms:.3f} ms -> {tokens / (kms / 1e3):.1f} tokens/s", file=sys.stderr,
                   flush=True)
+    # the remasking posterior (capped sigma, eta = 0.04 as in the paper's ReMDM-Cap runs)
+    remask = None
+    if not args.no_sweep:
+        sampler[0] = tadm.remask_sampler(0.04)
+        rms, _, _ = timed(K0, max(2, args.steps // 2), 1)
+        sampler[0] = None
+        remask = {"eta": 0.04, "K": K0, "tokens_per_s": tokens / (rms / 1e3), "ms_per_step": rms}
+        print(f"[bench] remasking sampler eta=0.04, K={K0}: {rms:.3f} ms -> {tokens / (rms / 1e3):.1f} tokens/s",
+              file=sys.stderr, flush=True)
     roof = None
     if dom:
         live = kernel_table(cfg, B, K0, dom_stages)[0]
@@ -471,6 +483,7 @@ def main():
         "config": {"workload": workload_name(cfg), "global_batch": B, "seq_len": P + G, "K": K0,
                    "parallelism": "none (1 GPU)"},
         "k_sweep": sweep,
+        "remask_sampler": remask,
         "stages_ms_per_step": {k: v["ms_per_step"] for k, v in stages.items()},
         "kernels": [{k: v for k, v in r.items() if k != "stages"} for r in kernels],
         "roofline": roof,

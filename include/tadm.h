@@ -76,7 +76,17 @@ typedef struct {
   float inv_temp;      /* 1 / temperature, > 0                                       */
   const int32_t* n_unmask_rows;  /* nullable device [B]: per-row counts (each >= 0, clamped
                                     to the row's masked count) used instead of n_unmask  */
+  int32_t mode;        /* TADM_STEP_RANKED: confidence-ranked unmasking (n_unmask);
+                          TADM_STEP_REMASK: remasking posterior (p_unmask, sigma)    */
+  float p_unmask;      /* REMASK: probability that a masked position takes its token  */
+  float sigma;         /* REMASK: probability that a decoded position is remasked     */
 } tadm_step_args;
+
+/* Reverse-step kinds.  REMASK is the posterior of eq. inf-post-TADM (the ReMDM form,
+ * Sec. 3 and App. B): per canvas position, one uniform u from Philox4x32-10 word 0 at
+ * counter (2^31, absolute position, row, step_id); a masked position becomes its
+ * Gumbel-max token iff u < p_unmask, a decoded one becomes the mask iff u < sigma. */
+enum { TADM_STEP_RANKED = 0, TADM_STEP_REMASK = 1 };
 
 /* ---------------------------------------------------------------- model ---- */
 /* Number of weight tensors of a configuration, and the shape of tensor `index`
@@ -171,6 +181,26 @@ tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, i
 
 /* Pure host helper: n_i of the linear schedule. */
 int32_t tadm_unmask_count(int32_t M0, int32_t i, int32_t T);
+
+/* Sampler of a whole generation.  kind TADM_STEP_RANKED: confidence-ranked unmasking
+ * with the linear schedule (the default of tadm_generate).  kind TADM_STEP_REMASK:
+ * the remasking posterior with sigma_i = min(eta, (1 - alpha_s) / alpha_t), the
+ * largest remasking probability that keeps the posterior's mask probability
+ * 1 - alpha_s - sigma alpha_t non-negative (ReMDM-Cap's form; eta = 0 is the plain
+ * absorbing posterior), on the linear schedule alpha_t = 1 - t. */
+typedef struct {
+  int32_t kind;
+  float eta;
+} tadm_sampler;
+
+/* Pure host helper: (sigma, p_unmask) of reverse step i under the capped schedule,
+ * computed in double and rounded to float. */
+void tadm_remask_probs(int32_t i, int32_t T, float eta, float* sigma, float* p_unmask);
+
+/* tadm_generate with a sampler (NULL: confidence-ranked). */
+tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int32_t B, int32_t P,
+                                  int32_t gen_len, int32_t T, int32_t K, int32_t block_len, uint64_t seed,
+                                  float temperature, const tadm_sampler* sampler, int32_t* tokens_dev);
 
 /* -------------------------------------------------------- observability ---- */
 /* Copies (float32) a buffer of the last step into dst_dev:

@@ -40,7 +40,15 @@ class tadm_config(C.Structure):
 class tadm_step_args(C.Structure):
     _fields_ = [("i", C.c_int32), ("T", C.c_int32), ("n_unmask", C.c_int32),
                 ("step_id", C.c_uint32), ("seed", C.c_uint64), ("inv_temp", C.c_float),
-                ("n_unmask_rows", C.c_void_p)]
+                ("n_unmask_rows", C.c_void_p), ("mode", C.c_int32), ("p_unmask", C.c_float),
+                ("sigma", C.c_float)]
+
+
+class tadm_sampler(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("eta", C.c_float)]
+
+
+STEP_RANKED, STEP_REMASK = 0, 1
 
 
 class TadmError(RuntimeError):
@@ -71,7 +79,10 @@ _SIGS = {
     "tadm_denoise_step": (_I, [_P, _P, _P, _I, _I, _I, _P, C.POINTER(tadm_step_args), _P, _P]),
     "tadm_sample": (_I, [_P, _P, _P, _I, _I, _I, _I, C.POINTER(tadm_step_args), _P, _P, _P]),
     "tadm_generate": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, C.c_uint64, C.c_float, _P]),
+    "tadm_generate_sampler": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, C.c_uint64, C.c_float,
+                                   C.POINTER(tadm_sampler), _P]),
     "tadm_unmask_count": (_I, [_I, _I, _I]),
+    "tadm_remask_probs": (None, [_I, _I, C.c_float, C.POINTER(C.c_float), C.POINTER(C.c_float)]),
     "tadm_debug_read": (_I, [_P, _I, _P, C.c_size_t]),
     "tadm_debug_taps": (_I, [_P, _I]),
     "tadm_profile_enable": (_I, [_P, _I]),
@@ -191,11 +202,15 @@ def tadm_anchor_forward(m, ctx, canvas, B, L, i, T, cache):
     check(lib.tadm_anchor_forward(m, ctx, ptr(canvas), B, L, i, T, cache))
 
 
-def step_args(i, T, n_unmask, step_id, seed, inv_temp, n_unmask_rows=None):
+def step_args(i, T, n_unmask, step_id, seed, inv_temp, n_unmask_rows=None, remask=None):
     """n_unmask_rows: optional device int32 tensor [B] of per-row counts (kept alive by
-    the caller until the step has run)."""
-    return tadm_step_args(i=i, T=T, n_unmask=n_unmask, step_id=step_id, seed=seed,
-                          inv_temp=inv_temp, n_unmask_rows=ptr(n_unmask_rows))
+    the caller until the step has run).  remask: optional (p_unmask, sigma) selecting the
+    remasking posterior instead of confidence-ranked unmasking."""
+    a = tadm_step_args(i=i, T=T, n_unmask=n_unmask, step_id=step_id, seed=seed,
+                       inv_temp=inv_temp, n_unmask_rows=ptr(n_unmask_rows))
+    if remask is not None:
+        a.mode, a.p_unmask, a.sigma = STEP_REMASK, remask[0], remask[1]
+    return a
 
 
 def tadm_denoise_step(m, ctx, canvas, B, L, canvas_off, cache, args, logits, next_canvas):
@@ -213,8 +228,25 @@ def tadm_generate(m, prompt, B, P, gen_len, T, K, block_len, seed, temperature, 
                             ptr(tokens)))
 
 
+def tadm_generate_sampler(m, prompt, B, P, gen_len, T, K, block_len, seed, temperature, sampler, tokens):
+    """sampler: None (confidence-ranked) or a tadm_sampler."""
+    check(lib.tadm_generate_sampler(m, ptr(prompt), B, P, gen_len, T, K, block_len, seed, temperature,
+                                    C.byref(sampler) if sampler is not None else None, ptr(tokens)))
+
+
+def remask_sampler(eta):
+    return tadm_sampler(kind=STEP_REMASK, eta=eta)
+
+
 def tadm_unmask_count(M0, i, T):
     return lib.tadm_unmask_count(M0, i, T)
+
+
+def tadm_remask_probs(i, T, eta):
+    """(sigma, p_unmask) as float32 values computed by the library."""
+    sg, pu = C.c_float(), C.c_float()
+    lib.tadm_remask_probs(i, T, eta, C.byref(sg), C.byref(pu))
+    return sg.value, pu.value
 
 
 def tadm_debug_read(m, tap, dst):

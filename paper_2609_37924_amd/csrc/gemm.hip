@@ -28,11 +28,19 @@ struct Epi<EPI_STORE_F32, T> {
 template <class T>
 struct Epi<EPI_RESID, T> {
   static constexpr bool kGlu = false;
-  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
-    float4* r = reinterpret_cast<float4*>(e.resid + (size_t)m * e.ldr + n);
-    float4 x = *r;
+  static constexpr int kPre = 1;
+  __device__ static void pre(const EpiParams& e, int m, int n, float4* o) {
+    o[0] = *reinterpret_cast<const float4*>(e.resid + (size_t)m * e.ldr + n);
+  }
+  __device__ static void apply_pre(const EpiParams& e, int m, int n, f32x4 v, const float4* o) {
+    float4 x = o[0];
     x.x += v[0]; x.y += v[1]; x.z += v[2]; x.w += v[3];
-    *r = x;
+    *reinterpret_cast<float4*>(e.resid + (size_t)m * e.ldr + n) = x;
+  }
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    float4 o;
+    pre(e, m, n, &o);
+    apply_pre(e, m, n, v, &o);
   }
 };
 template <class T>

@@ -32,6 +32,15 @@ struct TileEpi : std::false_type {};
 template <class E>
 struct TileEpi<E, std::void_t<decltype(E::kTile)>> : std::true_type {};
 
+// An epilogue that reads other tensors may define kPre (float4 loads per fragment),
+// pre() and apply_pre(): the kernel then issues those loads before the main loop,
+// where their latency hides behind the K tiles, when the tile keeps them in at most
+// 16 float4 registers per lane.
+template <class E, class = void>
+struct PreCount { static constexpr int value = 0; };
+template <class E>
+struct PreCount<E, std::void_t<decltype(E::kPre)>> { static constexpr int value = E::kPre; };
+
 // waitcnt immediate for "at most n vector-memory operations outstanding" (gfx9 encoding)
 constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
 
@@ -115,6 +124,22 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
 #pragma unroll
     for (int b = 0; b < TM; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // epilogue operands, loaded before the K tiles so that they are the oldest
+  // vector-memory operations (the vmcnt waits below only ever wait for older ones)
+  constexpr int NPRE = PreCount<E>::value;
+  constexpr bool PRE = NPRE > 0 && TN * TM * NPRE <= 16;
+  float4 pre[PRE ? TN : 1][PRE ? TM : 1][PRE ? NPRE : 1];
+  if constexpr (PRE) {
+    const int mw0 = m0 + wm * WTM + (lane & 15), nw0 = n0 + wn * WTN + 4 * (lane >> 4);
+#pragma unroll
+    for (int a = 0; a < TN; ++a)
+#pragma unroll
+      for (int b = 0; b < TM; ++b) {
+        const int m = mw0 + b * 16, n = nw0 + a * 16;
+        if (m < p.M && n < p.N) E::pre(ep, m, n, pre[a][b]);
+      }
+  }
+
   const int nk = p.K / 64;
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
@@ -168,7 +193,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
 #pragma unroll
       for (int b = 0; b < TM; ++b) {
         const int m = mw + b * 16, n = nw + a * 16;
-        if (m < p.M && n < p.N) E::apply(ep, m, n, acc[a][b]);
+        if (m < p.M && n < p.N) {
+          if constexpr (PRE)
+            E::apply_pre(ep, m, n, acc[a][b], pre[a][b]);
+          else
+            E::apply(ep, m, n, acc[a][b]);
+        }
       }
   }
 }

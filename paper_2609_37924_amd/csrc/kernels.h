@@ -166,6 +166,12 @@ hipError_t head_sample(const GemmProblem& p, const EpiParams& e, hipStream_t s);
 hipError_t sample_finalize(const SamplePart* part, int n_groups, int V, const int32_t* row_map,
                            const int32_t* canvas, int B, int L, int canvas_off, int mask_id, int32_t* choice,
                            float* conf, hipStream_t s);
+// Remasking posterior: per entry of canvas rows [b, off + j), one uniform u = Philox
+// word 0 at counter (2^31, pos0 + off + j, b, step_id); masked -> choice iff
+// u < p_unmask, decoded -> mask iff u < sigma; columns before off are copied.
+hipError_t remask_update(const int32_t* canvas, const int32_t* choice, int B, int L, int canvas_off, int mask_id,
+                         int pos0, uint32_t step_id, uint64_t seed, float p_unmask, float sigma, int32_t* next,
+                         hipStream_t s);
 // Largest vocabulary the sampler handles: its per-group partials (64 entries per
 // group, 12 bytes each) live in 48 KB of LDS.
 constexpr int SAMPLE_MAX_VOCAB = 4096 * 64;

@@ -717,7 +717,25 @@ static tadm_status check_args(const tadm_step_args* a, int Lc) {
   if (a->T < 1 || a->i < 1 || a->i > a->T) return fail(TADM_ERR_INVALID, "step i=%d T=%d", a->i, a->T);
   if (a->n_unmask < 0) return fail(TADM_ERR_INVALID, "negative n_unmask");
   if (!(a->inv_temp > 0) || !std::isfinite(a->inv_temp)) return fail(TADM_ERR_INVALID, "inv_temp must be finite and > 0");
+  if (a->mode != TADM_STEP_RANKED && a->mode != TADM_STEP_REMASK) return fail(TADM_ERR_INVALID, "step mode %d", a->mode);
+  if (a->mode == TADM_STEP_REMASK && !(a->p_unmask >= 0.f && a->p_unmask <= 1.f && a->sigma >= 0.f && a->sigma <= 1.f))
+    return fail(TADM_ERR_INVALID, "remasking probabilities must lie in [0, 1]");
   (void)Lc;
+  return TADM_OK;
+}
+
+// The step's canvas update from the sampled tokens: confidence-ranked unmasking or the
+// remasking posterior.
+static tadm_status canvas_update(tadm_model* m, const int32_t* canvas, const int32_t* choice, const float* conf,
+                                 int B, int L, int off, int pos0, const tadm_step_args* a, int32_t* next) {
+  TRY(prof_begin(m, TADM_STAGE_SELECT));
+  if (a->mode == TADM_STEP_REMASK)
+    HIPCHK(remask_update(canvas, choice, B, L, off, m->cfg.vocab, pos0, a->step_id, a->seed, a->p_unmask, a->sigma,
+                         next, m->stream));
+  else
+    HIPCHK(select_unmask(canvas, choice, conf, B, L, off, m->cfg.vocab, a->n_unmask, a->n_unmask_rows, next,
+                         m->stream));
+  TRY(prof_end(m, TADM_STAGE_SELECT));
   return TADM_OK;
 }
 
@@ -1038,10 +1056,7 @@ static tadm_status sample_impl(tadm_model* m, const float* logits, const int32_t
   HIPCHK(sample_tokens(logits, row_map, canvas, B, L, off, m->cfg.vocab, mask, pos0, a->step_id, a->seed,
                        a->inv_temp, choice, conf, m->stream));
   TRY(prof_end(m, TADM_STAGE_SAMPLE));
-  TRY(prof_begin(m, TADM_STAGE_SELECT));
-  HIPCHK(select_unmask(canvas, choice, conf, B, L, off, mask, a->n_unmask, a->n_unmask_rows, next, m->stream));
-  TRY(prof_end(m, TADM_STAGE_SELECT));
-  return TADM_OK;
+  return canvas_update(m, canvas, choice, conf, B, L, off, pos0, a, next);
 }
 
 // One reverse step.  With caller logits every canvas row goes through the head;
@@ -1114,11 +1129,7 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
   HIPCHK(sample_finalize(reinterpret_cast<const SamplePart*>(s.logits), ng, cf.vocab, s.row_map, canvas, B, L, off,
                          cf.vocab, s.choice, s.conf, m->stream));
   TRY(prof_end(m, TADM_STAGE_SAMPLE));
-  TRY(prof_begin(m, TADM_STAGE_SELECT));
-  HIPCHK(select_unmask(canvas, s.choice, s.conf, B, L, off, cf.vocab, a->n_unmask, a->n_unmask_rows, next,
-                       m->stream));
-  TRY(prof_end(m, TADM_STAGE_SELECT));
-  return TADM_OK;
+  return canvas_update(m, canvas, s.choice, s.conf, B, L, off, pos0, a, next);
 }
 
 tadm_status tadm_denoise_step(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev, int32_t B,
@@ -1154,10 +1165,29 @@ tadm_status tadm_sample(tadm_model* m, const float* logits_dev, const int32_t* c
 // --------------------------------------------------------------- generate ---
 // Algorithm 1 per block; the model-owned cache, context and window are reused
 // across calls, so a warm generation allocates nothing and never synchronises.
+void tadm_remask_probs(int32_t i, int32_t T, float eta, float* sigma, float* p_unmask) {
+  const double a_t = 1.0 - (double)i / T, a_s = 1.0 - (double)(i - 1) / T;
+  const double cap = a_t > 0.0 ? (1.0 - a_s) / a_t : INFINITY;
+  const double sg = std::min((double)eta, cap);
+  if (sigma) *sigma = (float)sg;
+  if (p_unmask) *p_unmask = (float)((a_s - (1.0 - sg) * a_t) / (1.0 - a_t));
+}
+
 tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, int32_t P, int32_t gen_len,
                           int32_t T, int32_t K, int32_t block_len, uint64_t seed, float temperature,
                           int32_t* tokens_dev) {
+  return tadm_generate_sampler(m, prompt_dev, B, P, gen_len, T, K, block_len, seed, temperature, nullptr,
+                               tokens_dev);
+}
+
+tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int32_t B, int32_t P, int32_t gen_len,
+                                  int32_t T, int32_t K, int32_t block_len, uint64_t seed, float temperature,
+                                  const tadm_sampler* sampler, int32_t* tokens_dev) {
   TRY(check_model(m));
+  const bool remask = sampler && sampler->kind == TADM_STEP_REMASK;
+  if (sampler && sampler->kind != TADM_STEP_RANKED && !remask)
+    return fail(TADM_ERR_INVALID, "sampler kind %d", sampler->kind);
+  if (remask && !(sampler->eta >= 0.f && sampler->eta <= 1.f)) return fail(TADM_ERR_INVALID, "eta outside [0, 1]");
   if (!tokens_dev || (P > 0 && !prompt_dev)) return fail(TADM_ERR_INVALID, "null argument");
   if (B < 1 || B > m->cfg.max_batch) return fail(TADM_ERR_INVALID, "B=%d outside [1, %d]", B, m->cfg.max_batch);
   if (P < 0 || gen_len < 1 || block_len < 1 || gen_len % block_len)
@@ -1175,19 +1205,25 @@ tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, i
   a.T = T;
   a.seed = seed;
   a.inv_temp = (float)(1.0 / (double)temperature);
+  a.mode = remask ? TADM_STEP_REMASK : TADM_STEP_RANKED;
+  // masked positions entering step i: exactly B floor(M0 i / T) for the ranked sampler;
+  // any number up to B M0 under remasking
+  auto masked_bound = [&](int M0, int i) { return remask ? B * M0 : (int)(B * (((int64_t)M0 * i) / T)); };
+  auto set_step = [&](int M0, int i) {
+    a.i = i;
+    a.n_unmask = tadm_unmask_count(M0, i, T);
+    if (remask) tadm_remask_probs(i, T, sampler->eta, &a.sigma, &a.p_unmask);
+  };
   HIPCHK(init_canvas(prompt_dev, B, P, gen_len, mask, tokens_dev, m->stream));
   tadm_cache* cache = m->gcache;
   if (single) {
     cache->B = B;
     cache->L = L;
     for (int i = T; i >= 1; --i) {
-      a.i = i;
+      set_step(gen_len, i);
       a.step_id = (uint32_t)(T - i);
-      a.n_unmask = tadm_unmask_count(gen_len, i, T);
       if ((T - i) % K == 0) TRY(anchor_impl(m, nullptr, tokens_dev, B, L, i, cache));
-      // every row started with gen_len masked positions and reveals n_i per step
-      const int masked = (int)(((int64_t)gen_len * i) / T);
-      TRY(denoise_impl(m, nullptr, tokens_dev, B, L, P, cache, &a, nullptr, tokens_dev, B * masked));
+      TRY(denoise_impl(m, nullptr, tokens_dev, B, L, P, cache, &a, nullptr, tokens_dev, masked_bound(gen_len, i)));
     }
     return TADM_OK;
   }
@@ -1207,12 +1243,10 @@ tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, i
   for (int j = 0; j < nblocks; ++j) {
     HIPCHK(fill_i32(win, (size_t)B * block_len, mask, m->stream));
     for (int i = T; i >= 1; --i) {
-      a.i = i;
+      set_step(block_len, i);
       a.step_id = (uint32_t)(j * T + (T - i));
-      a.n_unmask = tadm_unmask_count(block_len, i, T);
       if ((T - i) % K == 0) TRY(anchor_impl(m, ctx, win, B, block_len, i, cache));
-      const int masked = (int)(((int64_t)block_len * i) / T);
-      TRY(denoise_impl(m, ctx, win, B, block_len, 0, cache, &a, nullptr, win, B * masked));
+      TRY(denoise_impl(m, ctx, win, B, block_len, 0, cache, &a, nullptr, win, masked_bound(block_len, i)));
     }
     HIPCHK(hipMemcpy2DAsync(tokens_dev + P + j * block_len, (size_t)L * 4, win, (size_t)block_len * 4,
                             (size_t)block_len * 4, B, hipMemcpyDeviceToDevice, m->stream));

@@ -274,7 +274,39 @@ __global__ __launch_bounds__(SELECT_THREADS) void select_kernel(const int32_t* c
   }
 }
 
+// grid (ceil(L / 256), B): one thread per canvas entry; in place (each entry is read and
+// written by its own thread).
+__global__ __launch_bounds__(256) void remask_kernel(const int32_t* canvas, const int32_t* choice, int L, int off,
+                                                     int mask_id, int pos0, uint32_t step_id, uint32_t k0,
+                                                     uint32_t k1, float p_unmask, float sigma, int32_t* next) {
+  const int l = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
+  if (l >= L) return;
+  const int t = canvas[(size_t)b * L + l];
+  int nt = t;
+  if (l >= off) {
+    const int j = l - off, Lc = L - off;
+    uint32_t c[4] = {0x80000000u, (uint32_t)(pos0 + l), (uint32_t)b, step_id};
+    philox4x32_10(c, k0, k1);
+    const float u = uniform01(c[0]);
+    if (t == mask_id)
+      nt = u < p_unmask ? choice[(size_t)b * Lc + j] : mask_id;
+    else if (u < sigma)
+      nt = mask_id;
+  }
+  next[(size_t)b * L + l] = nt;
+}
+
 }  // namespace
+
+hipError_t remask_update(const int32_t* canvas, const int32_t* choice, int B, int L, int canvas_off, int mask_id,
+                         int pos0, uint32_t step_id, uint64_t seed, float p_unmask, float sigma, int32_t* next,
+                         hipStream_t s) {
+  if (B * L == 0) return hipSuccess;
+  const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
+  hipLaunchKernelGGL(remask_kernel, dim3((L + 255) / 256, B), dim3(256), 0, s, canvas, choice, L, canvas_off, mask_id,
+                     pos0, step_id, k0, k1, p_unmask, sigma, next);
+  return hipGetLastError();
+}
 
 hipError_t compact_masked(const int32_t* canvas, int B, int L, int canvas_off, int mask_id,
                           int32_t* idx, int32_t* row_map, int* count, hipStream_t s) {

@@ -5,6 +5,7 @@ import ctypes as C
 import os
 import re
 
+import numpy as np
 import pytest
 
 import synth
@@ -72,3 +73,14 @@ def test_invalid_arguments_fail_before_device_work():
     assert tadm.lib.tadm_context_reset(None) == tadm.TADM_ERR_INVALID
     with pytest.raises(tadm.TadmError):
         tadm.check(tadm.lib.tadm_model_destroy(None))
+
+
+def test_remask_probs_match_the_oracle():
+    """The library's per-step (sigma, p_unmask) are the oracle's float32 numbers."""
+    from oracle import loop
+    for T in (1, 7, 16, 64, 128, 1024):
+        for eta in (0.0, 0.02, 0.04, 0.3, 1.0):
+            for i in sorted({1, 2, 3, T // 2 or 1, T - 1 or 1, T}):
+                sg, pu = tadm.tadm_remask_probs(i, T, eta)
+                rs, rp = loop.remask_probs(i, T, eta)
+                assert np.float32(sg) == rs and np.float32(pu) == rp, (i, T, eta)

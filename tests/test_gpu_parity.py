@@ -163,6 +163,34 @@ def test_sampler_per_row_counts():
         tadm.tadm_model_destroy(m)
 
 
+@pytest.mark.parametrize("V,off,sigma,p_unmask", [(300, 5, 0.3, 0.6), (64, 0, 0.0, 0.125), (1001, 3, 0.04, 1.0)])
+def test_remask_step_bit_exact(V, off, sigma, p_unmask):
+    """Remasking posterior on given logits: every entry's move (unmask to its Gumbel-max
+    token, stay masked, keep, remask) equals the oracle's bit for bit."""
+    B, L = 4, 40
+    cfg = synth.get_config("tiny", vocab=V)
+    m = tadm.tadm_model_create(tadm.make_config(cfg, max_batch=B, max_seq=L))
+    tadm.tadm_set_stream(m, torch.cuda.current_stream().cuda_stream)
+    try:
+        g = torch.Generator().manual_seed(V)
+        canvas = torch.randint(0, V, (B, L), generator=g, dtype=torch.int32)
+        canvas[:, off:][torch.rand(B, L - off, generator=g) < 0.5] = V
+        logits = synth.make_logits(B * (L - off), V, seed=V, std=2.0).view(B, L - off, V)
+        sg, pu = np.float32(sigma), np.float32(p_unmask)
+        args = tadm.step_args(5, 16, 0, 9, 0xABCDEF, 1.0, remask=(float(pu), float(sg)))
+        d_can = canvas.to(dev())
+        nxt = torch.empty_like(d_can)
+        tadm.tadm_sample(m, logits.to(dev()), d_can, B, L, off, 12, args, nxt)
+        sync()
+        for b in range(B):
+            ref, _ = S.remask_step(logits[b].numpy(), canvas[b, off:].numpy().astype(np.int64), V, pu, sg, 12 + off, b,
+                                   9, 0xABCDEF, np.float32(1.0))
+            assert np.array_equal(nxt[b, off:].cpu().numpy(), ref), b
+            assert np.array_equal(nxt[b, :off].cpu().numpy(), canvas[b, :off].numpy())
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
 def test_tiny_fp32_step_parity():
     _teacher_step_parity(synth.get_config("tiny", batch=2), 2, FP32_TOL)
 
@@ -330,6 +358,30 @@ def test_tiny_generation_matches_oracle(K):
     np.testing.assert_array_equal(got, ref)
 
 
+@pytest.mark.parametrize("eta,block", [(0.04, False), (0.5, False), (0.3, True)])
+def test_tiny_remask_generation_matches_oracle(eta, block):
+    """Whole generations with the remasking sampler (capped sigma) are token-identical
+    to the oracle's Algorithm 1 with the same posterior, and end fully unmasked."""
+    cfg = synth.get_config("tiny", batch=2, n_kv_heads=2 if block else 4)
+    K = 4
+    B, P, G, T = 2, cfg["prompt_len"], cfg["gen_len"], cfg["T"]
+    bl = 8 if block else G
+    tensors = synth.make_weights(cfg, perturb=True)
+    prompt = synth.make_prompt(cfg, batch=B)
+    m = gpu_model(cfg, tensors, B, P + G)
+    try:
+        out = torch.empty(B, P + G, dtype=torch.int32, device=dev())
+        tadm.tadm_generate_sampler(m, prompt.to(dev()), B, P, G, T, K, bl, 2, 1.0, tadm.remask_sampler(eta), out)
+        sync()
+        got = out.cpu().numpy()
+    finally:
+        tadm.tadm_model_destroy(m)
+    net = oracle_net(cfg, tensors)
+    ref = loop.generate(net, prompt.numpy(), G, T, K, bl, 2, 1.0, synth.mask_id(cfg), remask_eta=eta)
+    np.testing.assert_array_equal(got, ref)
+    assert (got != synth.mask_id(cfg)).all()
+
+
 def test_tiny_block_generation_matches_oracle():
     cfg = synth.get_config("tiny", batch=2, n_kv_heads=2)
     tensors, prompt, got = _generate(cfg, 4, block_len=8)
@@ -453,6 +505,18 @@ def test_fused_head_sampler_matches_unfused(vocab, d, masked):
             np.testing.assert_array_equal(got["fused"][1][msk], r_choice[msk])
             np.testing.assert_array_equal(got["fused"][2].view(np.int32)[msk], r_conf.view(np.int32)[msk])
             np.testing.assert_array_equal(got["fused"][0], r_next)
+            # the remasking posterior on top of the fused head: same bits as from the logits
+            rargs = tadm.step_args(5, 8, 0, 11, 0xDEAD_BEEF_0042, float(np.float32(1 / 0.9)), remask=(0.4, 0.2))
+            nx = {}
+            for name, lg in (("unfused", logits), ("fused", None)):
+                nx[name] = torch.empty_like(z)
+                tadm.tadm_denoise_step(m, None, z, B, L, P, cache, rargs, lg, nx[name])
+            sync()
+            assert torch.equal(nx["unfused"], nx["fused"]), n_masked
+            r_next = np.stack([S.remask_step(logits[b].cpu().numpy(), z[b, P:].cpu().numpy().astype(np.int64), vocab,
+                                             np.float32(0.4), np.float32(0.2), P, b, 11, 0xDEAD_BEEF_0042,
+                                             np.float32(rargs.inv_temp))[0] for b in range(B)])
+            np.testing.assert_array_equal(nx["fused"][:, P:].cpu().numpy(), r_next)
         tadm.tadm_cache_destroy(cache)
     finally:
         tadm.tadm_model_destroy(m)
