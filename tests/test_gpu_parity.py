@@ -382,6 +382,33 @@ def test_tiny_remask_generation_matches_oracle(eta, block):
     assert (got != synth.mask_id(cfg)).all()
 
 
+@pytest.mark.parametrize("T,K,block_len,temp", [
+    (1, 1, None, 1.0),     # a single reverse step reveals everything
+    (40, 3, None, 0.5),    # more steps than positions: many steps reveal nothing; K does not divide T
+    (16, 50, None, 2.0),   # K > T: only the first step refreshes the anchor
+    (6, 2, 1, 1.0),        # one-token blocks, each appended to the context
+])
+def test_degenerate_schedules_match_oracle(T, K, block_len, temp):
+    """Schedule edge cases of Algorithm 1 and the linear unmask count, token-identical to
+    the oracle."""
+    cfg = synth.get_config("tiny", batch=2, n_kv_heads=2)
+    B, P, G = 2, cfg["prompt_len"], cfg["gen_len"]
+    bl = block_len or G
+    tensors = synth.make_weights(cfg, perturb=True)
+    prompt = synth.make_prompt(cfg, batch=B)
+    m = gpu_model(cfg, tensors, B, P + G)
+    try:
+        out = torch.empty(B, P + G, dtype=torch.int32, device=dev())
+        tadm.tadm_generate(m, prompt.to(dev()), B, P, G, T, K, bl, 5, temp, out)
+        sync()
+        got = out.cpu().numpy()
+    finally:
+        tadm.tadm_model_destroy(m)
+    ref = loop.generate(oracle_net(cfg, tensors), prompt.numpy(), G, T, K, bl, 5, temp, synth.mask_id(cfg))
+    np.testing.assert_array_equal(got, ref)
+    assert (got != synth.mask_id(cfg)).all()
+
+
 def test_tiny_block_generation_matches_oracle():
     cfg = synth.get_config("tiny", batch=2, n_kv_heads=2)
     tensors, prompt, got = _generate(cfg, 4, block_len=8)
