@@ -56,11 +56,11 @@ class Counts:
 
 
 def generate(net, prompt, gen_len, T, K, block_len, seed, temperature, mask_id,
-             counts=None, trace=None, sample_fn=None, remask_eta=None):
+             counts=None, trace=None, sample_fn=None, remask_eta=None, top_p=1.0):
     """Run Algorithm 1 on every row of ``prompt`` [B, P]; returns tokens [B, P+gen_len].
 
     ``remask_eta`` selects the remasking posterior with sigma = min(eta, cap) instead of
-    confidence-ranked unmasking.  ``trace`` (list) receives per-step dicts (i, step_id,
+    confidence-ranked unmasking; ``top_p`` < 1 samples its tokens from the nucleus.  ``trace`` (list) receives per-step dicts (i, step_id,
     refresh, canvas before the step) for tests; ``sample_fn`` replaces the reverse step
     (used by counting tests).
     """
@@ -111,7 +111,7 @@ def generate(net, prompt, gen_len, T, K, block_len, seed, temperature, mask_id,
                 else:
                     sigma, p_unmask = remask_probs(i, T, remask_eta)
                     nxt, _ = smp.remask_step(logits, seq[b, c0:w1], mask_id, p_unmask, sigma, c0, b,
-                                             step_id, seed, inv_temp)
+                                             step_id, seed, inv_temp, top_p)
                 seq[b, c0:w1] = nxt
         if not single:
             for b in range(B):

@@ -28,6 +28,14 @@ individually rounded +, -, *, / (no fused multiply-add):
   output tiles) computes the same confidence as one that sees the whole row;
 * ranking key: confidence descending, then position ascending.
 
+Nucleus truncation (top-p, used with the remasking sampler): with m = max l', each
+entry has the fixed-point weight q_v = rint(exp(l'_v - m) 2^40) (int64) and Q = sum_v q_v.
+The nucleus is {v : q_v >= tau}, tau the largest weight whose tail sum
+sum_{q_v >= tau} q_v reaches ceil(p Q) (p a float32, the product exact), i.e. the
+highest-probability entries until their mass reaches p, with every entry tied at the
+boundary kept.  The token is the Gumbel-max over the nucleus; the confidence stays the
+untruncated log-probability.
+
 Remasking posterior (eq. inf-post-TADM, the ReMDM form with sigma_t > 0), an
 alternative reverse step: each position of the active canvas decides on its own
 with one more uniform, word 0 of Philox4x32-10 at counter (2^31, l, b, step_id) --
@@ -159,7 +167,20 @@ def normaliser(lp):
     return m, int(terms.sum())
 
 
-def sample_position(logits_row, inv_temp, pos, row, step_id, seed):
+def nucleus(lp, top_p):
+    """Boolean mask of the top-p nucleus of the scaled logits lp (module docstring)."""
+    m = lp.max()
+    q = np.rint(exp32(lp - m) * F32(2.0 ** 40)).astype(np.int64)
+    Q = int(q.sum())
+    num, den = float(np.float32(top_p)).as_integer_ratio()
+    target = -(-(num * Q) // den)                         # ceil(p Q), exact
+    qs = np.sort(q)[::-1]
+    idx = int(np.searchsorted(np.cumsum(qs), target))     # first prefix whose sum >= target
+    tau = int(qs[min(idx, qs.size - 1)])
+    return q >= tau
+
+
+def sample_position(logits_row, inv_temp, pos, row, step_id, seed, top_p=1.0):
     """(token, confidence) for one masked position; logits_row is float32 [V]."""
     lg = np.asarray(logits_row, dtype=F32)
     V = lg.shape[0]
@@ -167,6 +188,8 @@ def sample_position(logits_row, inv_temp, pos, row, step_id, seed):
     u = uniforms(V, pos, row, step_id, seed)
     gumbel = -log32(-log32(u))
     score = lp + gumbel
+    if np.float32(top_p) < 1.0:
+        score = np.where(nucleus(lp, top_p), score, -np.inf)
     tok = int(np.argmax(score))            # first maximum: smallest v on ties
     m, S = normaliser(lp)
     norm = F32(np.int64(S).astype(F32)) * F32(2.0 ** -40)
@@ -213,7 +236,7 @@ def decision_uniforms(pos, row, step_id, seed):
     return bits_to_uniform(w[0])
 
 
-def remask_step(logits, canvas, mask_id, p_unmask, sigma, pos0, row, step_id, seed, inv_temp):
+def remask_step(logits, canvas, mask_id, p_unmask, sigma, pos0, row, step_id, seed, inv_temp, top_p=1.0):
     """One reverse step of the remasking posterior for one row of the active canvas.
 
     logits [Lc, V] float32, canvas [Lc], pos0 = absolute position of canvas entry 0,
@@ -227,7 +250,7 @@ def remask_step(logits, canvas, mask_id, p_unmask, sigma, pos0, row, step_id, se
     choice = np.full(Lc, -1, dtype=np.int64)
     for j in range(Lc):
         if canvas[j] == mask_id:
-            choice[j] = sample_position(logits[j], inv_temp, pos0 + j, row, step_id, seed)[0]
+            choice[j] = sample_position(logits[j], inv_temp, pos0 + j, row, step_id, seed, top_p)[0]
             if u[j] < F32(p_unmask):
                 nxt[j] = choice[j]
         elif u[j] < F32(sigma):

@@ -80,3 +80,54 @@ def test_chain_preserves_the_forward_marginal():
             assert abs(frac - expect) < 5 * math.sqrt(max(expect * (1 - expect), 1e-9) / Lc) + 1e-9
             assert abs(frac - (i - 1) / T) < 0.06, (eta, i, frac)
         assert (z != V).all()
+
+
+def test_nucleus_matches_the_sorted_cumulative_definition():
+    """Away from the boundary the fixed-point nucleus is the float64 textbook one: the
+    smallest set of highest-probability entries whose mass reaches p."""
+    rng = np.random.default_rng(8)
+    checked = 0
+    for trial in range(200):
+        V = int(rng.integers(3, 300))
+        lp = (rng.normal(size=V) * rng.uniform(0.3, 4)).astype(np.float32)
+        p = float(rng.uniform(0.05, 0.99))
+        got = S.nucleus(lp, p)
+        pr = np.exp(lp.astype(np.float64) - lp.max())
+        pr /= pr.sum()
+        order = np.argsort(-pr, kind="stable")
+        cum = np.cumsum(pr[order])
+        k = int(np.searchsorted(cum, p)) + 1               # entries needed to reach p
+        if k < V and (cum[k - 1] - p > 1e-6) and (k < 2 or p - cum[k - 2] > 1e-6) and \
+                (k == V or pr[order[k - 1]] - pr[order[k]] > 1e-9):
+            ref = np.zeros(V, bool)
+            ref[order[:k]] = True
+            assert np.array_equal(got, ref), trial
+            checked += 1
+    assert checked > 150
+
+
+def test_nucleus_extremes():
+    lp = np.array([0.5, 2.0, 2.0, -1.0, 1.9], np.float32)
+    assert np.array_equal(S.nucleus(lp, 1e-6), [False, True, True, False, False])  # ties at the top kept
+    assert S.nucleus(np.full(50, 3.0, np.float32), 0.3).all()                       # all tied: all kept
+    big = (np.random.default_rng(2).normal(size=4000) * 2).astype(np.float32)
+    tok = S.sample_position(big, 1.0, 5, 1, 3, 9)
+    assert S.sample_position(big, 1.0, 5, 1, 3, 9, top_p=1.0) == tok                 # p = 1: untruncated
+
+
+def test_nucleus_sampling_follows_the_truncated_softmax():
+    """Gumbel-max restricted to the nucleus draws from the renormalised truncation:
+    chi-square over 20000 step ids."""
+    lp = np.array([1.5, 1.0, 0.2, -0.5, 2.0, -2.0], np.float32)
+    p = 0.8
+    keep = S.nucleus(lp, p)
+    pr = np.where(keep, np.exp(lp.astype(np.float64) - lp.max()), 0.0)
+    pr /= pr.sum()
+    n = 20000
+    counts = np.zeros(6)
+    for k in range(n):
+        counts[S.sample_position(lp, 1.0, 3, 0, k, 41, top_p=p)[0]] += 1
+    assert (counts[~keep] == 0).all()
+    e = n * pr[keep]
+    chi2 = ((counts[keep] - e) ** 2 / e).sum()
+    assert chi2 < 25.0  # <= 5 dof, p ~ 1e-4
