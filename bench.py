@@ -448,15 +448,19 @@ def main():
             sweep[f"K={K}"] = {"tokens_per_s": tokens / (kms / 1e3), "ms_per_step": kms}
             print(f"[bench] K={K}: {kms:.3f} ms -> {tokens / (kms / 1e3):.1f} tokens/s", file=sys.stderr,
                   flush=True)
-    # the remasking posterior (capped sigma, eta = 0.04 as in the paper's ReMDM-Cap runs)
+    # the remasking posterior (capped sigma, eta = 0.04) without and with the nucleus p = 0.9
+    # of the paper's ReMDM-Cap runs
     remask = None
     if not args.no_sweep:
-        sampler[0] = tadm.remask_sampler(0.04)
-        rms, _, _ = timed(K0, max(2, args.steps // 2), 1)
+        remask = {}
+        for top_p in (0.0, 0.9):
+            sampler[0] = tadm.remask_sampler(0.04, top_p)
+            rms, _, _ = timed(K0, max(2, args.steps // 2), 1)
+            key = f"eta=0.04,top_p={top_p or 1.0}"
+            remask[key] = {"K": K0, "tokens_per_s": tokens / (rms / 1e3), "ms_per_step": rms}
+            print(f"[bench] remasking sampler {key}, K={K0}: {rms:.3f} ms -> {tokens / (rms / 1e3):.1f} tokens/s",
+                  file=sys.stderr, flush=True)
         sampler[0] = None
-        remask = {"eta": 0.04, "K": K0, "tokens_per_s": tokens / (rms / 1e3), "ms_per_step": rms}
-        print(f"[bench] remasking sampler eta=0.04, K={K0}: {rms:.3f} ms -> {tokens / (rms / 1e3):.1f} tokens/s",
-              file=sys.stderr, flush=True)
     roof = None
     if dom:
         live = kernel_table(cfg, B, K0, dom_stages)[0]

@@ -80,6 +80,8 @@ typedef struct {
                           TADM_STEP_REMASK: remasking posterior (p_unmask, sigma)    */
   float p_unmask;      /* REMASK: probability that a masked position takes its token  */
   float sigma;         /* REMASK: probability that a decoded position is remasked     */
+  float top_p;         /* in (0, 1): tokens come from the top-p nucleus (exact fixed-point
+                          weights, ties at the boundary kept); 0 or 1: the whole vocabulary */
 } tadm_step_args;
 
 /* Reverse-step kinds.  REMASK is the posterior of eq. inf-post-TADM (the ReMDM form,
@@ -191,6 +193,7 @@ int32_t tadm_unmask_count(int32_t M0, int32_t i, int32_t T);
 typedef struct {
   int32_t kind;
   float eta;
+  float top_p;  /* nucleus of the sampled tokens (0 or 1: off); the paper's runs use 0.9 */
 } tadm_sampler;
 
 /* Pure host helper: (sigma, p_unmask) of reverse step i under the capped schedule,

@@ -204,7 +204,7 @@ def rank_order(conf, candidates):
     return cand[order]
 
 
-def reverse_step(logits, canvas, mask_id, n_unmask, pos0, row, step_id, seed, inv_temp):
+def reverse_step(logits, canvas, mask_id, n_unmask, pos0, row, step_id, seed, inv_temp, top_p=1.0):
     """One reverse step for one row of the active canvas.
 
     logits [Lc, V] float32 (all canvas positions), canvas [Lc] ints, pos0 = absolute
@@ -217,7 +217,7 @@ def reverse_step(logits, canvas, mask_id, n_unmask, pos0, row, step_id, seed, in
     choice = np.full(Lc, -1, dtype=np.int64)
     conf = np.full(Lc, -np.inf, dtype=F32)
     for j in np.flatnonzero(masked):
-        choice[j], conf[j] = sample_position(logits[j], inv_temp, pos0 + j, row, step_id, seed)
+        choice[j], conf[j] = sample_position(logits[j], inv_temp, pos0 + j, row, step_id, seed, top_p)
     n = min(int(n_unmask), int(masked.sum()))
     sel = rank_order(conf, masked)[:n]
     nxt = canvas.copy()

@@ -41,11 +41,11 @@ class tadm_step_args(C.Structure):
     _fields_ = [("i", C.c_int32), ("T", C.c_int32), ("n_unmask", C.c_int32),
                 ("step_id", C.c_uint32), ("seed", C.c_uint64), ("inv_temp", C.c_float),
                 ("n_unmask_rows", C.c_void_p), ("mode", C.c_int32), ("p_unmask", C.c_float),
-                ("sigma", C.c_float)]
+                ("sigma", C.c_float), ("top_p", C.c_float)]
 
 
 class tadm_sampler(C.Structure):
-    _fields_ = [("kind", C.c_int32), ("eta", C.c_float)]
+    _fields_ = [("kind", C.c_int32), ("eta", C.c_float), ("top_p", C.c_float)]
 
 
 STEP_RANKED, STEP_REMASK = 0, 1
@@ -202,12 +202,12 @@ def tadm_anchor_forward(m, ctx, canvas, B, L, i, T, cache):
     check(lib.tadm_anchor_forward(m, ctx, ptr(canvas), B, L, i, T, cache))
 
 
-def step_args(i, T, n_unmask, step_id, seed, inv_temp, n_unmask_rows=None, remask=None):
+def step_args(i, T, n_unmask, step_id, seed, inv_temp, n_unmask_rows=None, remask=None, top_p=0.0):
     """n_unmask_rows: optional device int32 tensor [B] of per-row counts (kept alive by
     the caller until the step has run).  remask: optional (p_unmask, sigma) selecting the
     remasking posterior instead of confidence-ranked unmasking."""
     a = tadm_step_args(i=i, T=T, n_unmask=n_unmask, step_id=step_id, seed=seed,
-                       inv_temp=inv_temp, n_unmask_rows=ptr(n_unmask_rows))
+                       inv_temp=inv_temp, n_unmask_rows=ptr(n_unmask_rows), top_p=top_p)
     if remask is not None:
         a.mode, a.p_unmask, a.sigma = STEP_REMASK, remask[0], remask[1]
     return a
@@ -234,8 +234,8 @@ def tadm_generate_sampler(m, prompt, B, P, gen_len, T, K, block_len, seed, tempe
                                     C.byref(sampler) if sampler is not None else None, ptr(tokens)))
 
 
-def remask_sampler(eta):
-    return tadm_sampler(kind=STEP_REMASK, eta=eta)
+def remask_sampler(eta, top_p=0.0):
+    return tadm_sampler(kind=STEP_REMASK, eta=eta, top_p=top_p)
 
 
 def tadm_unmask_count(M0, i, T):

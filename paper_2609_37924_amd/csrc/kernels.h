@@ -177,8 +177,25 @@ hipError_t remask_update(const int32_t* canvas, const int32_t* choice, int B, in
 constexpr int SAMPLE_MAX_VOCAB = 4096 * 64;
 // For every masked canvas position: Gumbel-max token and fixed-point confidence.
 // Logits row of position (b, j) is row_map[b * Lc + j] if row_map is set, else b * Lc + j.
-hipError_t sample_tokens(const float* logits, const int32_t* row_map, const int32_t* canvas, int B,
-                         int L, int canvas_off, int V, int mask_id, int pos0, uint32_t step_id,
+// Nucleus threshold of one masked position: the global maximum m of the scaled logits
+// and the weight threshold tau of the top-p nucleus {v : rint(exp(l'_v - m) 2^40) >= tau}.
+// y_in / y_out screen membership without the exponential: y = l'_v - m >= y_in implies
+// v is in the nucleus, y < y_out that it is not (margins cover the error of the float32
+// exponential and the rounding to integer weights); only y in between is tested exactly.
+struct NucleusThr {
+  float m;
+  float y_in, y_out;
+  int pad;
+  long long tau;
+};
+// For every masked canvas position, its nucleus threshold at top_p (0 < top_p < 1);
+// thr is indexed like choice / conf (b * Lc + j).
+hipError_t nucleus_thresholds(const float* logits, const int32_t* row_map, const int32_t* canvas, int B, int L,
+                              int canvas_off, int V, int mask_id, float inv_temp, float top_p, NucleusThr* thr,
+                              hipStream_t s);
+// thr (nullable): draw each token from its position's nucleus.
+hipError_t sample_tokens(const float* logits, const int32_t* row_map, const NucleusThr* thr, const int32_t* canvas,
+                         int B, int L, int canvas_off, int V, int mask_id, int pos0, uint32_t step_id,
                          uint64_t seed, float inv_temp, int32_t* choice, float* conf, hipStream_t s);
 // Per row: reveal the n most confident masked positions (n = n_rows[b] if n_rows is
 // set, else n_unmask; clamped to the row's masked count); copy the rest.

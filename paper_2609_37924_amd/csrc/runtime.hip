@@ -233,6 +233,7 @@ struct Workspace {
   int32_t* choice = nullptr;
   int32_t *cidx = nullptr, *row_map = nullptr;  // masked-position list and its inverse
   int* count = nullptr;                         // number of masked positions (device)
+  NucleusThr* nthr = nullptr;                   // per-position nucleus thresholds
   float* logits = nullptr;
   size_t logits_cap = 0;
   int kv_cap = 0;
@@ -390,6 +391,7 @@ static tadm_status ensure_workspace(tadm_model* m) {
   TRY(ws_alloc(m, (void**)&w.row_map, N * 4));
   TRY(ws_alloc(m, (void**)&w.count, 256));
   TRY(ws_alloc(m, (void**)&w.conf, N * 4));
+  TRY(ws_alloc(m, (void**)&w.nthr, N * sizeof(NucleusThr)));
   w.n_tok = (int)N;
   w.n_canvas = (int)N;
   return TADM_OK;
@@ -720,6 +722,7 @@ static tadm_status check_args(const tadm_step_args* a, int Lc) {
   if (a->mode != TADM_STEP_RANKED && a->mode != TADM_STEP_REMASK) return fail(TADM_ERR_INVALID, "step mode %d", a->mode);
   if (a->mode == TADM_STEP_REMASK && !(a->p_unmask >= 0.f && a->p_unmask <= 1.f && a->sigma >= 0.f && a->sigma <= 1.f))
     return fail(TADM_ERR_INVALID, "remasking probabilities must lie in [0, 1]");
+  if (!(a->top_p >= 0.f && a->top_p <= 1.f)) return fail(TADM_ERR_INVALID, "top_p outside [0, 1]");
   (void)Lc;
   return TADM_OK;
 }
@@ -1053,8 +1056,12 @@ static tadm_status sample_impl(tadm_model* m, const float* logits, const int32_t
                                const tadm_step_args* a, int32_t* next, int32_t* choice, float* conf) {
   const int mask = m->cfg.vocab;
   TRY(prof_begin(m, TADM_STAGE_SAMPLE));
-  HIPCHK(sample_tokens(logits, row_map, canvas, B, L, off, m->cfg.vocab, mask, pos0, a->step_id, a->seed,
-                       a->inv_temp, choice, conf, m->stream));
+  const bool nucleus = a->top_p > 0.f && a->top_p < 1.f;
+  if (nucleus)
+    HIPCHK(nucleus_thresholds(logits, row_map, canvas, B, L, off, m->cfg.vocab, mask, a->inv_temp, a->top_p,
+                              m->ws.nthr, m->stream));
+  HIPCHK(sample_tokens(logits, row_map, nucleus ? m->ws.nthr : nullptr, canvas, B, L, off, m->cfg.vocab, mask, pos0,
+                       a->step_id, a->seed, a->inv_temp, choice, conf, m->stream));
   TRY(prof_end(m, TADM_STAGE_SAMPLE));
   return canvas_update(m, canvas, choice, conf, B, L, off, pos0, a, next);
 }
@@ -1093,7 +1100,7 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
   m->tap_final = full;
   // bf16 masked-only head: the sampler runs in the projection's epilogue and only
   // per-(row, 64-entry group) partials reach memory
-  const bool fused = !full && m->dt == BF16;
+  const bool fused = !full && m->dt == BF16 && !(a->top_p > 0.f && a->top_p < 1.f);  // nucleus needs whole rows
   const int ng = (cf.vocab + 63) / 64;
   if (!full) {
     TRY(ensure_logits(m, fused ? (size_t)B * Lc * ng * (sizeof(SamplePart) / 4) : (size_t)B * Lc * cf.vocab));
@@ -1188,6 +1195,7 @@ tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int3
   if (sampler && sampler->kind != TADM_STEP_RANKED && !remask)
     return fail(TADM_ERR_INVALID, "sampler kind %d", sampler->kind);
   if (remask && !(sampler->eta >= 0.f && sampler->eta <= 1.f)) return fail(TADM_ERR_INVALID, "eta outside [0, 1]");
+  if (sampler && !(sampler->top_p >= 0.f && sampler->top_p <= 1.f)) return fail(TADM_ERR_INVALID, "top_p outside [0, 1]");
   if (!tokens_dev || (P > 0 && !prompt_dev)) return fail(TADM_ERR_INVALID, "null argument");
   if (B < 1 || B > m->cfg.max_batch) return fail(TADM_ERR_INVALID, "B=%d outside [1, %d]", B, m->cfg.max_batch);
   if (P < 0 || gen_len < 1 || block_len < 1 || gen_len % block_len)
@@ -1206,6 +1214,7 @@ tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int3
   a.seed = seed;
   a.inv_temp = (float)(1.0 / (double)temperature);
   a.mode = remask ? TADM_STEP_REMASK : TADM_STEP_RANKED;
+  a.top_p = sampler ? sampler->top_p : 0.f;
   // masked positions entering step i: exactly B floor(M0 i / T) for the ranked sampler;
   // any number up to B M0 under remasking
   auto masked_bound = [&](int M0, int i) { return remask ? B * M0 : (int)(B * (((int64_t)M0 * i) / T)); };

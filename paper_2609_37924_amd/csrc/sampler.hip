@@ -46,8 +46,8 @@ constexpr int UNROLL = 4;       // chunks whose loads are in flight together
 // are scored exactly, otherwise every entry is scored exactly in a second pass.
 // Dynamic LDS: ceil(V / 64) x (float + int64).
 __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const int32_t* row_map,
-                                                     const int32_t* canvas, int L, int off, int Lc, int V,
-                                                     int mask_id, int pos0, uint32_t step_id, uint32_t k0,
+                                                     const NucleusThr* thr, const int32_t* canvas, int L, int off,
+                                                     int Lc, int V, int mask_id, int pos0, uint32_t step_id, uint32_t k0,
                                                      uint32_t k1, float inv_temp, int32_t* choice,
                                                      float* conf) {
   extern __shared__ long long s_dyn[];
@@ -73,6 +73,17 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const bool vec = (V & 3) == 0;
   const int nchunk = (V + CHUNK - 1) / CHUNK;
+  // nucleus: entry v takes part iff rint(exp(l'_v - nm) 2^40) >= ntau
+  const bool nuc = thr != nullptr;
+  const float nm = nuc ? thr[row].m : 0.f;
+  const float y_in = nuc ? thr[row].y_in : -INFINITY, y_out = nuc ? thr[row].y_out : -INFINITY;
+  const long long ntau = nuc ? thr[row].tau : 0;
+  auto in_nucleus = [&](float lp) {
+    const float y = lp - nm;
+    if (y >= y_in) return true;
+    if (y < y_out) return false;
+    return (long long)rintf(own_exp(y) * 1099511627776.0f) >= ntau;
+  };
 
   Top2 top;
   for (int c0 = 0; c0 < nchunk; c0 += UNROLL) {
@@ -118,7 +129,7 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
       philox4x32_10(ctr, k0, k1);
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (4 * q + e < V) top.add(screen_score(lp[e], uniform01(ctr[e])), 4 * q + e);
+        if (4 * q + e < V && in_nucleus(lp[e])) top.add(screen_score(lp[e], uniform01(ctr[e])), 4 * q + e);
     }
   }
   __syncthreads();
@@ -165,7 +176,9 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
       for (int e = 0; e < 4; ++e) {
         const int v = 4 * q + e;
         if (v >= V) break;
-        const float sc = exact_score_of(lg[v] * inv_temp, uniform01(ctr[e]));
+        const float lpv = lg[v] * inv_temp;
+        if (!in_nucleus(lpv)) continue;
+        const float sc = exact_score_of(lpv, uniform01(ctr[e]));
         if (sc > best.score) best = Best{sc, v};
       }
     }
@@ -190,6 +203,185 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
     const float norm = (float)S * 9.094947017729282379150390625e-13f;  // * 2^-40, exact
     choice[row] = best.v;
     conf[row] = (lpx - mx) - own_log(norm);
+  }
+}
+
+// grid (Lc, B), NUC_THREADS threads: the nucleus threshold of each masked position.
+// Weights q_v = rint(exp(l'_v - m) 2^40) (int64), Q = sum q_v, target = ceil(top_p Q) (exact,
+// in 128-bit integers); tau is found by four radix passes over the 41-bit weights (digits of
+// 11, 11, 11 and 8 bits, high to low): each pass sums, per digit, the weights of the entries
+// that share the digits chosen so far, and keeps the highest digit at which the weights
+// above plus that digit's reach the target.  All sums are integers: any order, same tau.
+// The first pass also accumulates Q.  Digit 0 collects every small weight of a pass (most
+// of the vocabulary), so it is not accumulated by atomics: its sum is the pass's total (Q,
+// then the previous pass's chosen digit's sum) minus the other digits'.
+// A weight is held as the float w = rint(exp(l'_v - m) 2^40), an integer below 2^41 with
+// 24 significant bits, so its digits and prefixes are exact float operations:
+// floor(w 2^-s) is q >> s, and floor(w 2^-s) - floor(w 2^-(s+b)) 2^b is its b-bit digit.
+// PER > 0: V <= NUC_THREADS * PER and V % 4 == 0; each thread keeps the weights of its PER
+// entries in registers, read once as float4.  PER = 0: every pass recomputes them.
+constexpr int NUC_THREADS = 1024;
+template <int PER>
+__global__ __launch_bounds__(NUC_THREADS) void nucleus_kernel(const float* logits, const int32_t* row_map,
+                                                              const int32_t* canvas, int L, int off, int Lc, int V,
+                                                              int mask_id, float inv_temp, float top_p,
+                                                              NucleusThr* thr) {
+  constexpr int NW = NUC_THREADS / 64;
+  constexpr bool CACHED = PER > 0;
+  constexpr int NE = CACHED ? PER : 1;
+  constexpr float TWO40 = 1099511627776.0f;
+  __shared__ unsigned long long hist[2048];
+  __shared__ float s_f[NW];
+  __shared__ unsigned long long s_u[NW];
+  __shared__ unsigned long long s_sel[3];
+  const int j = blockIdx.x, b = blockIdx.y, row = b * Lc + j;
+  if (canvas[(size_t)b * L + off + j] != mask_id) return;
+  const float* lg = logits + (size_t)(row_map ? row_map[row] : row) * V;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // cached entry i of this thread: v = 4 (tid + NUC_THREADS (i / 4)) + i % 4
+  auto vof = [&](int i) { return 4 * (tid + NUC_THREADS * (i >> 2)) + (i & 3); };
+
+  float ev[NE];  // l'_v, then the weight w_v
+  float mx = -INFINITY;
+  if constexpr (CACHED) {
+#pragma unroll
+    for (int i = 0; i < NE; i += 4) {
+      const float4 x = vof(i) < V ? *reinterpret_cast<const float4*>(lg + vof(i))
+                                  : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+      ev[i] = x.x * inv_temp;
+      ev[i + 1] = x.y * inv_temp;
+      ev[i + 2] = x.z * inv_temp;
+      ev[i + 3] = x.w * inv_temp;
+      mx = fmaxf(mx, fmaxf(fmaxf(ev[i], ev[i + 1]), fmaxf(ev[i + 2], ev[i + 3])));
+    }
+  } else {
+    for (int v = tid; v < V; v += NUC_THREADS) mx = fmaxf(mx, lg[v] * inv_temp);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  if (lane == 0) s_f[wave] = mx;
+  __syncthreads();
+  mx = s_f[0];
+  for (int w = 1; w < NW; ++w) mx = fmaxf(mx, s_f[w]);
+  if constexpr (CACHED) {
+#pragma unroll
+    for (int i = 0; i < NE; i += 4) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ev[i + e] = rintf(own_exp_sel(ev[i + e] - mx) * TWO40);  // padding: 0
+      asm volatile("" : "+v"(ev[i]), "+v"(ev[i + 1]), "+v"(ev[i + 2]), "+v"(ev[i + 3])::"memory");
+    }
+  }
+  // calls f(w) for every entry of the row (the cached padding entries have w = 0)
+  auto for_each_weight = [&](auto f) {
+    if constexpr (CACHED) {
+#pragma unroll
+      for (int i = 0; i < NE; i += 4) {
+        // four entries at a time, in order: fresh copies per pass (the int64 conversions are
+        // not kept live across passes) and a barrier per group (bounded temporaries)
+        float w0 = ev[i], w1 = ev[i + 1], w2 = ev[i + 2], w3 = ev[i + 3];
+        asm volatile("" : "+v"(w0), "+v"(w1), "+v"(w2), "+v"(w3)::"memory");
+        f(w0);
+        f(w1);
+        f(w2);
+        f(w3);
+      }
+    } else {
+      for (int v = tid; v < V; v += NUC_THREADS) f(rintf(own_exp(lg[v] * inv_temp - mx) * TWO40));
+    }
+  };
+
+  // first pass: Q and the top 11-bit digit (q >> 30) of every weight
+  for (int i = tid; i < 2048; i += NUC_THREADS) hist[i] = 0;
+  __syncthreads();
+  unsigned long long Q = 0;
+  for_each_weight([&](float w) {
+    const unsigned long long q = (unsigned long long)w;
+    Q += q;
+    const int d = (int)(w * 0x1p-30f);  // truncation = floor (w >= 0)
+    if (d != 0) atomicAdd(&hist[d], q);
+  });
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) Q += __shfl_xor(Q, o, 64);
+  if (lane == 0) s_u[wave] = Q;
+  __syncthreads();
+  Q = 0;
+  for (int w = 0; w < NW; ++w) Q += s_u[w];
+  // target = ceil(top_p Q): top_p = mant 2^-sh with a 24-bit integer mant (normal, < 1)
+  const uint32_t pb = __float_as_uint(top_p);
+  const unsigned long long mant = (pb & 0x7FFFFFu) | 0x800000u;
+  const int sh = 150 - (int)((pb >> 23) & 0xFF);
+  const unsigned __int128 prod = (unsigned __int128)mant * Q;  // < 2^82
+  const unsigned long long target =
+      sh >= 100 ? 1ull : (unsigned long long)((prod + (((unsigned __int128)1 << sh) - 1)) >> sh);
+
+  unsigned long long prefix = 0, above = 0, total = Q;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int shk = k == 0 ? 30 : k == 1 ? 19 : k == 2 ? 8 : 0, bk = k == 3 ? 8 : 11;
+    const int nb = 1 << bk;
+    if (k > 0) {  // histogram of digit k over the weights whose higher digits equal prefix
+      const float top_scale = __uint_as_float((uint32_t)(127 - shk - bk) << 23);  // 2^-(shk + bk)
+      const float dig_scale = __uint_as_float((uint32_t)(127 - shk) << 23);       // 2^-shk
+      const float pre_f = (float)prefix;  // exact: the prefix of an existing weight
+      const float base = (float)(1 << bk);
+      for_each_weight([&](float w) {
+        const float hi = floorf(w * top_scale);
+        if (hi == pre_f) {
+          const int d = (int)(floorf(w * dig_scale) - hi * base);
+          if (d != 0) atomicAdd(&hist[d], (unsigned long long)w);
+        }
+      });
+      __syncthreads();
+    }
+    if (wave == 0) {  // lane l owns digits [l c, (l + 1) c); suffix sums over lanes, high to low
+      const int c = nb / 64;
+      unsigned long long own = 0;
+      for (int i = 0; i < c; ++i) own += hist[lane * c + i];
+      unsigned long long rest = own;  // digits 1.. of the pass
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) rest += __shfl_xor(rest, o, 64);
+      if (lane == 0) {  // digit 0 is the remainder of the pass's total
+        hist[0] = total - rest;
+        own += total - rest;
+      }
+      unsigned long long suf = own;  // sum over this lane's digits and every higher lane's
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const unsigned long long t = __shfl_down(suf, o, 64);
+        if (lane + o < 64) suf += t;
+      }
+      const unsigned long long higher = above + (suf - own);  // weight in digits above this lane's
+      if (higher < target && higher + own >= target) {
+        unsigned long long acc = higher;
+        for (int d = lane * c + c - 1; d >= lane * c; --d) {
+          if (acc + hist[d] >= target) {
+            s_sel[0] = (unsigned long long)d;
+            s_sel[1] = acc;
+            s_sel[2] = hist[d];
+            break;
+          }
+          acc += hist[d];
+        }
+      }
+    }
+    __syncthreads();
+    prefix = (prefix << bk) | s_sel[0];
+    above = s_sel[1];
+    total = s_sel[2];
+    if (k < 3) {
+      const int nb_next = k == 2 ? 256 : 2048;
+      for (int i = tid; i < nb_next; i += NUC_THREADS) hist[i] = 0;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    // exp(y) >= (tau + 1/2) 2^-40 e^(1e-4) makes the float32 weight round to >= tau; below
+    // (tau - 1/2) 2^-40 e^(-1e-4) it rounds below tau (the float32 exponential and the
+    // rounding of y = l' - m are within 1e-5 relative of exp(y))
+    const double t = (double)prefix;
+    const float y_in = (float)(log((t + 0.5) * 0x1p-40) + 1e-4);
+    const float y_out = t > 0.5 ? (float)(log((t - 0.5) * 0x1p-40) - 1e-4) : -INFINITY;
+    thr[row] = NucleusThr{mx, y_in, y_out, 0, (long long)prefix};
   }
 }
 
@@ -315,16 +507,28 @@ hipError_t compact_masked(const int32_t* canvas, int B, int L, int canvas_off, i
   return hipGetLastError();
 }
 
-hipError_t sample_tokens(const float* logits, const int32_t* row_map, const int32_t* canvas, int B,
-                         int L, int canvas_off, int V, int mask_id, int pos0, uint32_t step_id,
+hipError_t nucleus_thresholds(const float* logits, const int32_t* row_map, const int32_t* canvas, int B, int L,
+                              int canvas_off, int V, int mask_id, float inv_temp, float top_p, NucleusThr* thr,
+                              hipStream_t s) {
+  const int Lc = L - canvas_off;
+  if (B * Lc == 0) return hipSuccess;
+  auto kernel = nucleus_kernel<0>;
+  if (V % 4 == 0 && V <= NUC_THREADS * 32) kernel = V <= NUC_THREADS * 16 ? nucleus_kernel<16> : nucleus_kernel<32>;
+  hipLaunchKernelGGL(kernel, dim3(Lc, B), dim3(NUC_THREADS), 0, s, logits, row_map, canvas, L, canvas_off, Lc, V,
+                     mask_id, inv_temp, top_p, thr);
+  return hipGetLastError();
+}
+
+hipError_t sample_tokens(const float* logits, const int32_t* row_map, const NucleusThr* thr, const int32_t* canvas,
+                         int B, int L, int canvas_off, int V, int mask_id, int pos0, uint32_t step_id,
                          uint64_t seed, float inv_temp, int32_t* choice, float* conf, hipStream_t s) {
   const int Lc = L - canvas_off;
   if (B * Lc == 0) return hipSuccess;
   if (V > SAMPLE_MAX_VOCAB) return hipErrorInvalidValue;
   const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
   const uint32_t lds = (uint32_t)(((V + GROUP - 1) / GROUP) * (sizeof(long long) + sizeof(float)));
-  launch_timed(sample_kernel, dim3(Lc, B), dim3(256), lds, s, logits, row_map, canvas, L, canvas_off, Lc, V, mask_id,
-               pos0, step_id, k0, k1, inv_temp, choice, conf);
+  launch_timed(sample_kernel, dim3(Lc, B), dim3(256), lds, s, logits, row_map, thr, canvas, L, canvas_off, Lc, V,
+               mask_id, pos0, step_id, k0, k1, inv_temp, choice, conf);
   return hipGetLastError();
 }
 

@@ -79,6 +79,14 @@ __device__ __forceinline__ float own_exp(float y) {
   return p * scale;
 }
 
+// own_exp without a branch: the same rounded operations for y >= -30 (and NaN), and 0 below,
+// selected rather than branched on, for loops that unroll many exponentials.
+__device__ __forceinline__ float own_exp_sel(float y) {
+  const bool under = y < -30.0f;
+  const float e = own_exp(under ? -30.0f : y);
+  return under ? 0.0f : e;
+}
+
 struct Best {
   float score;
   int v;

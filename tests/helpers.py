@@ -54,7 +54,7 @@ def oracle_step(net, canvas_row, pos, cache, off):
     return c, ht, xf[off:], net.head(xf[off:]).astype(np.float32)
 
 
-def oracle_sample_rows(logits, canvas, mask_id, n, pos0, off, step_id, seed, inv_temp):
+def oracle_sample_rows(logits, canvas, mask_id, n, pos0, off, step_id, seed, inv_temp, top_p=1.0):
     """Oracle reverse step for every row: (next canvas, choice, conf) as arrays."""
     B = canvas.shape[0]
     nxt = canvas.copy()
@@ -62,7 +62,7 @@ def oracle_sample_rows(logits, canvas, mask_id, n, pos0, off, step_id, seed, inv
     conf = np.full((B, canvas.shape[1] - off), -np.inf, dtype=np.float32)
     for b in range(B):
         nx, ch, cf = S.reverse_step(logits[b], canvas[b, off:], mask_id, n, pos0 + off, b, step_id,
-                                    seed, np.float32(inv_temp))
+                                    seed, np.float32(inv_temp), top_p)
         nxt[b, off:] = nx
         choice[b] = ch
         conf[b] = cf

@@ -133,6 +133,47 @@ def _teacher_step_parity(cfg, B, tol, rows=None, seed=0, n_masked=(None, None), 
         tadm.tadm_model_destroy(m)
 
 
+@pytest.mark.parametrize("V,B,L,off,top_p,std,ties", [
+    (256, 2, 40, 8, 0.9, 2.0, False),
+    (1001, 2, 24, 0, 0.5, 1.0, False),      # vocabulary not a multiple of 4
+    (64, 2, 32, 0, 0.3, 2.0, True),         # planted ties, duplicated rows
+    (4, 4, 64, 0, 0.5, 0.0, False),         # all logits equal: the whole vocabulary is the nucleus
+    (32768, 1, 12, 2, 0.95, 0.5, False),    # largest row kept in registers
+    (50304, 1, 6, 0, 0.9, 30.0, False),     # peaked: a nucleus of a few entries
+    (128, 2, 16, 0, 1e-7, 1.0, False),      # tiny p: the top entries only
+    (4096, 2, 8, 0, 0.9999, 3.0, False),    # threshold deep in the small weights (digit 0 of each pass)
+    (65536, 1, 4, 0, 0.8, 3.0, False),      # weights recomputed per pass
+    (131072, 1, 4, 0, 0.9, 1.0, False),
+])
+def test_nucleus_sampler_bit_exact(V, B, L, off, top_p, std, ties):
+    """Confidence-ranked step with top-p tokens: choice, confidence and next canvas equal
+    the oracle's bit for bit (threshold by four radix passes over exact int64 weights)."""
+    cfg = synth.get_config("tiny", vocab=V)
+    m = tadm.tadm_model_create(tadm.make_config(cfg, max_batch=B, max_seq=L))
+    tadm.tadm_set_stream(m, torch.cuda.current_stream().cuda_stream)
+    try:
+        g = torch.Generator().manual_seed(V + 1)
+        canvas = torch.randint(0, V, (B, L), generator=g, dtype=torch.int32)
+        canvas[:, off:][torch.rand(B, L - off, generator=g) < 0.7] = V
+        logits = synth.make_logits(B * (L - off), V, seed=V + 1, std=std, ties=ties).view(B, L - off, V)
+        tp = float(np.float32(top_p))
+        args = tadm.step_args(3, 8, 5, 6, 0x5EED, 1.0, top_p=tp)
+        d_can = canvas.to(dev())
+        nxt = torch.empty_like(d_can)
+        choice = torch.empty(B, L - off, dtype=torch.int32, device=dev())
+        conf = torch.empty(B, L - off, dtype=torch.float32, device=dev())
+        tadm.tadm_sample(m, logits.to(dev()), d_can, B, L, off, 9, args, nxt, choice, conf)
+        sync()
+        r_next, r_choice, r_conf = oracle_sample_rows(logits.numpy(), canvas.numpy().astype(np.int64), V, 5, 9, off,
+                                                      6, 0x5EED, 1.0, top_p=tp)
+        masked = canvas[:, off:].numpy() == V
+        np.testing.assert_array_equal(choice.cpu().numpy()[masked], r_choice[masked])
+        np.testing.assert_array_equal(conf.cpu().numpy().view(np.int32)[masked], r_conf.view(np.int32)[masked])
+        np.testing.assert_array_equal(nxt.cpu().numpy(), r_next)
+    finally:
+        tadm.tadm_model_destroy(m)
+
+
 def test_sampler_per_row_counts():
     """Per-row unmask counts from a device array (clamped to each row's masked count,
     negative counts reveal nothing) against the oracle step with each row's own n."""
@@ -358,8 +399,9 @@ def test_tiny_generation_matches_oracle(K):
     np.testing.assert_array_equal(got, ref)
 
 
-@pytest.mark.parametrize("eta,block", [(0.04, False), (0.5, False), (0.3, True)])
-def test_tiny_remask_generation_matches_oracle(eta, block):
+@pytest.mark.parametrize("eta,block,top_p", [(0.04, False, 0.0), (0.5, False, 0.0), (0.3, True, 0.0),
+                                             (0.04, False, 0.9), (0.3, True, 0.6)])
+def test_tiny_remask_generation_matches_oracle(eta, block, top_p):
     """Whole generations with the remasking sampler (capped sigma) are token-identical
     to the oracle's Algorithm 1 with the same posterior, and end fully unmasked."""
     cfg = synth.get_config("tiny", batch=2, n_kv_heads=2 if block else 4)
@@ -371,13 +413,15 @@ def test_tiny_remask_generation_matches_oracle(eta, block):
     m = gpu_model(cfg, tensors, B, P + G)
     try:
         out = torch.empty(B, P + G, dtype=torch.int32, device=dev())
-        tadm.tadm_generate_sampler(m, prompt.to(dev()), B, P, G, T, K, bl, 2, 1.0, tadm.remask_sampler(eta), out)
+        tadm.tadm_generate_sampler(m, prompt.to(dev()), B, P, G, T, K, bl, 2, 1.0, tadm.remask_sampler(eta, top_p),
+                                   out)
         sync()
         got = out.cpu().numpy()
     finally:
         tadm.tadm_model_destroy(m)
     net = oracle_net(cfg, tensors)
-    ref = loop.generate(net, prompt.numpy(), G, T, K, bl, 2, 1.0, synth.mask_id(cfg), remask_eta=eta)
+    ref = loop.generate(net, prompt.numpy(), G, T, K, bl, 2, 1.0, synth.mask_id(cfg), remask_eta=eta,
+                        top_p=float(np.float32(top_p)) if top_p else 1.0)
     np.testing.assert_array_equal(got, ref)
     assert (got != synth.mask_id(cfg)).all()
 
