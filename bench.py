@@ -390,8 +390,10 @@ def main():
 
     sampler = [None]  # None: confidence-ranked (the headline); else a tadm_sampler
 
+    T_run = [T]
+
     def gen(K):
-        tadm.tadm_generate_sampler(m, prompt, B, P, G, T, K, bl, cfg["sampler_seed"], cfg["temperature"],
+        tadm.tadm_generate_sampler(m, prompt, B, P, G, T_run[0], K, bl, cfg["sampler_seed"], cfg["temperature"],
                                    sampler[0], out)
 
     def timed(K, steps, warmup, profile=0, profiled_steps=None):
@@ -460,6 +462,16 @@ def main():
             remask[key] = {"K": K0, "tokens_per_s": tokens / (rms / 1e3), "ms_per_step": rms}
             print(f"[bench] remasking sampler {key}, K={K0}: {rms:.3f} ms -> {tokens / (rms / 1e3):.1f} tokens/s",
                   file=sys.stderr, flush=True)
+        # ReMDM-Loop, the paper's sampler when the step budget reaches the generation
+        # length: T = block length, eta = 0.02, t_on = 0.55, t_off = 0.05, alpha_on = 0.9
+        sampler[0] = tadm.loop_sampler(0.02, 0.55, 0.05, 0.9, 0.9)
+        T_run[0] = max(T, bl)
+        rms, _, _ = timed(K0, 2, 1)
+        key = f"loop,T={T_run[0]},eta=0.02,top_p=0.9"
+        remask[key] = {"K": K0, "T": T_run[0], "tokens_per_s": tokens / (rms / 1e3), "ms_per_step": rms}
+        print(f"[bench] remasking sampler {key}, K={K0}: {rms:.3f} ms -> {tokens / (rms / 1e3):.1f} tokens/s",
+              file=sys.stderr, flush=True)
+        T_run[0] = T
         sampler[0] = None
     roof = None
     if dom:

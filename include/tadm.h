@@ -189,16 +189,28 @@ int32_t tadm_unmask_count(int32_t M0, int32_t i, int32_t T);
  * the remasking posterior with sigma_i = min(eta, (1 - alpha_s) / alpha_t), the
  * largest remasking probability that keeps the posterior's mask probability
  * 1 - alpha_s - sigma alpha_t non-negative (ReMDM-Cap's form; eta = 0 is the plain
- * absorbing posterior), on the linear schedule alpha_t = 1 - t. */
+ * absorbing posterior), on the linear schedule alpha_t = 1 - t.
+ * kind TADM_SAMPLER_LOOP: the ReMDM-Loop schedule (the paper's sampler for T >= L,
+ * App. D sampler details, with eta = 0.02, t_on = 0.55, t_off = 0.05, alpha_on = 0.9):
+ * alpha rises linearly from 0 at t = 1 to alpha_on at t_on, stays at alpha_on down to
+ * t_off and rises linearly to 1 at t = 0; steps wholly inside [t_off, t_on] remask with
+ * sigma = min(eta, (1 - alpha_s) / alpha_t), the others have sigma = 0.  Its steps run
+ * in TADM_STEP_REMASK mode.  Needs 0 < t_off < t_on < 1 and 0 < alpha_on < 1. */
+enum { TADM_SAMPLER_LOOP = 2 };
 typedef struct {
   int32_t kind;
   float eta;
   float top_p;  /* nucleus of the sampled tokens (0 or 1: off); the paper's runs use 0.9 */
+  double t_on, t_off, alpha_on;  /* TADM_SAMPLER_LOOP only */
 } tadm_sampler;
 
 /* Pure host helper: (sigma, p_unmask) of reverse step i under the capped schedule,
  * computed in double and rounded to float. */
 void tadm_remask_probs(int32_t i, int32_t T, float eta, float* sigma, float* p_unmask);
+/* Pure host helper: (sigma, p_unmask) of reverse step i (t = i/T, s = (i-1)/T) under the
+ * ReMDM-Loop schedule described above, computed in double and rounded to float. */
+void tadm_loop_probs(int32_t i, int32_t T, float eta, double t_on, double t_off, double alpha_on, float* sigma,
+                     float* p_unmask);
 
 /* tadm_generate with a sampler (NULL: confidence-ranked). */
 tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int32_t B, int32_t P,

@@ -44,6 +44,37 @@ def remask_probs(i, T, eta):
     return np.float32(sigma), np.float32(p)
 
 
+def loop_alpha(t, t_on, t_off, alpha_on):
+    """alpha(t) of the ReMDM-Loop schedule (reading of the sampler details, App. D, after
+    the ReMDM paper): rises linearly from 0 at t = 1 to alpha_on at t_on, stays at
+    alpha_on down to t_off, rises linearly to 1 at t = 0."""
+    if t >= t_on:
+        return alpha_on * (1.0 - t) / (1.0 - t_on)
+    if t >= t_off:
+        return alpha_on
+    return alpha_on + (1.0 - alpha_on) * (t_off - t) / t_off
+
+
+def loop_probs(i, T, eta, t_on, t_off, alpha_on):
+    """(sigma, p_unmask) of reverse step i (t = i/T -> s = (i-1)/T) under ReMDM-Loop.
+
+    Steps wholly inside the plateau [t_off, t_on] (alpha_s = alpha_t = alpha_on) remask
+    with sigma = min(eta, (1 - alpha_s) / alpha_t); the other steps are plain absorbing
+    steps (sigma = 0).  p_unmask = (alpha_s - (1 - sigma) alpha_t) / (1 - alpha_t) as in
+    eq. inf-post-TADM.  eta is a float32 parameter (as for ReMDM-Cap), the schedule's
+    times and alpha_on are float64; the arithmetic is float64 and the two results are
+    rounded to float32."""
+    eta = float(np.float32(eta))
+    t, s = i / T, (i - 1) / T
+    a_t = loop_alpha(t, t_on, t_off, alpha_on)
+    a_s = loop_alpha(s, t_on, t_off, alpha_on)
+    sigma = 0.0
+    if t <= t_on and s >= t_off:
+        sigma = min(eta, (1.0 - a_s) / a_t)
+    p = (a_s - (1.0 - sigma) * a_t) / (1.0 - a_t)
+    return np.float32(sigma), np.float32(p)
+
+
 def is_refresh(i, T, K):
     return (T - i) % K == 0
 
@@ -56,11 +87,13 @@ class Counts:
 
 
 def generate(net, prompt, gen_len, T, K, block_len, seed, temperature, mask_id,
-             counts=None, trace=None, sample_fn=None, remask_eta=None, top_p=1.0):
+             counts=None, trace=None, sample_fn=None, remask_eta=None, top_p=1.0, loop=None):
     """Run Algorithm 1 on every row of ``prompt`` [B, P]; returns tokens [B, P+gen_len].
 
     ``remask_eta`` selects the remasking posterior with sigma = min(eta, cap) instead of
-    confidence-ranked unmasking; ``top_p`` < 1 samples its tokens from the nucleus.  ``trace`` (list) receives per-step dicts (i, step_id,
+    confidence-ranked unmasking; ``loop`` = (eta, t_on, t_off, alpha_on) selects it on
+    the ReMDM-Loop schedule; ``top_p`` < 1 samples tokens from the nucleus.
+    ``trace`` (list) receives per-step dicts (i, step_id,
     refresh, canvas before the step) for tests; ``sample_fn`` replaces the reverse step
     (used by counting tests).
     """
@@ -105,11 +138,15 @@ def generate(net, prompt, gen_len, T, K, block_len, seed, temperature, mask_id,
                 ht = net.fuse(c, caches[b])
                 xf = net.denoise(ht, pos, ctx[b])
                 logits = net.head(xf[c0 - w0:]).astype(np.float32)
-                if remask_eta is None:
+                if remask_eta is None and loop is None:
+                    extra = {} if sample_fn else {"top_p": top_p}
                     nxt, _, _ = sample(logits, seq[b, c0:w1], mask_id, n, c0, b, step_id,
-                                       seed, inv_temp)
+                                       seed, inv_temp, **extra)
                 else:
-                    sigma, p_unmask = remask_probs(i, T, remask_eta)
+                    if loop is not None:
+                        sigma, p_unmask = loop_probs(i, T, *loop)
+                    else:
+                        sigma, p_unmask = remask_probs(i, T, remask_eta)
                     nxt, _ = smp.remask_step(logits, seq[b, c0:w1], mask_id, p_unmask, sigma, c0, b,
                                              step_id, seed, inv_temp, top_p)
                 seq[b, c0:w1] = nxt

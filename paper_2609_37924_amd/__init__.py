@@ -45,10 +45,12 @@ class tadm_step_args(C.Structure):
 
 
 class tadm_sampler(C.Structure):
-    _fields_ = [("kind", C.c_int32), ("eta", C.c_float), ("top_p", C.c_float)]
+    _fields_ = [("kind", C.c_int32), ("eta", C.c_float), ("top_p", C.c_float),
+                ("t_on", C.c_double), ("t_off", C.c_double), ("alpha_on", C.c_double)]
 
 
 STEP_RANKED, STEP_REMASK = 0, 1
+SAMPLER_LOOP = 2
 
 
 class TadmError(RuntimeError):
@@ -83,6 +85,8 @@ _SIGS = {
                                    C.POINTER(tadm_sampler), _P]),
     "tadm_unmask_count": (_I, [_I, _I, _I]),
     "tadm_remask_probs": (None, [_I, _I, C.c_float, C.POINTER(C.c_float), C.POINTER(C.c_float)]),
+    "tadm_loop_probs": (None, [_I, _I, C.c_float, C.c_double, C.c_double, C.c_double, C.POINTER(C.c_float),
+                               C.POINTER(C.c_float)]),
     "tadm_debug_read": (_I, [_P, _I, _P, C.c_size_t]),
     "tadm_debug_taps": (_I, [_P, _I]),
     "tadm_profile_enable": (_I, [_P, _I]),
@@ -238,6 +242,11 @@ def remask_sampler(eta, top_p=0.0):
     return tadm_sampler(kind=STEP_REMASK, eta=eta, top_p=top_p)
 
 
+def loop_sampler(eta=0.02, t_on=0.55, t_off=0.05, alpha_on=0.9, top_p=0.0):
+    """ReMDM-Loop remasking sampler (defaults: the paper's settings for T >= L)."""
+    return tadm_sampler(kind=SAMPLER_LOOP, eta=eta, top_p=top_p, t_on=t_on, t_off=t_off, alpha_on=alpha_on)
+
+
 def tadm_unmask_count(M0, i, T):
     return lib.tadm_unmask_count(M0, i, T)
 
@@ -246,6 +255,13 @@ def tadm_remask_probs(i, T, eta):
     """(sigma, p_unmask) as float32 values computed by the library."""
     sg, pu = C.c_float(), C.c_float()
     lib.tadm_remask_probs(i, T, eta, C.byref(sg), C.byref(pu))
+    return sg.value, pu.value
+
+
+def tadm_loop_probs(i, T, eta, t_on, t_off, alpha_on):
+    """(sigma, p_unmask) of the ReMDM-Loop schedule as float32 values computed by the library."""
+    sg, pu = C.c_float(), C.c_float()
+    lib.tadm_loop_probs(i, T, eta, t_on, t_off, alpha_on, C.byref(sg), C.byref(pu))
     return sg.value, pu.value
 
 

@@ -1173,9 +1173,32 @@ tadm_status tadm_sample(tadm_model* m, const float* logits_dev, const int32_t* c
 // Algorithm 1 per block; the model-owned cache, context and window are reused
 // across calls, so a warm generation allocates nothing and never synchronises.
 void tadm_remask_probs(int32_t i, int32_t T, float eta, float* sigma, float* p_unmask) {
+#pragma clang fp contract(off)
   const double a_t = 1.0 - (double)i / T, a_s = 1.0 - (double)(i - 1) / T;
   const double cap = a_t > 0.0 ? (1.0 - a_s) / a_t : INFINITY;
   const double sg = std::min((double)eta, cap);
+  if (sigma) *sigma = (float)sg;
+  if (p_unmask) *p_unmask = (float)((a_s - (1.0 - sg) * a_t) / (1.0 - a_t));
+}
+
+namespace {
+// alpha(t) of the ReMDM-Loop schedule: linear 0 -> alpha_on on [t_on, 1], flat on
+// [t_off, t_on], linear alpha_on -> 1 on [0, t_off]
+double loop_alpha(double t, double t_on, double t_off, double a_on) {
+#pragma clang fp contract(off)
+  if (t >= t_on) return a_on * (1.0 - t) / (1.0 - t_on);
+  if (t >= t_off) return a_on;
+  return a_on + (1.0 - a_on) * (t_off - t) / t_off;
+}
+}  // namespace
+
+void tadm_loop_probs(int32_t i, int32_t T, float eta, double t_on, double t_off, double alpha_on, float* sigma,
+                     float* p_unmask) {
+#pragma clang fp contract(off)
+  const double t = (double)i / T, s = (double)(i - 1) / T;
+  const double a_t = loop_alpha(t, t_on, t_off, alpha_on), a_s = loop_alpha(s, t_on, t_off, alpha_on);
+  double sg = 0.0;
+  if (t <= t_on && s >= t_off) sg = std::min((double)eta, (1.0 - a_s) / a_t);
   if (sigma) *sigma = (float)sg;
   if (p_unmask) *p_unmask = (float)((a_s - (1.0 - sg) * a_t) / (1.0 - a_t));
 }
@@ -1190,12 +1213,16 @@ tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, i
 tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int32_t B, int32_t P, int32_t gen_len,
                                   int32_t T, int32_t K, int32_t block_len, uint64_t seed, float temperature,
                                   const tadm_sampler* sampler, int32_t* tokens_dev) {
-  TRY(check_model(m));
-  const bool remask = sampler && sampler->kind == TADM_STEP_REMASK;
+  const bool loop = sampler && sampler->kind == TADM_SAMPLER_LOOP;
+  const bool remask = loop || (sampler && sampler->kind == TADM_STEP_REMASK);
   if (sampler && sampler->kind != TADM_STEP_RANKED && !remask)
     return fail(TADM_ERR_INVALID, "sampler kind %d", sampler->kind);
   if (remask && !(sampler->eta >= 0.f && sampler->eta <= 1.f)) return fail(TADM_ERR_INVALID, "eta outside [0, 1]");
+  if (loop && !(0.0 < sampler->t_off && sampler->t_off < sampler->t_on && sampler->t_on < 1.0 &&
+                0.0 < sampler->alpha_on && sampler->alpha_on < 1.0))
+    return fail(TADM_ERR_INVALID, "loop schedule needs 0 < t_off < t_on < 1 and 0 < alpha_on < 1");
   if (sampler && !(sampler->top_p >= 0.f && sampler->top_p <= 1.f)) return fail(TADM_ERR_INVALID, "top_p outside [0, 1]");
+  TRY(check_model(m));
   if (!tokens_dev || (P > 0 && !prompt_dev)) return fail(TADM_ERR_INVALID, "null argument");
   if (B < 1 || B > m->cfg.max_batch) return fail(TADM_ERR_INVALID, "B=%d outside [1, %d]", B, m->cfg.max_batch);
   if (P < 0 || gen_len < 1 || block_len < 1 || gen_len % block_len)
@@ -1221,7 +1248,10 @@ tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int3
   auto set_step = [&](int M0, int i) {
     a.i = i;
     a.n_unmask = tadm_unmask_count(M0, i, T);
-    if (remask) tadm_remask_probs(i, T, sampler->eta, &a.sigma, &a.p_unmask);
+    if (loop)
+      tadm_loop_probs(i, T, sampler->eta, sampler->t_on, sampler->t_off, sampler->alpha_on, &a.sigma, &a.p_unmask);
+    else if (remask)
+      tadm_remask_probs(i, T, sampler->eta, &a.sigma, &a.p_unmask);
   };
   HIPCHK(init_canvas(prompt_dev, B, P, gen_len, mask, tokens_dev, m->stream));
   tadm_cache* cache = m->gcache;

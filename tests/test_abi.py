@@ -84,3 +84,24 @@ def test_remask_probs_match_the_oracle():
                 sg, pu = tadm.tadm_remask_probs(i, T, eta)
                 rs, rp = loop.remask_probs(i, T, eta)
                 assert np.float32(sg) == rs and np.float32(pu) == rp, (i, T, eta)
+
+
+def test_loop_probs_match_the_oracle():
+    """The library's ReMDM-Loop (sigma, p_unmask) are the oracle's float32 numbers at every
+    step, including the steps at the plateau's edges."""
+    from oracle import loop
+    for T in (1, 2, 20, 40, 64, 100, 1024, 4096):
+        for params in ((0.02, 0.55, 0.05, 0.9), (0.04, 0.7, 0.2, 0.5), (0.5, 0.55, 0.05, 0.9), (0.0, 0.5, 0.25, 0.6)):
+            for i in range(1, T + 1):
+                sg, pu = tadm.tadm_loop_probs(i, T, *params)
+                rs, rp = loop.loop_probs(i, T, *params)
+                assert np.float32(sg) == rs and np.float32(pu) == rp, (i, T, params)
+
+
+def test_loop_sampler_rejects_bad_schedules():
+    cfg = synth.get_config("tiny")
+    for bad in (dict(t_on=0.05, t_off=0.55), dict(t_on=1.0), dict(t_off=0.0), dict(alpha_on=1.0), dict(eta=1.5)):
+        smp = tadm.loop_sampler(**bad)
+        st = tadm.lib.tadm_generate_sampler(None, None, 1, 0, 8, 4, 1, 8, 0, 1.0, C.byref(smp), None)
+        assert st != 0
+        assert re.search(rb"loop schedule|eta", tadm.lib.tadm_last_error()), bad

@@ -426,6 +426,37 @@ def test_tiny_remask_generation_matches_oracle(eta, block, top_p):
     assert (got != synth.mask_id(cfg)).all()
 
 
+@pytest.mark.parametrize("T,block,top_p,params", [
+    (32, False, 0.0, (0.02, 0.55, 0.05, 0.9)),   # the paper's ReMDM-Loop settings, T >= L
+    (48, True, 0.9, (0.02, 0.55, 0.05, 0.9)),
+    (40, False, 0.0, (0.3, 0.7, 0.2, 0.5)),      # long plateau, strong remasking
+])
+def test_tiny_loop_generation_matches_oracle(T, block, top_p, params):
+    """Whole generations with the ReMDM-Loop schedule are token-identical to the oracle's
+    Algorithm 1 with the same posterior, and end fully unmasked."""
+    cfg = synth.get_config("tiny", batch=2, n_kv_heads=2 if block else 4)
+    K = 4
+    B, P, G = 2, cfg["prompt_len"], cfg["gen_len"]
+    bl = 8 if block else G
+    tensors = synth.make_weights(cfg, perturb=True)
+    prompt = synth.make_prompt(cfg, batch=B)
+    m = gpu_model(cfg, tensors, B, P + G)
+    eta, t_on, t_off, a_on = params
+    try:
+        out = torch.empty(B, P + G, dtype=torch.int32, device=dev())
+        tadm.tadm_generate_sampler(m, prompt.to(dev()), B, P, G, T, K, bl, 5, 1.0,
+                                   tadm.loop_sampler(eta, t_on, t_off, a_on, top_p), out)
+        sync()
+        got = out.cpu().numpy()
+    finally:
+        tadm.tadm_model_destroy(m)
+    net = oracle_net(cfg, tensors)
+    ref = loop.generate(net, prompt.numpy(), G, T, K, bl, 5, 1.0, synth.mask_id(cfg), loop=params,
+                        top_p=float(np.float32(top_p)) if top_p else 1.0)
+    np.testing.assert_array_equal(got, ref)
+    assert (got != synth.mask_id(cfg)).all()
+
+
 @pytest.mark.parametrize("T,K,block_len,temp", [
     (1, 1, None, 1.0),     # a single reverse step reveals everything
     (40, 3, None, 0.5),    # more steps than positions: many steps reveal nothing; K does not divide T

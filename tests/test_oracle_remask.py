@@ -131,3 +131,86 @@ def test_nucleus_sampling_follows_the_truncated_softmax():
     e = n * pr[keep]
     chi2 = ((counts[keep] - e) ** 2 / e).sum()
     assert chi2 < 25.0  # <= 5 dof, p ~ 1e-4
+
+
+LOOP = (0.02, 0.55, 0.05, 0.9)  # eta, t_on, t_off, alpha_on of the paper's runs with T >= L
+
+
+def _loop_marginals(T, params):
+    """Expected masked fraction after each reverse step, by the posterior's own
+    recursion m_s = m_t (1 - p_unmask) + (1 - m_t) sigma from the all-mask canvas."""
+    m, out = 1.0, []
+    for i in range(T, 0, -1):
+        sigma, p = loop.loop_probs(i, T, *params)
+        m = m * (1.0 - float(p)) + (1.0 - m) * float(sigma)
+        out.append(((i - 1) / T, m, float(sigma), float(p)))
+    return out
+
+
+def test_loop_schedule_phases():
+    """ReMDM-Loop: the masked fraction falls linearly from 1 to 1 - alpha_on while t goes
+    from 1 to t_on, holds there (remasking with sigma = eta) down to t_off, and falls
+    linearly to 0 at t = 0; sigma is eta exactly on the plateau steps and 0 elsewhere."""
+    eta, t_on, t_off, a_on = LOOP
+    for T in (20, 64, 100, 1024):
+        rows = _loop_marginals(T, LOOP)
+        assert rows[-1][1] == 0.0 or abs(rows[-1][1]) < 1e-12           # all decoded at t = 0
+        for k, (s, m, sigma, p) in enumerate(rows):
+            t = s + 1 / T
+            plateau = t <= t_on + 1e-12 and s >= t_off - 1e-12
+            assert 0.0 <= p <= 1.0 and 0.0 <= sigma <= 1.0
+            if plateau:
+                assert sigma == np.float32(eta)
+                assert abs(m - (1 - a_on)) < 1e-6, (T, s, m)             # the loop holds the marginal
+            else:
+                assert sigma == 0.0
+        # linear on each side of the plateau: constant decrements per step
+        for lo, hi in ((t_on, 1.0), (0.0, t_off)):
+            ms = [m for s, m, _, _ in rows if lo + 1e-9 < s + 1 / T and s < hi + 1e-9 and lo - 1e-9 <= s]
+            d = np.diff([1.0] + ms) if hi == 1.0 else np.diff(ms)
+            if len(d) > 1:
+                assert np.ptp(d) < 1e-6, (T, lo, hi)
+        # endpoints of the two ramps
+        first_plateau = min(s for s, _, sg, _ in rows if sg > 0)
+        assert abs(dict((s, m) for s, m, _, _ in rows)[first_plateau] - (1 - a_on)) < 1e-6
+
+
+def test_loop_with_eta_zero_is_an_absorbing_chain():
+    """eta = 0: every step is the absorbing posterior p = (alpha_s - alpha_t)/(1 - alpha_t)
+    of the piecewise schedule; the plateau steps then reveal nothing."""
+    T = 40
+    for i in range(T, 0, -1):
+        sigma, p = loop.loop_probs(i, T, 0.0, 0.55, 0.05, 0.9)
+        assert sigma == 0.0
+        t, s = i / T, (i - 1) / T
+        if t <= 0.55 and s >= 0.05:
+            assert p == 0.0
+
+
+def test_loop_chain_follows_its_marginal_and_remasks():
+    """Simulated ReMDM-Loop chain through the oracle's reverse step: the masked fraction
+    tracks the posterior's recursion, decoded tokens are remasked on the plateau at rate
+    sigma, and the chain ends fully decoded."""
+    rng = np.random.default_rng(3)
+    Lc, V, T = 4000, 3, 40
+    logits = rng.normal(size=(Lc, V)).astype(np.float32)
+    z = np.full(Lc, V)
+    remasked_total = 0
+    for i in range(T, 0, -1):
+        sigma, p = loop.loop_probs(i, T, *LOOP)
+        frac_t = (z == V).mean()
+        expect = frac_t * (1 - float(p)) + (1 - frac_t) * float(sigma)
+        nxt, _ = S.remask_step(logits, z, V, p, sigma, 0, 1, T - i, 23, np.float32(1.0))
+        decoded = z != V
+        remasked = (decoded & (nxt == V)).sum()
+        if sigma > 0:
+            n = decoded.sum()
+            assert abs(remasked / n - float(sigma)) < 5 * math.sqrt(float(sigma) * (1 - float(sigma)) / n) + 1e-9
+        else:
+            assert remasked == 0
+        remasked_total += remasked
+        z = nxt
+        frac = (z == V).mean()
+        assert abs(frac - expect) < 5 * math.sqrt(max(expect * (1 - expect), 1e-9) / Lc) + 1e-9
+    assert remasked_total > 0
+    assert (z != V).all()
