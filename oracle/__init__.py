@@ -11,10 +11,14 @@ computes, written from the paper:
   whose decisions are taken in float32, the precision the GPU kernel uses
   (App. B.1.1, MDLM zero-masking and carry-over);
 * ``loop``     -- anchor-cache inference (Algorithm 1) with the linear unmask
-  schedule and block diffusion with a context KV.
+  schedule and block diffusion with a context KV, the remasking samplers (ReMDM-Cap
+  and ReMDM-Loop) and the uniform-state generation of Algorithm 2;
+* ``usdm``     -- the entropy-bound sampler of Algorithm 2: temperature schedule,
+  Gumbel-max draw, fixed-point entropy, entropy-bound acceptance, uniform re-noising
+  and the self-conditioning signal.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's ``cpu_baseline``
 leg may import this package.  It shares no code with the GPU path; the only common
 dependency is the seeded input module ``synth``.
 """
-from . import network, sampler, loop  # noqa: F401
+from . import network, sampler, loop, usdm  # noqa: F401

@@ -161,6 +161,64 @@ def generate(net, prompt, gen_len, T, K, block_len, seed, temperature, mask_id,
     return seq
 
 
+def generate_usdm(net, prompt, gen_len, T, K, block_len, seed, eta=0.1, tau_max=0.8, tau_min=0.4, trace=None):
+    """Algorithm 1 with the entropy-bound sampler of Algorithm 2 (uniform-state
+    diffusion) on every row of ``prompt`` [B, P]; returns tokens [B, P+gen_len].
+
+    Each block starts from uniform noise (``usdm.initial_tokens``) and a zero
+    self-conditioning signal; step n uses temperature tau_n and the anchor is refreshed
+    iff (T - n) mod K == 0, with the self-conditioning signal of the previous step
+    added to the canvas embeddings of every decoder pass (the anchor's included).  The
+    last step leaves the argmax canvas.  Step ids and block mode as in ``generate``."""
+    from . import usdm
+    cfg = net.cfg
+    prompt = np.asarray(prompt, dtype=np.int64)
+    B, P = prompt.shape
+    V, d = cfg["vocab"], cfg["d_model"]
+    if gen_len % block_len != 0 or T < 1 or K < 1:
+        raise ValueError("invalid generation arguments")
+    seq = np.concatenate([prompt, np.zeros((B, gen_len), dtype=np.int64)], axis=1)
+    single = block_len == gen_len
+    if single:
+        windows = [(0, P, P + gen_len)]
+        ctx = [None] * B
+    else:
+        windows = [(P + j * block_len, P + j * block_len, P + (j + 1) * block_len)
+                   for j in range(gen_len // block_len)]
+        ctx = [net.fresh_kv(seq[b, :P], np.arange(P)) if P > 0 else None for b in range(B)]
+    E = net.W["embed"]
+    for j, (w0, c0, w1) in enumerate(windows):
+        pos = np.arange(w0, w1)
+        for b in range(B):
+            seq[b, c0:w1] = usdm.initial_tokens(np.arange(c0, w1), b, j, seed, V)
+        caches = [None] * B
+        sc = np.zeros((B, w1 - w0, d))
+        for n in range(T, 0, -1):
+            step_id = j * T + (T - n)
+            inv_temp = usdm.inv_temperature(n, T, tau_max, tau_min)
+            refresh = is_refresh(n, T, K)
+            for b in range(B):
+                c = net.shared(seq[b, w0:w1], pos, ctx[b], sc=sc[b])
+                if refresh:
+                    caches[b] = net.anchor_cache(c, pos, ctx[b])
+                xf = net.denoise(net.fuse(c, caches[b]), pos, ctx[b])
+                logits = net.head(xf[c0 - w0:]).astype(np.float32)
+                r = usdm.entropy_step(logits, n, inv_temp, eta, c0, b, step_id, seed)
+                if trace is not None:
+                    trace.append(dict(block=j, n=n, row=b, step_id=step_id, refresh=refresh,
+                                      canvas=seq[b, c0:w1].copy(), **r))
+                if n > 1:
+                    sc[b, c0 - w0:] = usdm.selfcond(logits, inv_temp, E)
+                seq[b, c0:w1] = r["next"]
+        if not single:
+            for b in range(B):
+                kv = net.fresh_kv(seq[b, w0:w1], pos, ctx[b])
+                ctx[b] = kv if ctx[b] is None else {
+                    li: (np.concatenate([ctx[b][li][0], kv[li][0]]),
+                         np.concatenate([ctx[b][li][1], kv[li][1]])) for li in kv}
+    return seq
+
+
 def layer_call_count(T, K, L_shared, L_anchor, L_denoise):
     """Closed form of eq. anchor-cache-compute: T (L_S + L_D) + ceil(T/K) L_A."""
     return T * (L_shared + L_denoise) + -(-T // K) * L_anchor

@@ -162,9 +162,13 @@ def run_layers(W, part, x, pos, ctx=None, kv_out=None):
 
 
 # ------------------------------------------------------------------- S, A, D, head
-def shared(W, z, pos, ctx=None, kv_out=None):
-    """c = S(z): embedding lookup (the embedding has a row for the mask id)."""
+def shared(W, z, pos, ctx=None, kv_out=None, sc=None):
+    """c = S(z): embedding lookup (the embedding has a row for the mask id).  sc, the
+    self-conditioning signal of Algorithm 2 ([len(z), d] or None), is added to the
+    embeddings."""
     c = W["embed"][np.asarray(z)]
+    if sc is not None:
+        c = c + np.asarray(sc, dtype=np.float64)
     return run_layers(W, "shared", c, pos, ctx, kv_out)
 
 
@@ -261,8 +265,8 @@ class Network:
         self.W = W
         self.cfg = W.cfg
 
-    def shared(self, z, pos, ctx=None):
-        return shared(self.W, z, pos, ctx)
+    def shared(self, z, pos, ctx=None, sc=None):
+        return shared(self.W, z, pos, ctx, sc=sc)
 
     def anchor_cache(self, c, pos, ctx=None):
         """Anchor refresh: the cache stores h' = A(c') and c' itself."""
