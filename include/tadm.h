@@ -191,7 +191,7 @@ int32_t tadm_unmask_count(int32_t M0, int32_t i, int32_t T);
  * 1 - alpha_s - sigma alpha_t non-negative (ReMDM-Cap's form; eta = 0 is the plain
  * absorbing posterior), on the linear schedule alpha_t = 1 - t.
  * kind TADM_SAMPLER_LOOP: the ReMDM-Loop schedule (the paper's sampler for T >= L,
- * App. D sampler details, with eta = 0.02, t_on = 0.55, t_off = 0.05, alpha_on = 0.9):
+ * App. C.2 sampler details, with eta = 0.02, t_on = 0.55, t_off = 0.05, alpha_on = 0.9):
  * alpha rises linearly from 0 at t = 1 to alpha_on at t_on, stays at alpha_on down to
  * t_off and rises linearly to 1 at t = 0; steps wholly inside [t_off, t_on] remask with
  * sigma = min(eta, (1 - alpha_s) / alpha_t), the others have sigma = 0.  Its steps run

@@ -45,7 +45,7 @@ def remask_probs(i, T, eta):
 
 
 def loop_alpha(t, t_on, t_off, alpha_on):
-    """alpha(t) of the ReMDM-Loop schedule (reading of the sampler details, App. D, after
+    """alpha(t) of the ReMDM-Loop schedule (reading of the sampler details, App. C.2, after
     the ReMDM paper): rises linearly from 0 at t = 1 to alpha_on at t_on, stays at
     alpha_on down to t_off, rises linearly to 1 at t = 0."""
     if t >= t_on:
