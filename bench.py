@@ -472,6 +472,17 @@ def main():
         print(f"[bench] remasking sampler {key}, K={K0}: {rms:.3f} ms -> {tokens / (rms / 1e3):.1f} tokens/s",
               file=sys.stderr, flush=True)
         T_run[0] = T
+        # the entropy-bound sampler of uniform-state diffusion (eta = 0.1, tau 0.8 -> 0.4,
+        # T = 48, self-conditioning) at the refresh intervals the paper pairs with it
+        sampler[0] = tadm.entropy_sampler(0.1, 0.8, 0.4)
+        T_run[0] = 48
+        for K in (1, 2, 3):
+            rms, _, _ = timed(K, 2, 1)
+            key = f"entropy,T=48,eta=0.1,K={K}"
+            remask[key] = {"K": K, "T": 48, "tokens_per_s": tokens / (rms / 1e3), "ms_per_step": rms}
+            print(f"[bench] entropy-bound sampler T=48, K={K}: {rms:.3f} ms -> {tokens / (rms / 1e3):.1f} tokens/s",
+                  file=sys.stderr, flush=True)
+        T_run[0] = T
         sampler[0] = None
     roof = None
     if dom:
@@ -499,7 +510,7 @@ def main():
         "config": {"workload": workload_name(cfg), "global_batch": B, "seq_len": P + G, "K": K0,
                    "parallelism": "none (1 GPU)"},
         "k_sweep": sweep,
-        "remask_sampler": remask,
+        "samplers": remask,
         "stages_ms_per_step": {k: v["ms_per_step"] for k, v in stages.items()},
         "kernels": [{k: v for k, v in r.items() if k != "stages"} for r in kernels],
         "roofline": roof,

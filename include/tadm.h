@@ -82,13 +82,29 @@ typedef struct {
   float sigma;         /* REMASK: probability that a decoded position is remasked     */
   float top_p;         /* in (0, 1): tokens come from the top-p nucleus (exact fixed-point
                           weights, ties at the boundary kept); 0 or 1: the whole vocabulary */
+  float entropy_eta;   /* ENTROPY: the entropy bound eta >= 0                          */
+  const float* sc_in;  /* ENTROPY: nullable device [B, L - canvas_off, d] float32, the
+                          self-conditioning signal added to the canvas embeddings      */
+  float* sc_out;       /* ENTROPY: nullable device [B, L - canvas_off, d] float32,
+                          receives s = softmax(logits * inv_temp) E (may alias sc_in)  */
 } tadm_step_args;
 
 /* Reverse-step kinds.  REMASK is the posterior of eq. inf-post-TADM (the ReMDM form,
  * Sec. 3 and App. B): per canvas position, one uniform u from Philox4x32-10 word 0 at
  * counter (2^31, absolute position, row, step_id); a masked position becomes its
  * Gumbel-max token iff u < p_unmask, a decoded one becomes the mask iff u < sigma. */
-enum { TADM_STEP_RANKED = 0, TADM_STEP_REMASK = 1 };
+/* ENTROPY is a step of the uniform-state entropy-bound sampler (Algorithm 2, App. C.1):
+ * every canvas position gets x_hat = argmax of its logits, x_tilde = the Gumbel-max
+ * draw at inv_temp (the counters of the masked sampler) and the entropy H of
+ * softmax(logits * inv_temp), summed in 2^-40 fixed point (A = sum rint(e 2^40),
+ * B = sum rint(-y e 2^40), e = exp(y), y = l' - max l'; H = log(A 2^-40) + B / A).
+ * Positions in ascending (H, position) order are accepted while the entropies ranked
+ * before them sum to at most eta (exact integer sums of rint(H 2^40)); accepted
+ * positions take x_tilde, the others a uniform token ((w V) >> 32, w = Philox word 0
+ * at counter (2^31 + 1, absolute position, row, step_id)); at i = 1 every position
+ * takes x_hat.  The decoder adds sc_in to the canvas embeddings of its passes (the
+ * reading of Decoder(z, s)), and sc_out receives the next step's signal. */
+enum { TADM_STEP_RANKED = 0, TADM_STEP_REMASK = 1, TADM_STEP_ENTROPY = 2 };
 
 /* ---------------------------------------------------------------- model ---- */
 /* Number of weight tensors of a configuration, and the shape of tensor `index`
@@ -140,13 +156,20 @@ tadm_status tadm_context_destroy(tadm_context* ctx);
  * NULL: positions [0, L)).  (i, T) is recorded as the refresh step. */
 tadm_status tadm_anchor_forward(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev,
                                 int32_t B, int32_t L, int32_t i, int32_t T, tadm_cache* cache);
+/* The same with a self-conditioning signal sc_dev [B, L - canvas_off, d] float32 added to
+ * the embeddings of the canvas columns [canvas_off, L) (the decoder input of Algorithm 2;
+ * NULL: none). */
+tadm_status tadm_anchor_forward_sc(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev,
+                                   int32_t B, int32_t L, int32_t i, int32_t T, const float* sc_dev,
+                                   int32_t canvas_off, tadm_cache* cache);
 
 /* One reverse step on a stale (or fresh) cache (Sec. 3.1, eq. DenoiserOp;
  * MDLM posterior with carry-over, App. B.1.1):
  * c = S(canvas), h~ = Phi(c, cache), x = D(h~), logits = head(x) for the canvas
  * columns [canvas_off, L), then tadm_sample.  logits_dev (float32
  * [B, L - canvas_off, V]) may be NULL: then the head runs only on the masked
- * positions (the only ones whose logits the reverse step uses).  next_canvas_dev
+ * positions (the only ones whose logits the reverse step uses; in ENTROPY mode every
+ * canvas position goes through the head).  next_canvas_dev
  * [B, L] receives the canvas after the step (it may alias canvas_dev).  The cache
  * is read only. */
 tadm_status tadm_denoise_step(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev,
@@ -166,7 +189,10 @@ tadm_status tadm_denoise_step(tadm_model* m, const tadm_context* ctx, const int3
  * (confidence, then lowest position) take their token; every other entry of
  * canvas_dev is copied.
  * choice_dev / conf_dev ([B, L - canvas_off], nullable) receive the sampled token
- * and confidence (-1 / -inf where not masked). */
+ * and confidence (-1 / -inf where not masked).
+ * In ENTROPY mode every position is sampled: choice_dev receives x_tilde and conf_dev
+ * the entropy H; the rest follows TADM_STEP_ENTROPY (sc_in is not used here, the
+ * self-conditioning signal needs the model's embedding; L - canvas_off <= 8192). */
 tadm_status tadm_sample(tadm_model* m, const float* logits_dev, const int32_t* canvas_dev,
                         int32_t B, int32_t L, int32_t canvas_off, int32_t pos0,
                         const tadm_step_args* args, int32_t* next_canvas_dev,
@@ -197,11 +223,20 @@ int32_t tadm_unmask_count(int32_t M0, int32_t i, int32_t T);
  * sigma = min(eta, (1 - alpha_s) / alpha_t), the others have sigma = 0.  Its steps run
  * in TADM_STEP_REMASK mode.  Needs 0 < t_off < t_on < 1 and 0 < alpha_on < 1. */
 enum { TADM_SAMPLER_LOOP = 2 };
+/* kind TADM_SAMPLER_ENTROPY: uniform-state generation with the entropy-bound sampler
+ * (Algorithm 2; the paper's settings eta = 0.1, tau 0.8 -> 0.4, T = 48, canvas blocks of
+ * 256): each block starts from uniform tokens ((w V) >> 32, w = Philox word 0 at
+ * counter (2^31 + 2, absolute position, row, block index)) and a zero self-conditioning
+ * signal; step n runs at 1 / tau_n = tadm_entropy_inv_temp(n, T, tau_max, tau_min) in
+ * TADM_STEP_ENTROPY mode with eta the entropy bound, feeding each step's signal s = pE
+ * to the next.  The result is the last step's argmax canvas; `temperature` is unused. */
+enum { TADM_SAMPLER_ENTROPY = 3 };
 typedef struct {
   int32_t kind;
   float eta;
   float top_p;  /* nucleus of the sampled tokens (0 or 1: off); the paper's runs use 0.9 */
   double t_on, t_off, alpha_on;  /* TADM_SAMPLER_LOOP only */
+  float tau_max, tau_min;        /* TADM_SAMPLER_ENTROPY only: 0 < tau_min <= tau_max */
 } tadm_sampler;
 
 /* Pure host helper: (sigma, p_unmask) of reverse step i under the capped schedule,
@@ -211,6 +246,10 @@ void tadm_remask_probs(int32_t i, int32_t T, float eta, float* sigma, float* p_u
  * ReMDM-Loop schedule described above, computed in double and rounded to float. */
 void tadm_loop_probs(int32_t i, int32_t T, float eta, double t_on, double t_off, double alpha_on, float* sigma,
                      float* p_unmask);
+
+/* Pure host helper: float32(1 / tau_n), tau_n = tau_min + (tau_max - tau_min) n / T
+ * computed in double (the temperature schedule of Algorithm 2). */
+float tadm_entropy_inv_temp(int32_t n, int32_t T, float tau_max, float tau_min);
 
 /* tadm_generate with a sampler (NULL: confidence-ranked). */
 tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int32_t B, int32_t P,
@@ -246,7 +285,9 @@ enum {
    * feed-forward up (gate+up) and down projections, fusion GEMM 1 and 2 */
   TADM_STAGE_QKV = 8, TADM_STAGE_ATTN = 9, TADM_STAGE_OPROJ = 10, TADM_STAGE_FFN_UP = 11,
   TADM_STAGE_FFN_DOWN = 12, TADM_STAGE_FUSION1 = 13, TADM_STAGE_FUSION2 = 14,
-  TADM_STAGE_COUNT = 15
+  /* the self-conditioning product s = pE of the entropy-bound sampler */
+  TADM_STAGE_SELFCOND = 15,
+  TADM_STAGE_COUNT = 16
 };
 tadm_status tadm_profile_enable(tadm_model* m, int32_t stage_mask);
 tadm_status tadm_profile_read(tadm_model* m, int32_t stage, double* total_ms, int64_t* count);

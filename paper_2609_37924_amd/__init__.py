@@ -26,7 +26,7 @@ FUSION = {"gated_mlp": 0, "paired": 1}
 CACHE_H, CACHE_C, CACHE_A = 0, 1, 2
 TAP_EMBED, TAP_FUSED, TAP_FINAL, TAP_CHOICE, TAP_CONF = 0, 1, 2, 3, 4
 STAGES = ["embed", "anchor", "fusion", "denoise", "head", "sample", "select", "context",
-          "qkv", "attn", "oproj", "ffn_up", "ffn_down", "fusion1", "fusion2"]
+          "qkv", "attn", "oproj", "ffn_up", "ffn_down", "fusion1", "fusion2", "selfcond"]
 
 
 class tadm_config(C.Structure):
@@ -41,16 +41,18 @@ class tadm_step_args(C.Structure):
     _fields_ = [("i", C.c_int32), ("T", C.c_int32), ("n_unmask", C.c_int32),
                 ("step_id", C.c_uint32), ("seed", C.c_uint64), ("inv_temp", C.c_float),
                 ("n_unmask_rows", C.c_void_p), ("mode", C.c_int32), ("p_unmask", C.c_float),
-                ("sigma", C.c_float), ("top_p", C.c_float)]
+                ("sigma", C.c_float), ("top_p", C.c_float), ("entropy_eta", C.c_float),
+                ("sc_in", C.c_void_p), ("sc_out", C.c_void_p)]
 
 
 class tadm_sampler(C.Structure):
     _fields_ = [("kind", C.c_int32), ("eta", C.c_float), ("top_p", C.c_float),
-                ("t_on", C.c_double), ("t_off", C.c_double), ("alpha_on", C.c_double)]
+                ("t_on", C.c_double), ("t_off", C.c_double), ("alpha_on", C.c_double),
+                ("tau_max", C.c_float), ("tau_min", C.c_float)]
 
 
-STEP_RANKED, STEP_REMASK = 0, 1
-SAMPLER_LOOP = 2
+STEP_RANKED, STEP_REMASK, STEP_ENTROPY = 0, 1, 2
+SAMPLER_LOOP, SAMPLER_ENTROPY = 2, 3
 
 
 class TadmError(RuntimeError):
@@ -78,6 +80,8 @@ _SIGS = {
     "tadm_context_reset": (_I, [_P]),
     "tadm_context_destroy": (_I, [_P]),
     "tadm_anchor_forward": (_I, [_P, _P, _P, _I, _I, _I, _I, _P]),
+    "tadm_anchor_forward_sc": (_I, [_P, _P, _P, _I, _I, _I, _I, _P, _I, _P]),
+    "tadm_entropy_inv_temp": (C.c_float, [_I, _I, C.c_float, C.c_float]),
     "tadm_denoise_step": (_I, [_P, _P, _P, _I, _I, _I, _P, C.POINTER(tadm_step_args), _P, _P]),
     "tadm_sample": (_I, [_P, _P, _P, _I, _I, _I, _I, C.POINTER(tadm_step_args), _P, _P, _P]),
     "tadm_generate": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, C.c_uint64, C.c_float, _P]),
@@ -206,15 +210,28 @@ def tadm_anchor_forward(m, ctx, canvas, B, L, i, T, cache):
     check(lib.tadm_anchor_forward(m, ctx, ptr(canvas), B, L, i, T, cache))
 
 
-def step_args(i, T, n_unmask, step_id, seed, inv_temp, n_unmask_rows=None, remask=None, top_p=0.0):
+def step_args(i, T, n_unmask, step_id, seed, inv_temp, n_unmask_rows=None, remask=None, top_p=0.0,
+              entropy_eta=None, sc_in=None, sc_out=None):
     """n_unmask_rows: optional device int32 tensor [B] of per-row counts (kept alive by
     the caller until the step has run).  remask: optional (p_unmask, sigma) selecting the
-    remasking posterior instead of confidence-ranked unmasking."""
+    remasking posterior instead of confidence-ranked unmasking.  entropy_eta selects the
+    entropy-bound step of the uniform-state sampler, with the optional self-conditioning
+    tensors sc_in / sc_out (device float32 [B, Lc, d])."""
     a = tadm_step_args(i=i, T=T, n_unmask=n_unmask, step_id=step_id, seed=seed,
                        inv_temp=inv_temp, n_unmask_rows=ptr(n_unmask_rows), top_p=top_p)
     if remask is not None:
         a.mode, a.p_unmask, a.sigma = STEP_REMASK, remask[0], remask[1]
+    if entropy_eta is not None:
+        a.mode, a.entropy_eta, a.sc_in, a.sc_out = STEP_ENTROPY, entropy_eta, ptr(sc_in), ptr(sc_out)
     return a
+
+
+def tadm_anchor_forward_sc(m, ctx, canvas, B, L, i, T, sc, canvas_off, cache):
+    check(lib.tadm_anchor_forward_sc(m, ctx, ptr(canvas), B, L, i, T, ptr(sc), canvas_off, cache))
+
+
+def tadm_entropy_inv_temp(n, T, tau_max, tau_min):
+    return lib.tadm_entropy_inv_temp(n, T, tau_max, tau_min)
 
 
 def tadm_denoise_step(m, ctx, canvas, B, L, canvas_off, cache, args, logits, next_canvas):
@@ -240,6 +257,11 @@ def tadm_generate_sampler(m, prompt, B, P, gen_len, T, K, block_len, seed, tempe
 
 def remask_sampler(eta, top_p=0.0):
     return tadm_sampler(kind=STEP_REMASK, eta=eta, top_p=top_p)
+
+
+def entropy_sampler(eta=0.1, tau_max=0.8, tau_min=0.4):
+    """Entropy-bound sampler of uniform-state diffusion (defaults: the paper's settings)."""
+    return tadm_sampler(kind=SAMPLER_ENTROPY, eta=eta, tau_max=tau_max, tau_min=tau_min)
 
 
 def loop_sampler(eta=0.02, t_on=0.55, t_off=0.05, alpha_on=0.9, top_p=0.0):

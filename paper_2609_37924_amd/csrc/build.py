@@ -1,7 +1,7 @@
 """Builds libtadm.so (gfx950) from the HIP sources next to this file.
 
 Usage: python build.py [--jobs N].  Each source compiles to an object with hipcc
-(-O3, --offload-arch=gfx950, packed-fp32 instructions disabled); the sampler and
+(-O3, --offload-arch=gfx950, packed-fp32 instructions disabled); the samplers and
 the vocabulary projection with the sampling epilogue are compiled without
 floating-point contraction and with correctly rounded division, so that their
 float32 arithmetic is exactly the documented sequence of rounded operations.
@@ -14,9 +14,10 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
-SOURCES = ["runtime.hip", "gemm.hip", "attention.hip", "norm.hip", "sampler.hip", "head_sample.hip", "fusion.hip"]
+SOURCES = ["runtime.hip", "gemm.hip", "attention.hip", "norm.hip", "sampler.hip", "head_sample.hip", "fusion.hip",
+           "usdm.hip"]
 CONTRACT = ["-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt"]
-EXTRA = {"sampler.hip": CONTRACT, "head_sample.hip": CONTRACT}
+EXTRA = {"sampler.hip": CONTRACT, "head_sample.hip": CONTRACT, "usdm.hip": CONTRACT}
 OUT = os.path.join(PKG, "libtadm.so")
 
 

@@ -26,6 +26,14 @@ struct Epi<EPI_STORE_F32, T> {
   }
 };
 template <class T>
+struct Epi<EPI_SCALE_F32, T> {
+  static constexpr bool kGlu = false;
+  __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
+    const float r = e.row1[m];
+    store4(static_cast<float*>(e.out) + (size_t)m * e.ldo + n, r * v[0], r * v[1], r * v[2], r * v[3]);
+  }
+};
+template <class T>
 struct Epi<EPI_RESID, T> {
   static constexpr bool kGlu = false;
   static constexpr int kPre = 1;
@@ -262,6 +270,7 @@ hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e
   switch (kind) {
     case EPI_STORE: return dispatch<EPI_STORE>(dt, p, e, s);
     case EPI_STORE_F32: return dispatch<EPI_STORE_F32>(dt, p, e, s);
+    case EPI_SCALE_F32: return dispatch<EPI_SCALE_F32>(dt, p, e, s);
     case EPI_RESID: return dispatch<EPI_RESID>(dt, p, e, s);
     case EPI_GELU: return dispatch<EPI_GELU>(dt, p, e, s);
     case EPI_GLU_SILU: return dispatch<EPI_GLU_SILU>(dt, p, e, s);

@@ -57,6 +57,7 @@ enum EpiKind {
                       // weight rows) and scatter into the attention layouts (see EpiParams)
   EPI_SAMPLE,         // vocabulary projection: sampling partials per (row, 64-column
                       // group) instead of logits (head_sample only; see EpiParams)
+  EPI_SCALE_F32,      // out(float)[m, n] = row1[m] * acc
 };
 
 struct EpiParams {
@@ -172,6 +173,29 @@ hipError_t sample_finalize(const SamplePart* part, int n_groups, int V, const in
 hipError_t remask_update(const int32_t* canvas, const int32_t* choice, int B, int L, int canvas_off, int mask_id,
                          int pos0, uint32_t step_id, uint64_t seed, float p_unmask, float sigma, int32_t* next,
                          hipStream_t s);
+// Entropy-bound sampler of Algorithm 2 (usdm.hip), rows b * Lc + j at absolute
+// positions pos_base + j.  Per row: xhat = argmax of the logits, xtilde = Gumbel-max
+// draw of softmax(l * inv_temp), H / Hq = entropy in float and 2^-40 fixed point,
+// rscale = 2^40 / A (the softmax normaliser's reciprocal, for the self-conditioning
+// product); P (nullable, element type pt, leading dimension ldp >= V) receives the
+// unnormalised weights exp(l' - m), zero on columns [V, ldp).
+hipError_t entropy_stats(const float* logits, int B, int Lc, int V, int pos_base, uint32_t step_id, uint64_t seed,
+                         float inv_temp, int32_t* xhat, int32_t* xtilde, float* H, long long* Hq, float* rscale,
+                         DType pt, void* P, int ldp, hipStream_t s);
+// Acceptance and next canvas [B, L] (columns before off copied; next may alias canvas):
+// accepted positions take xtilde, the others a uniform token; last != 0 writes xhat.
+// Needs (L - off) * 8 bytes of LDS (L - off <= 8192).
+hipError_t entropy_accept(const long long* Hq, const int32_t* xhat, const int32_t* xtilde, const int32_t* canvas,
+                          int32_t* next, int B, int L, int off, int pos_base, uint32_t step_id, uint64_t seed, int V,
+                          long long etaq, int last, hipStream_t s);
+// A block's first canvas: uniform tokens of positions pos_base + t into tok[b * ld + col0 + t].
+hipError_t init_uniform_tokens(int32_t* tok, int ld, int col0, int B, int n, int pos_base, uint32_t block,
+                               uint64_t seed, int V, hipStream_t s);
+// c[b, off + j, :] += sc[b * (L - off) + j, :] (d % 4 == 0).
+hipError_t add_selfcond(float* c, const float* sc, int B, int L, int off, int d, hipStream_t s);
+// ET[n, v] = E[v, n] (v < V), zero for V <= v < ldt: E [V, d] row-major, ET [d, ldt].
+hipError_t transpose_rows(DType dt, const void* E, int V, int d, void* ET, int ldt, hipStream_t s);
+constexpr int ENTROPY_MAX_CANVAS = 8192;
 // Largest vocabulary the sampler handles: its per-group partials (64 entries per
 // group, 12 bytes each) live in 48 KB of LDS.
 constexpr int SAMPLE_MAX_VOCAB = 4096 * 64;

@@ -234,6 +234,14 @@ struct Workspace {
   int32_t *cidx = nullptr, *row_map = nullptr;  // masked-position list and its inverse
   int* count = nullptr;                         // number of masked positions (device)
   NucleusThr* nthr = nullptr;                   // per-position nucleus thresholds
+  // entropy-bound sampler: argmax, exact entropies, 2^40 / A per row, the weights e_v
+  // [rows, round64(V)] for the self-conditioning product (lazy) and generation's signal
+  int32_t* xhat = nullptr;
+  long long* hq = nullptr;
+  float* rscale = nullptr;
+  void* pw = nullptr;
+  size_t pw_cap = 0;
+  float* sc = nullptr;
   float* logits = nullptr;
   size_t logits_cap = 0;
   int kv_cap = 0;
@@ -268,6 +276,8 @@ struct tadm_model {
   tadm_cache* gcache = nullptr;    // anchor cache of tadm_generate
   tadm_context* gctx = nullptr;    // context of block-mode tadm_generate
   int32_t* gwin = nullptr;         // active block of block-mode tadm_generate
+  void* embT = nullptr;            // embedding rows [0, V) transposed, [d, round64(V)] (lazy)
+  bool embT_valid = false;
   int tap_B = 0, tap_L = 0, tap_Lc = 0;
   // profiling
   int32_t prof_mask = 0;  // bit s: record stage s
@@ -392,6 +402,9 @@ static tadm_status ensure_workspace(tadm_model* m) {
   TRY(ws_alloc(m, (void**)&w.count, 256));
   TRY(ws_alloc(m, (void**)&w.conf, N * 4));
   TRY(ws_alloc(m, (void**)&w.nthr, N * sizeof(NucleusThr)));
+  TRY(ws_alloc(m, (void**)&w.xhat, N * 4));
+  TRY(ws_alloc(m, (void**)&w.hq, N * 8));
+  TRY(ws_alloc(m, (void**)&w.rscale, N * 4));
   w.n_tok = (int)N;
   w.n_canvas = (int)N;
   return TADM_OK;
@@ -499,12 +512,14 @@ static tadm_status run_part(tadm_model* m, int first, int count, float* x, int B
   return TADM_OK;
 }
 
-// c = S(z): embedding gather then the shared layers (in place on `c`).
+// c = S(z): embedding gather (plus the self-conditioning signal sc on the columns
+// [off, L), if given) then the shared layers (in place on `c`).
 static tadm_status shared_net(tadm_model* m, const tadm_context* ctx, const int32_t* z, int B, int L,
-                              float* c) {
+                              float* c, const float* sc = nullptr, int off = 0) {
   const int pos0 = ctx ? ctx->len : 0;
   HIPCHK(embed_gather(m->dt, z, B * L, m->W(m->lay.embed), m->cfg.vocab + 1, m->cfg.d_model, c,
                       m->stream));
+  if (sc) HIPCHK(add_selfcond(c, sc, B, L, off, m->cfg.d_model, m->stream));
   return run_part(m, 0, m->cfg.n_shared, c, B, L, pos0, ctx);
 }
 
@@ -719,7 +734,14 @@ static tadm_status check_args(const tadm_step_args* a, int Lc) {
   if (a->T < 1 || a->i < 1 || a->i > a->T) return fail(TADM_ERR_INVALID, "step i=%d T=%d", a->i, a->T);
   if (a->n_unmask < 0) return fail(TADM_ERR_INVALID, "negative n_unmask");
   if (!(a->inv_temp > 0) || !std::isfinite(a->inv_temp)) return fail(TADM_ERR_INVALID, "inv_temp must be finite and > 0");
-  if (a->mode != TADM_STEP_RANKED && a->mode != TADM_STEP_REMASK) return fail(TADM_ERR_INVALID, "step mode %d", a->mode);
+  if (a->mode != TADM_STEP_RANKED && a->mode != TADM_STEP_REMASK && a->mode != TADM_STEP_ENTROPY)
+    return fail(TADM_ERR_INVALID, "step mode %d", a->mode);
+  if (a->mode == TADM_STEP_ENTROPY) {
+    if (!(a->entropy_eta >= 0.f) || !std::isfinite(a->entropy_eta))
+      return fail(TADM_ERR_INVALID, "entropy bound must be finite and >= 0");
+    if (a->top_p > 0.f && a->top_p < 1.f) return fail(TADM_ERR_UNSUPPORTED, "the entropy-bound sampler has no nucleus");
+    if (Lc > ENTROPY_MAX_CANVAS) return fail(TADM_ERR_UNSUPPORTED, "entropy sampler canvas %d > %d", Lc, ENTROPY_MAX_CANVAS);
+  }
   if (a->mode == TADM_STEP_REMASK && !(a->p_unmask >= 0.f && a->p_unmask <= 1.f && a->sigma >= 0.f && a->sigma <= 1.f))
     return fail(TADM_ERR_INVALID, "remasking probabilities must lie in [0, 1]");
   if (!(a->top_p >= 0.f && a->top_p <= 1.f)) return fail(TADM_ERR_INVALID, "top_p outside [0, 1]");
@@ -850,6 +872,7 @@ tadm_status tadm_model_load_weight(tadm_model* m, int32_t index, const void* src
   if (staging) (void)hipFree(staging);
   if (e != hipSuccess) return fail(TADM_ERR_DEVICE, "weight placement: %s", hipGetErrorString(e));
   m->loaded[index] = 1;
+  if (sp.target == m->lay.embed) m->embT_valid = false;
   return TADM_OK;
 }
 
@@ -860,6 +883,9 @@ tadm_status tadm_model_destroy(tadm_model* m) {
   if (m->gcache) tadm_cache_destroy(m->gcache);
   if (m->gctx) tadm_context_destroy(m->gctx);
   if (m->gwin) (void)hipFree(m->gwin);
+  if (m->embT) (void)hipFree(m->embT);
+  if (m->ws.pw) (void)hipFree(m->ws.pw);
+  if (m->ws.sc) (void)hipFree(m->ws.sc);
   for (void* p : m->ws.allocs) (void)hipFree(p);
   if (m->ws.logits) (void)hipFree(m->ws.logits);
   if (m->arena) (void)hipFree(m->arena);
@@ -1028,9 +1054,9 @@ tadm_status tadm_context_append(tadm_model* m, tadm_context* ctx, const int32_t*
 
 // ------------------------------------------------------------------ step ----
 static tadm_status anchor_impl(tadm_model* m, const tadm_context* ctx, const int32_t* canvas, int B,
-                               int L, int i, tadm_cache* cache) {
+                               int L, int i, tadm_cache* cache, const float* sc = nullptr, int off = 0) {
   TRY(prof_begin(m, TADM_STAGE_EMBED));
-  TRY(shared_net(m, ctx, canvas, B, L, m->ws.c));
+  TRY(shared_net(m, ctx, canvas, B, L, m->ws.c, sc, off));
   TRY(prof_end(m, TADM_STAGE_EMBED));
   TRY(prof_begin(m, TADM_STAGE_ANCHOR));
   TRY(anchor_net(m, ctx, B, L, m->ws.c, cache));
@@ -1051,6 +1077,20 @@ tadm_status tadm_anchor_forward(tadm_model* m, const tadm_context* ctx, const in
   return anchor_impl(m, ctx, canvas_dev, B, L, i, cache);
 }
 
+tadm_status tadm_anchor_forward_sc(tadm_model* m, const tadm_context* ctx, const int32_t* canvas_dev, int32_t B,
+                                   int32_t L, int32_t i, int32_t T, const float* sc_dev, int32_t canvas_off,
+                                   tadm_cache* cache) {
+  TRY(check_model(m));
+  if (!canvas_dev || !cache) return fail(TADM_ERR_INVALID, "null argument");
+  TRY(check_window(m, ctx, B, L));
+  if (T < 1 || i < 1 || i > T) return fail(TADM_ERR_INVALID, "step i=%d T=%d", i, T);
+  if (canvas_off < 0 || canvas_off >= L) return fail(TADM_ERR_INVALID, "canvas_off=%d with L=%d", canvas_off, L);
+  if (cache->model != m || cache->B != B || cache->L != L)
+    return fail(TADM_ERR_STATE, "cache built for another model or shape");
+  TRY(ensure_workspace(m));
+  return anchor_impl(m, ctx, canvas_dev, B, L, i, cache, sc_dev, canvas_off);
+}
+
 static tadm_status sample_impl(tadm_model* m, const float* logits, const int32_t* row_map,
                                const int32_t* canvas, int B, int L, int off, int pos0,
                                const tadm_step_args* a, int32_t* next, int32_t* choice, float* conf) {
@@ -1066,6 +1106,58 @@ static tadm_status sample_impl(tadm_model* m, const float* logits, const int32_t
   return canvas_update(m, canvas, choice, conf, B, L, off, pos0, a, next);
 }
 
+// Embedding rows [0, V) transposed to [d, round64(V)] (zero padding): the weight operand
+// of the self-conditioning product.  Rebuilt after the embedding is reloaded.
+static tadm_status ensure_embT(tadm_model* m) {
+  if (m->embT_valid) return TADM_OK;
+  const int V = m->cfg.vocab, Vp = round64(V), d = m->cfg.d_model;
+  if (!m->embT) HIPCHK(hipMalloc(&m->embT, (size_t)d * Vp * m->esz));
+  HIPCHK(transpose_rows(m->dt, m->W(m->lay.embed), V, d, m->embT, Vp, m->stream));
+  m->embT_valid = true;
+  return TADM_OK;
+}
+
+// Entropy-bound step (TADM_STEP_ENTROPY) from logits of every canvas row: per-row
+// statistics and draws, acceptance and the next canvas, then (sc_out) the
+// self-conditioning product s = diag(2^40 / A) e E on the MFMA GEMM.
+static tadm_status entropy_impl(tadm_model* m, const float* logits, const int32_t* canvas, int B, int L, int off,
+                                int pos0, const tadm_step_args* a, int32_t* next, int32_t* choice, float* conf) {
+  Workspace& s = m->ws;
+  const int Lc = L - off, V = m->cfg.vocab, Vp = round64(V), d = m->cfg.d_model, rows = B * Lc;
+  void* P = nullptr;
+  if (a->sc_out) {
+    const size_t need = (size_t)rows * Vp * m->esz;
+    if (s.pw_cap < need) {
+      if (s.pw) HIPCHK(hipFree(s.pw));
+      s.pw = nullptr;
+      HIPCHK(hipMalloc(&s.pw, need));
+      s.pw_cap = need;
+    }
+    P = s.pw;
+    TRY(ensure_embT(m));
+  }
+  TRY(prof_begin(m, TADM_STAGE_SAMPLE));
+  HIPCHK(entropy_stats(logits, B, Lc, V, pos0 + off, a->step_id, a->seed, a->inv_temp, s.xhat, choice, conf, s.hq,
+                       s.rscale, m->dt, P, Vp, m->stream));
+  TRY(prof_end(m, TADM_STAGE_SAMPLE));
+  TRY(prof_begin(m, TADM_STAGE_SELECT));
+  const long long etaq = (long long)std::nearbyint((double)a->entropy_eta * 1099511627776.0);
+  HIPCHK(entropy_accept(s.hq, s.xhat, choice, canvas, next, B, L, off, pos0 + off, a->step_id, a->seed, V, etaq,
+                        a->i == 1 ? 1 : 0, m->stream));
+  TRY(prof_end(m, TADM_STAGE_SELECT));
+  if (a->sc_out) {
+    TRY(prof_begin(m, TADM_STAGE_SELFCOND));
+    GemmProblem p{rows, d, Vp, P, Vp, Vp, nullptr, 0, m->embT, Vp};
+    EpiParams e;
+    e.out = a->sc_out;
+    e.ldo = d;
+    e.row1 = s.rscale;
+    HIPCHK(gemm(m->dt, p, EPI_SCALE_F32, e, m->stream));
+    TRY(prof_end(m, TADM_STAGE_SELFCOND));
+  }
+  return TADM_OK;
+}
+
 // One reverse step.  With caller logits every canvas row goes through the head;
 // otherwise only the masked positions do (carry-over makes the others' logits
 // unused), at most max_masked of them (an exact bound the caller guarantees, or B*Lc).
@@ -1075,18 +1167,19 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
   const tadm_config& cf = m->cfg;
   Workspace& s = m->ws;
   const int pos0 = ctx ? ctx->len : 0, Lc = L - off, d = cf.d_model;
+  const bool entropy = a->mode == TADM_STEP_ENTROPY;
   TRY(prof_begin(m, TADM_STAGE_EMBED));
-  TRY(shared_net(m, ctx, canvas, B, L, s.c));
+  TRY(shared_net(m, ctx, canvas, B, L, s.c, entropy ? a->sc_in : nullptr, off));
   TRY(prof_end(m, TADM_STAGE_EMBED));
   TRY(prof_begin(m, TADM_STAGE_FUSION));
   TRY(fusion(m, B, L, s.c, cache));
   TRY(prof_end(m, TADM_STAGE_FUSION));
   if (m->taps) HIPCHK(copy_f32(s.x, s.ht, (size_t)B * L * d, m->stream));
-  const bool full = logits != nullptr;
-  const int rows = full ? B * Lc : std::min(max_masked, B * Lc);
+  const bool full = logits != nullptr, all_rows = full || entropy;
+  const int rows = all_rows ? B * Lc : std::min(max_masked, B * Lc);
   TRY(prof_begin(m, TADM_STAGE_DENOISE));
   TRY(run_part(m, cf.n_shared + cf.n_anchor, cf.n_denoise, s.x, B, L, pos0, ctx));
-  if (full) {
+  if (all_rows) {
     HIPCHK(rms_norm(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, B * Lc, d, Lc, L, off, s.xn, m->stream));
   } else {
     HIPCHK(compact_masked(canvas, B, L, off, cf.vocab, s.cidx, s.row_map, s.count, m->stream));
@@ -1097,10 +1190,11 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
   m->tap_B = B;
   m->tap_L = L;
   m->tap_Lc = Lc;
-  m->tap_final = full;
+  m->tap_final = all_rows;
   // bf16 masked-only head: the sampler runs in the projection's epilogue and only
   // per-(row, 64-entry group) partials reach memory
-  const bool fused = !full && m->dt == BF16 && !(a->top_p > 0.f && a->top_p < 1.f);  // nucleus needs whole rows
+  // (the nucleus and the entropy-bound sampler need whole rows)
+  const bool fused = !all_rows && m->dt == BF16 && !(a->top_p > 0.f && a->top_p < 1.f);
   const int ng = (cf.vocab + 63) / 64;
   if (!full) {
     TRY(ensure_logits(m, fused ? (size_t)B * Lc * ng * (sizeof(SamplePart) / 4) : (size_t)B * Lc * cf.vocab));
@@ -1109,7 +1203,7 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
   TRY(prof_begin(m, TADM_STAGE_HEAD));
   {
     GemmProblem p{rows, cf.vocab, d, s.xn, d, d, nullptr, 0, m->W(m->lay.w_out), d};
-    if (!full) p.M_dev = s.count;
+    if (!all_rows) p.M_dev = s.count;
     EpiParams e;
     if (fused) {
       e.rows_idx = s.cidx;
@@ -1129,6 +1223,7 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
     }
   }
   TRY(prof_end(m, TADM_STAGE_HEAD));
+  if (entropy) return entropy_impl(m, logits, canvas, B, L, off, pos0, a, next, s.choice, s.conf);
   if (!fused)
     return sample_impl(m, logits, full ? nullptr : s.row_map, canvas, B, L, off, pos0, a, next, s.choice,
                        s.conf);
@@ -1165,6 +1260,9 @@ tadm_status tadm_sample(tadm_model* m, const float* logits_dev, const int32_t* c
     return fail(TADM_ERR_INVALID, "sample shape B=%d L=%d off=%d", B, L, canvas_off);
   TRY(check_args(args, L - canvas_off));
   TRY(ensure_workspace(m));
+  if (args->mode == TADM_STEP_ENTROPY)
+    return entropy_impl(m, logits_dev, canvas_dev, B, L, canvas_off, pos0, args, next_canvas_dev,
+                        choice_dev ? choice_dev : m->ws.choice, conf_dev ? conf_dev : m->ws.conf);
   return sample_impl(m, logits_dev, nullptr, canvas_dev, B, L, canvas_off, pos0, args, next_canvas_dev,
                      choice_dev ? choice_dev : m->ws.choice, conf_dev ? conf_dev : m->ws.conf);
 }
@@ -1203,6 +1301,12 @@ void tadm_loop_probs(int32_t i, int32_t T, float eta, double t_on, double t_off,
   if (p_unmask) *p_unmask = (float)((a_s - (1.0 - sg) * a_t) / (1.0 - a_t));
 }
 
+float tadm_entropy_inv_temp(int32_t n, int32_t T, float tau_max, float tau_min) {
+#pragma clang fp contract(off)
+  const double hi = tau_max, lo = tau_min;
+  return (float)(1.0 / (lo + (hi - lo) * n / T));
+}
+
 tadm_status tadm_generate(tadm_model* m, const int32_t* prompt_dev, int32_t B, int32_t P, int32_t gen_len,
                           int32_t T, int32_t K, int32_t block_len, uint64_t seed, float temperature,
                           int32_t* tokens_dev) {
@@ -1215,8 +1319,15 @@ tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int3
                                   const tadm_sampler* sampler, int32_t* tokens_dev) {
   const bool loop = sampler && sampler->kind == TADM_SAMPLER_LOOP;
   const bool remask = loop || (sampler && sampler->kind == TADM_STEP_REMASK);
-  if (sampler && sampler->kind != TADM_STEP_RANKED && !remask)
+  const bool entropy = sampler && sampler->kind == TADM_SAMPLER_ENTROPY;
+  if (sampler && sampler->kind != TADM_STEP_RANKED && !remask && !entropy)
     return fail(TADM_ERR_INVALID, "sampler kind %d", sampler->kind);
+  if (entropy && !(sampler->eta >= 0.f && std::isfinite(sampler->eta)))
+    return fail(TADM_ERR_INVALID, "entropy bound must be finite and >= 0");
+  if (entropy && !(sampler->tau_min > 0.f && sampler->tau_min <= sampler->tau_max && std::isfinite(sampler->tau_max)))
+    return fail(TADM_ERR_INVALID, "temperatures need 0 < tau_min <= tau_max");
+  if (entropy && sampler->top_p > 0.f && sampler->top_p < 1.f)
+    return fail(TADM_ERR_UNSUPPORTED, "the entropy-bound sampler has no nucleus");
   if (remask && !(sampler->eta >= 0.f && sampler->eta <= 1.f)) return fail(TADM_ERR_INVALID, "eta outside [0, 1]");
   if (loop && !(0.0 < sampler->t_off && sampler->t_off < sampler->t_on && sampler->t_on < 1.0 &&
                 0.0 < sampler->alpha_on && sampler->alpha_on < 1.0))
@@ -1233,15 +1344,19 @@ tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int3
   const bool single = block_len == gen_len;
   if (!single && P < 1) return fail(TADM_ERR_INVALID, "block mode needs a prompt");
   if (m->cfg.vocab % 4) return fail(TADM_ERR_UNSUPPORTED, "the vocabulary head needs vocab %% 4 == 0");
+  if (entropy && block_len > ENTROPY_MAX_CANVAS)
+    return fail(TADM_ERR_UNSUPPORTED, "entropy sampler canvas %d > %d", block_len, ENTROPY_MAX_CANVAS);
   TRY(ensure_workspace(m));
   if (!m->gcache) TRY(cache_alloc(m, m->cfg.max_batch, m->cfg.max_seq, &m->gcache));
+  if (entropy && !m->ws.sc) HIPCHK(hipMalloc((void**)&m->ws.sc, (size_t)m->ws.n_tok * m->cfg.d_model * 4));
   const int L = P + gen_len, mask = m->cfg.vocab;
   tadm_step_args a{};
   a.T = T;
   a.seed = seed;
   a.inv_temp = (float)(1.0 / (double)temperature);
-  a.mode = remask ? TADM_STEP_REMASK : TADM_STEP_RANKED;
+  a.mode = entropy ? TADM_STEP_ENTROPY : remask ? TADM_STEP_REMASK : TADM_STEP_RANKED;
   a.top_p = sampler ? sampler->top_p : 0.f;
+  if (entropy) a.entropy_eta = sampler->eta;
   // masked positions entering step i: exactly B floor(M0 i / T) for the ranked sampler;
   // any number up to B M0 under remasking
   auto masked_bound = [&](int M0, int i) { return remask ? B * M0 : (int)(B * (((int64_t)M0 * i) / T)); };
@@ -1252,16 +1367,22 @@ tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int3
       tadm_loop_probs(i, T, sampler->eta, sampler->t_on, sampler->t_off, sampler->alpha_on, &a.sigma, &a.p_unmask);
     else if (remask)
       tadm_remask_probs(i, T, sampler->eta, &a.sigma, &a.p_unmask);
+    if (entropy) {  // each step reads the previous step's signal and, unless last, writes the next
+      a.inv_temp = tadm_entropy_inv_temp(i, T, sampler->tau_max, sampler->tau_min);
+      a.sc_in = i == T ? nullptr : m->ws.sc;
+      a.sc_out = i > 1 ? m->ws.sc : nullptr;
+    }
   };
   HIPCHK(init_canvas(prompt_dev, B, P, gen_len, mask, tokens_dev, m->stream));
   tadm_cache* cache = m->gcache;
   if (single) {
     cache->B = B;
     cache->L = L;
+    if (entropy) HIPCHK(init_uniform_tokens(tokens_dev, L, P, B, gen_len, P, 0, seed, m->cfg.vocab, m->stream));
     for (int i = T; i >= 1; --i) {
       set_step(gen_len, i);
       a.step_id = (uint32_t)(T - i);
-      if ((T - i) % K == 0) TRY(anchor_impl(m, nullptr, tokens_dev, B, L, i, cache));
+      if ((T - i) % K == 0) TRY(anchor_impl(m, nullptr, tokens_dev, B, L, i, cache, a.sc_in, P));
       TRY(denoise_impl(m, nullptr, tokens_dev, B, L, P, cache, &a, nullptr, tokens_dev, masked_bound(gen_len, i)));
     }
     return TADM_OK;
@@ -1280,11 +1401,15 @@ tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int3
   TRY(prof_end(m, TADM_STAGE_CONTEXT));
   const int nblocks = gen_len / block_len;
   for (int j = 0; j < nblocks; ++j) {
-    HIPCHK(fill_i32(win, (size_t)B * block_len, mask, m->stream));
+    if (entropy)
+      HIPCHK(init_uniform_tokens(win, block_len, 0, B, block_len, P + j * block_len, (uint32_t)j, seed,
+                                 m->cfg.vocab, m->stream));
+    else
+      HIPCHK(fill_i32(win, (size_t)B * block_len, mask, m->stream));
     for (int i = T; i >= 1; --i) {
       set_step(block_len, i);
       a.step_id = (uint32_t)(j * T + (T - i));
-      if ((T - i) % K == 0) TRY(anchor_impl(m, ctx, win, B, block_len, i, cache));
+      if ((T - i) % K == 0) TRY(anchor_impl(m, ctx, win, B, block_len, i, cache, a.sc_in, 0));
       TRY(denoise_impl(m, ctx, win, B, block_len, 0, cache, &a, nullptr, win, masked_bound(block_len, i)));
     }
     HIPCHK(hipMemcpy2DAsync(tokens_dev + P + j * block_len, (size_t)L * 4, win, (size_t)block_len * 4,

@@ -98,6 +98,22 @@ def test_loop_probs_match_the_oracle():
                 assert np.float32(sg) == rs and np.float32(pu) == rp, (i, T, params)
 
 
+def test_entropy_inv_temp_matches_the_oracle():
+    from oracle import usdm
+    for T in (1, 7, 48, 100):
+        for hi, lo in ((0.8, 0.4), (1.0, 1.0), (2.5, 0.1)):
+            for n in range(1, T + 1):
+                assert np.float32(tadm.tadm_entropy_inv_temp(n, T, hi, lo)) == usdm.inv_temperature(n, T, hi, lo)
+
+
+def test_entropy_sampler_rejects_bad_settings():
+    for bad in (dict(eta=-0.1), dict(tau_min=0.0), dict(tau_max=0.3, tau_min=0.4), dict(eta=float("inf"))):
+        smp = tadm.entropy_sampler(**bad)
+        st = tadm.lib.tadm_generate_sampler(None, None, 1, 0, 8, 4, 1, 8, 0, 1.0, C.byref(smp), None)
+        assert st != 0
+        assert re.search(rb"entropy bound|temperatures", tadm.lib.tadm_last_error()), bad
+
+
 def test_loop_sampler_rejects_bad_schedules():
     cfg = synth.get_config("tiny")
     for bad in (dict(t_on=0.05, t_off=0.55), dict(t_on=1.0), dict(t_off=0.0), dict(alpha_on=1.0), dict(eta=1.5)):
