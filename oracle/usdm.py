@@ -10,7 +10,8 @@ One reverse step n (T .. 1) of one canvas row, given the decoder logits L [Lc, V
 * x_tilde ~ Cat(softmax(l')): the Gumbel-max draw of the masked sampler's contract
   (Philox counter (v/4, position, row, step id)), no nucleus;
 * entropy of softmax(l'), with m = max l', y_v = l'_v - m, e_v = exp32(y_v):
-  A = sum_v rint(e_v 2^40), B = sum_v rint((-y_v * e_v) 2^40) (int64, order-free),
+  A = sum_v rint(e_v 2^40), B = sum_v rint((-y_v * e_v) 2^40) over e_v > 0 (int64,
+  order-free),
   H = log32(float(A) 2^-40) + float(B) / float(A) (float32 operations; H = log Z +
   sum_v p_v (-y_v) is the entropy with Z = sum_v e_v), Hq = rint(H 2^40) (int64);
 * acceptance: positions ordered by (Hq ascending, position ascending); with C_m the
@@ -51,7 +52,9 @@ def entropy_stats(logits_row, inv_temp):
     y = (lp - m).astype(F32)
     e = smp.exp32(y)
     A = int(np.rint(e * TWO40).astype(np.int64).sum())
-    Bs = int(np.rint((-y * e).astype(F32) * TWO40).astype(np.int64).sum())
+    with np.errstate(invalid="ignore"):
+        terms = np.where(e > 0, np.rint((-y * e).astype(F32) * TWO40), 0.0)   # p log p -> 0 as p -> 0
+    Bs = int(terms.astype(np.int64).sum())
     fA, fB = np.array([A, Bs], dtype=np.int64).astype(F32)      # int64 -> float32, one rounding
     H = F32(smp.log32(np.array([fA * F32(2.0 ** -40)], F32))[0] + F32(fB / fA))
     Hq = int(np.rint(np.float64(H) * 2.0 ** 40))
