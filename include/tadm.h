@@ -272,7 +272,8 @@ tadm_status tadm_debug_read(tadm_model* m, int32_t tap, float* dst_dev, size_t b
 
 /* Per-stage timing on the model stream for each stage whose bit is set in stage_mask
  * (bit s = stage s; 0 = off, -1 = all).  Stages nest.  A single-kernel stage (HEAD,
- * SAMPLE and QKV..FUSION2; with fp32 weights FFN_UP times its GEMM only) hands a pair of
+ * SAMPLE and QKV..FUSION2; with fp32 weights FFN_UP times its GEMM only, with a nucleus
+ * SAMPLE times the draw and not the threshold kernel) hands a pair of
  * events to its kernel launch (hipExtLaunchKernel), which stamps the kernel's own start
  * and end and adds nothing to the stream; the other stages record events before and
  * after their launches.  read synchronises the stream and sums the intervals recorded
@@ -285,7 +286,9 @@ enum {
    * feed-forward up (gate+up) and down projections, fusion GEMM 1 and 2 */
   TADM_STAGE_QKV = 8, TADM_STAGE_ATTN = 9, TADM_STAGE_OPROJ = 10, TADM_STAGE_FFN_UP = 11,
   TADM_STAGE_FFN_DOWN = 12, TADM_STAGE_FUSION1 = 13, TADM_STAGE_FUSION2 = 14,
-  /* the self-conditioning product s = pE of the entropy-bound sampler */
+  /* the self-conditioning product s = pE of the entropy-bound sampler (its K-split
+   * GEMM and ordered reduction); in that sampler SAMPLE is the statistics kernel and
+   * SELECT the acceptance */
   TADM_STAGE_SELFCOND = 15,
   TADM_STAGE_COUNT = 16
 };

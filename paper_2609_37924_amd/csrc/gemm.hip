@@ -263,10 +263,67 @@ hipError_t dispatch(DType dt, const GemmProblem& p, const EpiParams& e, hipStrea
   return launch_bf16<64, 64, 2, 2, 2, 3, K>(p, e, s);
 }
 
+// out[m, n] = row1[m] * sum_s part[s, m, n], s ascending (float4 granules, N % 4 == 0)
+__global__ void splitk_reduce_kernel(const float* part, int S, int M, int N, const float* row1, float* out, int ldo) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x, n4 = N / 4;
+  if (i >= (long)M * n4) return;
+  const int m = (int)(i / n4), n = (int)(i % n4) * 4;
+  const size_t MN = (size_t)M * N;
+  float4 acc = *reinterpret_cast<const float4*>(part + (size_t)m * N + n);
+  for (int k = 1; k < S; ++k) {
+    const float4 v = *reinterpret_cast<const float4*>(part + k * MN + (size_t)m * N + n);
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  const float r = row1[m];
+  store4(out + (size_t)m * ldo + n, r * acc.x, r * acc.y, r * acc.z, r * acc.w);
+}
+
+// Row-scaled product with a long K and few output tiles (the self-conditioning product:
+// K = vocabulary, N = d_model): 128 x 128 tiles split over K so that the grid fills the
+// chip, the slices' fp32 products go to part [S, M, N], then an ordered reduction.
+// Returns false when the split does not apply.
+// K slices: double while the grid has fewer than 512 blocks, each slice keeps >= 8 K
+// tiles and the tiles divide evenly (at most 16)
+int split_slices(int M, int N, int K) {
+  const long tiles = (long)((M + 127) / 128) * ((N + 127) / 128);
+  const int nk = K / 64;
+  int S = 1;
+  while (S < 16 && tiles * S < 512 && nk % (2 * S) == 0 && nk / (2 * S) >= 8) S *= 2;
+  return S;
+}
+
+bool splitk_scale(const GemmProblem& p, const EpiParams& e, hipStream_t s, hipError_t* err) {
+  if (!e.part || p.M_dev || p.N % 4 || p.K1 != p.K) return false;
+  const int S = split_slices(p.M, p.N, p.K);
+  if (S == 1) return false;
+  GemmProblem q = p;
+  q.ksplit = S;
+  EpiParams f;
+  f.out = e.part;
+  f.ldo = p.N;
+  f.split_stride = (size_t)p.M * p.N;
+  *err = launch_bf16<128, 128, 2, 2, 2, 2, EPI_STORE_F32>(q, f, s);
+  if (*err != hipSuccess) return true;
+  const long total = (long)p.M * (p.N / 4);
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                     static_cast<const float*>(e.part), S, p.M, p.N, e.row1, static_cast<float*>(e.out), e.ldo);
+  *err = hipGetLastError();
+  return true;
+}
+
 }  // namespace
+
+int gemm_split_slices(int M, int N, int K) { return split_slices(M, N, K); }
 
 hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
+  if (kind == EPI_SCALE_F32 && dt == BF16) {
+    hipError_t err = hipSuccess;
+    if (splitk_scale(p, e, s, &err)) return err;
+  }
   switch (kind) {
     case EPI_STORE: return dispatch<EPI_STORE>(dt, p, e, s);
     case EPI_STORE_F32: return dispatch<EPI_STORE_F32>(dt, p, e, s);

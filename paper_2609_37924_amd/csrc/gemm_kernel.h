@@ -96,8 +96,9 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
   // this lane's source row inside an 8-row group and its swizzled chunk
   const int lrow = lane >> 3, lchunk = (lane & 7) ^ (lane >> 3);
 
+  const int nk = p.K / 64 / p.ksplit, kt_base = blockIdx.y * nk;  // this block's K slice
   auto issue = [&](int kt, int buf) {
-    const int k0 = kt * 64;
+    const int k0 = (kt_base + kt) * 64;
     const bf16* Ab = A1;
     int lda = p.lda1, kk = k0;
     if (k0 >= p.K1) { Ab = A2; lda = p.lda2; kk = k0 - p.K1; }
@@ -140,7 +141,6 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
       }
   }
 
-  const int nk = p.K / 64;
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nk) issue(s, s);
@@ -175,6 +175,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
 
   // lane holds C[n = nb + 4*(lane>>4) + j][m = mb + (lane & 15)]
   const int mw = m0 + wm * WTM + fr;
+  if constexpr (KIND == EPI_STORE_F32)
+    if (p.ksplit > 1) ep.out = static_cast<float*>(ep.out) + (size_t)blockIdx.y * ep.split_stride;
   if constexpr (TileEpi<E>::value) {  // the epilogue takes the wave's whole tile
     E::template tile<TN, TM>(ep, p, acc, m0 + wm * WTM, n0 + wn * WTN, lane);
   } else if constexpr (E::kGlu) {
@@ -225,8 +227,8 @@ hipError_t launch_bf16(const GemmProblem& p0, const EpiParams& e, hipStream_t s)
   GemmProblem p = p0;
   const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
   xcd_regions(tiles_m, tiles_n, BM, BN, p.rm, p.rn);
-  launch_timed(gemm_bf16_kernel<BM, BN, ST, WGM, WGN, MINB, K>, dim3(tiles_m * tiles_n), dim3(64 * WGM * WGN),
-               0, s, p, e);
+  launch_timed(gemm_bf16_kernel<BM, BN, ST, WGM, WGN, MINB, K>, dim3(tiles_m * tiles_n, p.ksplit),
+               dim3(64 * WGM * WGN), 0, s, p, e);
   return hipGetLastError();
 }
 

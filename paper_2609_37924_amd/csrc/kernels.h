@@ -37,6 +37,7 @@ struct GemmProblem {
   const void* W;  int ldw;
   const int* M_dev = nullptr;  // if set: rows actually present (<= M; M sizes the grid)
   int rm = 0, rn = 0;          // per-XCD tile region (set by the launcher)
+  int ksplit = 1;              // K slices (grid.y); slice s writes out + s * split_stride
 };
 
 enum EpiKind {
@@ -57,7 +58,8 @@ enum EpiKind {
                       // weight rows) and scatter into the attention layouts (see EpiParams)
   EPI_SAMPLE,         // vocabulary projection: sampling partials per (row, 64-column
                       // group) instead of logits (head_sample only; see EpiParams)
-  EPI_SCALE_F32,      // out(float)[m, n] = row1[m] * acc
+  EPI_SCALE_F32,      // out(float)[m, n] = row1[m] * acc; with part set and long K the
+                      // product is split over K into part [S, M, N] and reduced in order
 };
 
 struct EpiParams {
@@ -91,6 +93,7 @@ struct EpiParams {
   uint32_t step_id = 0, k0 = 0, k1 = 0;
   float inv_temp = 1.f;
   void* part = nullptr;
+  size_t split_stride = 0;  // elements between the K slices' outputs (EPI_STORE_F32, ksplit > 1)
 };
 
 // Sampling partial of one (row, 64-entry vocabulary group): the group maximum m_g of
@@ -103,6 +106,9 @@ struct SamplePart {
 };
 
 hipError_t gemm(DType dt, const GemmProblem& p, EpiKind epi, const EpiParams& e, hipStream_t s);
+// K slices the bf16 EPI_SCALE_F32 product uses (1: no split); its part buffer needs
+// slices * M * N floats.
+int gemm_split_slices(int M, int N, int K);
 
 // ---- norms / embedding / elementwise (norm.hip)
 // out[t, :] = embed[tok[t], :] as float32; `embed` has table_rows rows of length d

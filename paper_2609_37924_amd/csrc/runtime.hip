@@ -241,6 +241,8 @@ struct Workspace {
   float* rscale = nullptr;
   void* pw = nullptr;
   size_t pw_cap = 0;
+  float* kpart = nullptr;  // K-slice products of the self-conditioning GEMM (lazy)
+  size_t kpart_cap = 0;
   float* sc = nullptr;
   float* logits = nullptr;
   size_t logits_cap = 0;
@@ -321,7 +323,8 @@ static tadm_status prof_event(tadm_model* m, hipEvent_t* e) {
 // A single-kernel stage times its first launch with the launch's own timestamps;
 // the other stages bracket their launches with recorded events.
 static bool single_kernel_stage(int stage) {
-  return stage == TADM_STAGE_HEAD || stage == TADM_STAGE_SAMPLE || stage >= TADM_STAGE_QKV;
+  return stage == TADM_STAGE_HEAD || stage == TADM_STAGE_SAMPLE ||
+         (stage >= TADM_STAGE_QKV && stage != TADM_STAGE_SELFCOND);  // split product + reduction
 }
 
 // Stages nest (a kernel stage inside a layer stage); each end closes the latest begin.
@@ -885,6 +888,7 @@ tadm_status tadm_model_destroy(tadm_model* m) {
   if (m->gwin) (void)hipFree(m->gwin);
   if (m->embT) (void)hipFree(m->embT);
   if (m->ws.pw) (void)hipFree(m->ws.pw);
+  if (m->ws.kpart) (void)hipFree(m->ws.kpart);
   if (m->ws.sc) (void)hipFree(m->ws.sc);
   for (void* p : m->ws.allocs) (void)hipFree(p);
   if (m->ws.logits) (void)hipFree(m->ws.logits);
@@ -1152,6 +1156,17 @@ static tadm_status entropy_impl(tadm_model* m, const float* logits, const int32_
     e.out = a->sc_out;
     e.ldo = d;
     e.row1 = s.rscale;
+    const int S = m->dt == BF16 ? gemm_split_slices(rows, d, Vp) : 1;
+    if (S > 1) {
+      const size_t need = (size_t)S * rows * d;
+      if (s.kpart_cap < need) {
+        if (s.kpart) HIPCHK(hipFree(s.kpart));
+        s.kpart = nullptr;
+        HIPCHK(hipMalloc((void**)&s.kpart, need * 4));
+        s.kpart_cap = need;
+      }
+      e.part = s.kpart;
+    }
     HIPCHK(gemm(m->dt, p, EPI_SCALE_F32, e, m->stream));
     TRY(prof_end(m, TADM_STAGE_SELFCOND));
   }

@@ -80,20 +80,38 @@ __global__ __launch_bounds__(256) void entropy_kernel(const float* logits, int V
 
   long long A = 0, Bs = 0;
   Top2 top;
+  const bool vec = (V & 3) == 0;  // whole float4 granules (then ldp % 4 == 0 too)
   for (int q = tid; 4 * q < V; q += 256) {
+    float l[4];
+    if (vec) {
+      const float4 x = *reinterpret_cast<const float4*>(lg + 4 * q);
+      l[0] = x.x; l[1] = x.y; l[2] = x.z; l[3] = x.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) l[e] = 4 * q + e < V ? lg[4 * q + e] : 0.f;
+    }
     uint32_t c[4] = {(uint32_t)q, pos, (uint32_t)b, step_id};
     philox4x32_10(c, k0, k1);
+    float w[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int v = 4 * q + e;
-      if (v >= V) break;
-      const float lp = lg[v] * inv_temp;
+      w[e] = 0.f;
+      if (v >= V) continue;
+      const float lp = l[e] * inv_temp;
       const float y = lp - m;
       const float ex = own_exp(y);
+      w[e] = ex;
       A += (long long)rintf(ex * TWO40);
       if (ex > 0.f) Bs += (long long)rintf(((-y) * ex) * TWO40);
-      if (P) store_weight(P + (size_t)row * ldp + v, ex);
       top.add(screen_score(lp, uniform01(c[e])), v);
+    }
+    if (P) {
+      PT* dst = P + (size_t)row * ldp + 4 * q;
+      if (vec)
+        store4(dst, w[0], w[1], w[2], w[3]);
+      else
+        for (int e = 0; e < 4 && 4 * q + e < V; ++e) store_weight(dst + e, w[e]);
     }
   }
   if (P)
