@@ -15,10 +15,13 @@ computes, written from the paper:
   and ReMDM-Loop) and the uniform-state generation of Algorithm 2;
 * ``usdm``     -- the entropy-bound sampler of Algorithm 2: temperature schedule,
   Gumbel-max draw, fixed-point entropy, entropy-bound acceptance, uniform re-noising
-  and the self-conditioning signal.
+  and the self-conditioning signal;
+* ``train``    -- the pretraining objective (Theorem T-ANELBO with gamma = 0, sigma = 0):
+  training times with stale anchors, the corrupted pair (z_t, z_t') and the
+  1/t-weighted masked cross-entropy.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's ``cpu_baseline``
 leg may import this package.  It shares no code with the GPU path; the only common
 dependency is the seeded input module ``synth``.
 """
-from . import network, sampler, loop, usdm  # noqa: F401
+from . import network, sampler, loop, usdm, train  # noqa: F401
