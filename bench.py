@@ -484,6 +484,31 @@ def main():
                   file=sys.stderr, flush=True)
         T_run[0] = T
         sampler[0] = None
+    # the pretraining objective's forward pass (stale pair, anchor on z_t', denoiser on
+    # z_t, 1/t-weighted masked cross-entropy) over B sequences of P + G tokens
+    train_line = None
+    if not args.no_sweep:
+        Ltr = P + G
+        xtr = torch.randint(0, cfg["vocab"], (B, Ltr), generator=torch.Generator().manual_seed(5),
+                            dtype=torch.int32).to(dev)
+        tt, tts, _, _, _ = tadm.tadm_stale_times(B, 11, 0, 1e-3)
+        d_t, d_ts = torch.from_numpy(tt).to(dev), torch.from_numpy(tts).to(dev)
+        loss = torch.empty(B, device=dev)
+        for _ in range(2):
+            tadm.tadm_train_loss(m, xtr, B, Ltr, d_t, d_ts, 1e-3, 11, 0, loss)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = max(3, args.steps)
+        e0.record(stream)
+        for r in range(reps):
+            tadm.tadm_train_loss(m, xtr, B, Ltr, d_t, d_ts, 1e-3, 11, r, loss)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        tms = e0.elapsed_time(e1) / reps
+        train_line = {"tokens_per_s": B * Ltr / (tms / 1e3), "ms_per_batch": tms, "batch": B, "seq_len": Ltr,
+                      "what": "forward of the T-ANELBO objective (gamma = 0), no backward"}
+        print(f"[bench] training objective forward, {B}x{Ltr} tokens: {tms:.3f} ms -> "
+              f"{B * Ltr / (tms / 1e3):.1f} tokens/s", file=sys.stderr, flush=True)
     roof = None
     if dom:
         live = kernel_table(cfg, B, K0, dom_stages)[0]
@@ -511,6 +536,7 @@ def main():
                    "parallelism": "none (1 GPU)"},
         "k_sweep": sweep,
         "samplers": remask,
+        "train_forward": train_line,
         "stages_ms_per_step": {k: v["ms_per_step"] for k, v in stages.items()},
         "kernels": [{k: v for k, v in r.items() if k != "stages"} for r in kernels],
         "roofline": roof,

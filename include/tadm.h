@@ -256,6 +256,32 @@ tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int3
                                   int32_t gen_len, int32_t T, int32_t K, int32_t block_len, uint64_t seed,
                                   float temperature, const tadm_sampler* sampler, int32_t* tokens_dev);
 
+/* ------------------------------------------------------------- training ---- */
+/* Training objective of TADM:Pretraining (Sec. 5, Theorem T-ANELBO with gamma = 0 and
+ * sigma = 0; training details of App. C.2), forward pass.  Per row b of the clean tokens
+ * x_dev [B, L] (ids < vocab), with times t_dev[b] in (0, 1] and t_stale_dev[b] in
+ * [t_b, 1] (device float32 [B]):
+ *   z_t, z_t': position l is masked in z_t iff u < float((1 - eps) t_b), in z_t' iff
+ *     u < float((1 - eps) t'_b), u = (2 (w >> 9) + 1) 2^-24 with w Philox4x32-10 word 0
+ *     at counter (2^31 + 3, l, b, step) (the log-linear schedule alpha_t = 1 - (1-eps) t;
+ *     z_t' is z_t further corrupted, eq. fwd_t_t');
+ *   logits = head(D(Phi(S(z_t), (A(S(z_t')), S(z_t'))))) on the positions masked in z_t;
+ *   loss_dev[b] = (1 / t_b) sum over those positions of -log softmax(logits)[x] (the
+ *     continuous-time weight of lambda_t for this schedule).
+ * n_masked_dev [B], zt_dev / zs_dev [B, L] are optional outputs (NULL: not written).
+ * Positions [0, L) of one sequence, no context; B <= max_batch, L <= max_seq. */
+tadm_status tadm_train_loss(tadm_model* m, const int32_t* x_dev, int32_t B, int32_t L, const float* t_dev,
+                            const float* t_stale_dev, float eps, uint64_t seed, uint32_t step, float* loss_dev,
+                            int32_t* n_masked_dev, int32_t* zt_dev, int32_t* zs_dev);
+/* Pure host helper: the training times of a batch (App. C.2): with (w0, w1, w2, w3) =
+ * Philox4x32-10 at counter (2^31 + 4, b, step, 0) and u0 = (2 (w0 of row 0 >> 9) + 1) 2^-24,
+ * t_b = float(eps + (1 - eps) frac(u0 + b / B)) (antithetic), K_b = {1, 2, 4, 8}[w1 >> 30],
+ * T_b = {128, 256, 512, 1024, 2048, 4096}[(6 w2) >> 32], k_b = (K_b w3) >> 32 (the cache age),
+ * t'_b = float(min(1, t_b + k_b / T_b)); arithmetic in double.  Outputs are host arrays
+ * [B]; K, T, k may be NULL. */
+void tadm_stale_times(int32_t B, uint64_t seed, uint32_t step, float eps, float* t, float* t_stale, int32_t* K,
+                      int32_t* T, int32_t* k);
+
 /* -------------------------------------------------------- observability ---- */
 /* Copies (float32) a buffer of the last step into dst_dev:
  *   TADM_TAP_EMBED  c = S(z)          [B, L, d]

@@ -82,6 +82,8 @@ _SIGS = {
     "tadm_anchor_forward": (_I, [_P, _P, _P, _I, _I, _I, _I, _P]),
     "tadm_anchor_forward_sc": (_I, [_P, _P, _P, _I, _I, _I, _I, _P, _I, _P]),
     "tadm_entropy_inv_temp": (C.c_float, [_I, _I, C.c_float, C.c_float]),
+    "tadm_train_loss": (_I, [_P, _P, _I, _I, _P, _P, C.c_float, C.c_uint64, C.c_uint32, _P, _P, _P, _P]),
+    "tadm_stale_times": (None, [_I, C.c_uint64, C.c_uint32, C.c_float, _P, _P, _P, _P, _P]),
     "tadm_denoise_step": (_I, [_P, _P, _P, _I, _I, _I, _P, C.POINTER(tadm_step_args), _P, _P]),
     "tadm_sample": (_I, [_P, _P, _P, _I, _I, _I, _I, C.POINTER(tadm_step_args), _P, _P, _P]),
     "tadm_generate": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, C.c_uint64, C.c_float, _P]),
@@ -232,6 +234,22 @@ def tadm_anchor_forward_sc(m, ctx, canvas, B, L, i, T, sc, canvas_off, cache):
 
 def tadm_entropy_inv_temp(n, T, tau_max, tau_min):
     return lib.tadm_entropy_inv_temp(n, T, tau_max, tau_min)
+
+
+def tadm_train_loss(m, x, B, L, t, t_stale, eps, seed, step, loss, n_masked=None, zt=None, zs=None):
+    """Training objective forward pass (device tensors: x int32 [B, L], t / t_stale /
+    loss float32 [B], optional n_masked int32 [B], zt / zs int32 [B, L])."""
+    check(lib.tadm_train_loss(m, ptr(x), B, L, ptr(t), ptr(t_stale), eps, seed, step, ptr(loss), ptr(n_masked),
+                              ptr(zt), ptr(zs)))
+
+
+def tadm_stale_times(B, seed, step, eps):
+    """(t, t', K, T, k) of a training batch as numpy arrays, computed by the library."""
+    import numpy as np
+    t, ts = np.zeros(B, np.float32), np.zeros(B, np.float32)
+    K, T, k = (np.zeros(B, np.int32) for _ in range(3))
+    lib.tadm_stale_times(B, seed, step, eps, *(C.c_void_p(a.ctypes.data) for a in (t, ts, K, T, k)))
+    return t, ts, K, T, k
 
 
 def tadm_denoise_step(m, ctx, canvas, B, L, canvas_off, cache, args, logits, next_canvas):

@@ -15,9 +15,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 SOURCES = ["runtime.hip", "gemm.hip", "attention.hip", "norm.hip", "sampler.hip", "head_sample.hip", "fusion.hip",
-           "usdm.hip"]
+           "usdm.hip", "train.hip"]
 CONTRACT = ["-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt"]
-EXTRA = {"sampler.hip": CONTRACT, "head_sample.hip": CONTRACT, "usdm.hip": CONTRACT}
+EXTRA = {"sampler.hip": CONTRACT, "head_sample.hip": CONTRACT, "usdm.hip": CONTRACT, "train.hip": CONTRACT}
 OUT = os.path.join(PKG, "libtadm.so")
 
 

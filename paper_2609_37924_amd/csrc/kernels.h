@@ -202,6 +202,17 @@ hipError_t add_selfcond(float* c, const float* sc, int B, int L, int off, int d,
 // ET[n, v] = E[v, n] (v < V), zero for V <= v < ldt: E [V, d] row-major, ET [d, ldt].
 hipError_t transpose_rows(DType dt, const void* E, int V, int d, void* ET, int ldt, hipStream_t s);
 constexpr int ENTROPY_MAX_CANVAS = 8192;
+// Training objective (train.hip).  zt / zs [B, L] = the stale pair of clean tokens x:
+// masked iff u < float((1 - eps) t_b) (resp. t'_b), u from Philox word 0 at counter
+// (2^31 + 3, l, b, step).
+hipError_t corrupt_pair(const int32_t* x, int B, int L, const float* t, const float* ts, float eps, uint64_t seed,
+                        uint32_t step, int mask_id, int32_t* zt, int32_t* zs, hipStream_t s);
+// ce[r] = logsumexp(logits[r]) - logits[r][x[idx[r]]] for the rows r < *count (grid max_rows).
+hipError_t masked_ce(const float* logits, int V, int max_rows, const int* count, const int32_t* idx, const int32_t* x,
+                     float* ce, hipStream_t s);
+// loss[b] = (1 / t_b) sum_{l masked} ce[row_map[b L + l]] (row_map -1: not masked); n_masked nullable.
+hipError_t weighted_loss(const float* ce, const int32_t* row_map, int B, int L, const float* t, float* loss,
+                         int32_t* n_masked, hipStream_t s);
 // Largest vocabulary the sampler handles: its per-group partials (64 entries per
 // group, 12 bytes each) live in 48 KB of LDS.
 constexpr int SAMPLE_MAX_VOCAB = 4096 * 64;

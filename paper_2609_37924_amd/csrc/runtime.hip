@@ -243,6 +243,8 @@ struct Workspace {
   size_t pw_cap = 0;
   float* kpart = nullptr;  // K-slice products of the self-conditioning GEMM (lazy)
   size_t kpart_cap = 0;
+  int32_t *zt = nullptr, *zs = nullptr;  // training pair (lazy)
+  float* ce = nullptr;
   float* sc = nullptr;
   float* logits = nullptr;
   size_t logits_cap = 0;
@@ -276,6 +278,7 @@ struct tadm_model {
   // objects reused across calls so that a generation allocates nothing after warm-up
   tadm_cache* scratch = nullptr;   // anchor state of context appends (capacity max_batch x max_seq)
   tadm_cache* gcache = nullptr;    // anchor cache of tadm_generate
+  tadm_cache* tcache = nullptr;    // anchor cache of tadm_train_loss
   tadm_context* gctx = nullptr;    // context of block-mode tadm_generate
   int32_t* gwin = nullptr;         // active block of block-mode tadm_generate
   void* embT = nullptr;            // embedding rows [0, V) transposed, [d, round64(V)] (lazy)
@@ -884,6 +887,10 @@ tadm_status tadm_model_destroy(tadm_model* m) {
   (void)hipDeviceSynchronize();
   if (m->scratch) tadm_cache_destroy(m->scratch);
   if (m->gcache) tadm_cache_destroy(m->gcache);
+  if (m->tcache) tadm_cache_destroy(m->tcache);
+  if (m->ws.zt) (void)hipFree(m->ws.zt);
+  if (m->ws.zs) (void)hipFree(m->ws.zs);
+  if (m->ws.ce) (void)hipFree(m->ws.ce);
   if (m->gctx) tadm_context_destroy(m->gctx);
   if (m->gwin) (void)hipFree(m->gwin);
   if (m->embT) (void)hipFree(m->embT);
@@ -1438,6 +1445,107 @@ tadm_status tadm_generate_sampler(tadm_model* m, const int32_t* prompt_dev, int3
   return TADM_OK;
 }
 
+
+// ---------------------------------------------------------------- training ---
+namespace {
+// Philox4x32-10 on the host (the same rounds as the kernels' and the oracle's)
+void philox_host(uint32_t c[4], uint32_t k0, uint32_t k1) {
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c[0], p1 = (uint64_t)0xCD9E8D57u * c[2];
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c[1] ^ k0, n2 = (uint32_t)(p0 >> 32) ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = (uint32_t)p1;
+    c[2] = n2;
+    c[3] = (uint32_t)p0;
+  }
+}
+}  // namespace
+
+void tadm_stale_times(int32_t B, uint64_t seed, uint32_t step, float eps, float* t, float* t_stale, int32_t* K,
+                      int32_t* T, int32_t* k) {
+#pragma clang fp contract(off)
+  static const int Ks[4] = {1, 2, 4, 8}, Ts[6] = {128, 256, 512, 1024, 2048, 4096};
+  const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
+  double u0 = 0.0;
+  const double e = (double)eps;
+  for (int b = 0; b < B; ++b) {
+    uint32_t c[4] = {0x80000004u, (uint32_t)b, step, 0u};
+    philox_host(c, k0, k1);
+    if (b == 0) u0 = (double)((float)(2u * (c[0] >> 9) + 1u) * 5.9604644775390625e-08f);  // 2^-24
+    const double frac = std::fmod(u0 + (double)b / B, 1.0);
+    const float tb = (float)(e + (1.0 - e) * frac);
+    const int Kb = Ks[c[1] >> 30];
+    const int Tb = Ts[(int)(((uint64_t)c[2] * 6u) >> 32)];
+    const int kb = (int)(((uint64_t)c[3] * (uint32_t)Kb) >> 32);
+    if (t) t[b] = tb;
+    if (t_stale) t_stale[b] = (float)std::min(1.0, (double)tb + (double)kb / (double)Tb);
+    if (K) K[b] = Kb;
+    if (T) T[b] = Tb;
+    if (k) k[b] = kb;
+  }
+}
+
+tadm_status tadm_train_loss(tadm_model* m, const int32_t* x_dev, int32_t B, int32_t L, const float* t_dev,
+                            const float* t_stale_dev, float eps, uint64_t seed, uint32_t step, float* loss_dev,
+                            int32_t* n_masked_dev, int32_t* zt_dev, int32_t* zs_dev) {
+  TRY(check_model(m));
+  if (!x_dev || !t_dev || !t_stale_dev || !loss_dev) return fail(TADM_ERR_INVALID, "null argument");
+  if (B < 1 || B > m->cfg.max_batch || L < 1 || L > m->cfg.max_seq)
+    return fail(TADM_ERR_INVALID, "B=%d L=%d outside the model's capacity", B, L);
+  if (!(eps >= 0.f && eps < 1.f)) return fail(TADM_ERR_INVALID, "eps outside [0, 1)");
+  TRY(ensure_workspace(m));
+  const tadm_config& cf = m->cfg;
+  Workspace& s = m->ws;
+  const int N = B * L, d = cf.d_model, V = cf.vocab, mask = cf.vocab;
+  if (!s.zt) {
+    HIPCHK(hipMalloc((void**)&s.zt, (size_t)s.n_tok * 4));
+    HIPCHK(hipMalloc((void**)&s.zs, (size_t)s.n_tok * 4));
+    HIPCHK(hipMalloc((void**)&s.ce, (size_t)s.n_tok * 4));
+  }
+  if (!m->tcache) TRY(cache_alloc(m, cf.max_batch, cf.max_seq, &m->tcache));
+  tadm_cache* cache = m->tcache;
+  cache->B = B;
+  cache->L = L;
+  int32_t* zt = zt_dev ? zt_dev : s.zt;
+  int32_t* zs = zs_dev ? zs_dev : s.zs;
+  HIPCHK(corrupt_pair(x_dev, B, L, t_dev, t_stale_dev, eps, seed, step, mask, zt, zs, m->stream));
+  // stale anchor from z_t', current pass on z_t
+  TRY(anchor_impl(m, nullptr, zs, B, L, 1, cache));
+  TRY(prof_begin(m, TADM_STAGE_EMBED));
+  TRY(shared_net(m, nullptr, zt, B, L, s.c));
+  TRY(prof_end(m, TADM_STAGE_EMBED));
+  TRY(prof_begin(m, TADM_STAGE_FUSION));
+  TRY(fusion(m, B, L, s.c, cache));
+  TRY(prof_end(m, TADM_STAGE_FUSION));
+  TRY(prof_begin(m, TADM_STAGE_DENOISE));
+  TRY(run_part(m, cf.n_shared + cf.n_anchor, cf.n_denoise, s.x, B, L, 0, nullptr));
+  HIPCHK(compact_masked(zt, B, L, 0, mask, s.cidx, s.row_map, s.count, m->stream));
+  HIPCHK(rms_norm_gather(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, s.cidx, s.count, N, L, L, 0, d, s.xn,
+                         m->stream));
+  TRY(prof_end(m, TADM_STAGE_DENOISE));
+  TRY(ensure_logits(m, (size_t)N * V));
+  TRY(prof_begin(m, TADM_STAGE_HEAD));
+  {
+    GemmProblem p{N, V, d, s.xn, d, d, nullptr, 0, m->W(m->lay.w_out), d};
+    p.M_dev = s.count;
+    EpiParams e;
+    e.out = s.logits;
+    e.ldo = V;
+    HIPCHK(gemm(m->dt, p, EPI_STORE_F32, e, m->stream));
+  }
+  TRY(prof_end(m, TADM_STAGE_HEAD));
+  TRY(prof_begin(m, TADM_STAGE_SAMPLE));
+  HIPCHK(masked_ce(s.logits, V, N, s.count, s.cidx, x_dev, s.ce, m->stream));
+  TRY(prof_end(m, TADM_STAGE_SAMPLE));
+  TRY(prof_begin(m, TADM_STAGE_SELECT));
+  HIPCHK(weighted_loss(s.ce, s.row_map, B, L, t_dev, loss_dev, n_masked_dev, m->stream));
+  TRY(prof_end(m, TADM_STAGE_SELECT));
+  return TADM_OK;
+}
 
 // ---------------------------------------------------------- observability ---
 tadm_status tadm_debug_read(tadm_model* m, int32_t tap, float* dst_dev, size_t bytes) {

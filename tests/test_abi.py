@@ -106,6 +106,17 @@ def test_entropy_inv_temp_matches_the_oracle():
                 assert np.float32(tadm.tadm_entropy_inv_temp(n, T, hi, lo)) == usdm.inv_temperature(n, T, hi, lo)
 
 
+def test_stale_times_match_the_oracle():
+    """The library's training times (antithetic t, refresh interval, budget, cache age,
+    stale time) are the oracle's bit for bit."""
+    from oracle import train
+    for B, seed, step, eps in ((1, 0, 0, 1e-3), (16, 7, 3, 1e-3), (512, 2 ** 40 + 5, 99, 0.0), (37, 11, 1, 0.25)):
+        got = tadm.tadm_stale_times(B, seed, step, eps)
+        ref = train.stale_times(B, seed, step, eps)
+        for g, r, name in zip(got, ref, ("t", "t'", "K", "T", "k")):
+            assert np.array_equal(np.asarray(g), np.asarray(r).astype(np.asarray(g).dtype)), (name, B, seed)
+
+
 def test_entropy_sampler_rejects_bad_settings():
     for bad in (dict(eta=-0.1), dict(tau_min=0.0), dict(tau_max=0.3, tau_min=0.4), dict(eta=float("inf"))):
         smp = tadm.entropy_sampler(**bad)
