@@ -314,15 +314,67 @@ bool splitk_scale(const GemmProblem& p, const EpiParams& e, hipStream_t s, hipEr
   return true;
 }
 
+// resid[m, n] += sum_s part[s, m, n], s ascending (float4 granules, N % 4 == 0)
+__global__ void resid_reduce_kernel(const float* part, int S, int M, int N, float* resid, int ldr) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x, n4 = N / 4;
+  if (i >= (long)M * n4) return;
+  const int m = (int)(i / n4), n = (int)(i % n4) * 4;
+  const size_t MN = (size_t)M * N;
+  float4 acc = *reinterpret_cast<const float4*>(part + (size_t)m * N + n);
+  for (int k = 1; k < S; ++k) {
+    const float4 v = *reinterpret_cast<const float4*>(part + k * MN + (size_t)m * N + n);
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  float4* r = reinterpret_cast<float4*>(resid + (size_t)m * ldr + n);
+  float4 x = *r;
+  x.x += acc.x;
+  x.y += acc.y;
+  x.z += acc.z;
+  x.w += acc.w;
+  *r = x;
+}
+
+// K slices of a residual product with a long K and fewer than two 128 x 128 tiles per
+// CU: double while the grid has fewer than 512 blocks and each slice keeps >= 16 K tiles
+int resid_slices(int M, int N, int K) {
+  const long tiles = (long)((M + 127) / 128) * ((N + 127) / 128);
+  const int nk = K / 64;
+  if (tiles >= 512 || nk < 64 || N % 4) return 1;
+  int S = 1;
+  while (S < 8 && tiles * S < 512 && nk % (2 * S) == 0 && nk / (2 * S) >= 16) S *= 2;
+  return S;
+}
+
 }  // namespace
 
 int gemm_split_slices(int M, int N, int K) { return split_slices(M, N, K); }
+int gemm_resid_slices(int M, int N, int K) { return resid_slices(M, N, K); }
 
 hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
   if (kind == EPI_SCALE_F32 && dt == BF16) {
     hipError_t err = hipSuccess;
     if (splitk_scale(p, e, s, &err)) return err;
+  }
+  if (kind == EPI_RESID && dt == BF16 && e.part && !p.M_dev && p.K1 == p.K) {
+    const int S = resid_slices(p.M, p.N, p.K);
+    if (S > 1) {  // the slices' products to part [S, M, N], then an ordered sum into resid
+      GemmProblem q = p;
+      q.ksplit = S;
+      EpiParams f;
+      f.out = e.part;
+      f.ldo = p.N;
+      f.split_stride = (size_t)p.M * p.N;
+      hipError_t err = launch_bf16<128, 128, 2, 2, 2, 2, EPI_STORE_F32>(q, f, s);
+      if (err != hipSuccess) return err;
+      const long total = (long)p.M * (p.N / 4);
+      hipLaunchKernelGGL(resid_reduce_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                         static_cast<const float*>(e.part), S, p.M, p.N, e.resid, e.ldr);
+      return hipGetLastError();
+    }
   }
   switch (kind) {
     case EPI_STORE: return dispatch<EPI_STORE>(dt, p, e, s);

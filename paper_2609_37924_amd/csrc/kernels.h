@@ -43,7 +43,8 @@ struct GemmProblem {
 enum EpiKind {
   EPI_STORE = 0,      // out(T)[m, n] = acc
   EPI_STORE_F32,      // out(float)[m, n] = acc
-  EPI_RESID,          // resid(float)[m, n] += acc
+  EPI_RESID,          // resid(float)[m, n] += acc (bf16 with part set and a long K: split
+                      // over K into part [S, M, N], then an ordered sum into resid)
   EPI_GELU,           // out(T)[m, n] = gelu(acc)
   EPI_GLU_SILU,       // out(T)[m, f] = silu(gate) * up   (16-row interleaved weights)
   EPI_GLU_GELU,       // out(T)[m, f] = gelu(gate) * up
@@ -109,6 +110,9 @@ hipError_t gemm(DType dt, const GemmProblem& p, EpiKind epi, const EpiParams& e,
 // K slices the bf16 EPI_SCALE_F32 product uses (1: no split); its part buffer needs
 // slices * M * N floats.
 int gemm_split_slices(int M, int N, int K);
+// K slices of a bf16 EPI_RESID product given a part buffer (1: no split; else
+// part holds slices * M * N floats): long K with few 128 x 128 tiles.
+int gemm_resid_slices(int M, int N, int K);
 
 // ---- norms / embedding / elementwise (norm.hip)
 // out[t, :] = embed[tok[t], :] as float32; `embed` has table_rows rows of length d

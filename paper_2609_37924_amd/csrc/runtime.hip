@@ -241,7 +241,7 @@ struct Workspace {
   float* rscale = nullptr;
   void* pw = nullptr;
   size_t pw_cap = 0;
-  float* kpart = nullptr;  // K-slice products of the self-conditioning GEMM (lazy)
+  float* kpart = nullptr;  // K-slice products of split GEMMs (lazy)
   size_t kpart_cap = 0;
   int32_t *zt = nullptr, *zs = nullptr;  // training pair (lazy)
   float* ce = nullptr;
@@ -331,11 +331,13 @@ static bool single_kernel_stage(int stage) {
 }
 
 // Stages nest (a kernel stage inside a layer stage); each end closes the latest begin.
-static tadm_status prof_begin(tadm_model* m, int stage) {
+// multi: a single-kernel stage that this time launches more than one kernel (events
+// are recorded around its launches instead)
+static tadm_status prof_begin(tadm_model* m, int stage, bool multi = false) {
   if (!((m->prof_mask >> stage) & 1)) return TADM_OK;
   OpenStage o{stage, nullptr, nullptr};
   TRY(prof_event(m, &o.a));
-  if (single_kernel_stage(stage)) {
+  if (single_kernel_stage(stage) && !multi) {
     TRY(prof_event(m, &o.b));
     next_launch_events = LaunchEvents{o.a, o.b};
   } else {
@@ -426,6 +428,17 @@ static tadm_status ensure_logits(tadm_model* m, size_t n) {
   return TADM_OK;
 }
 
+// Workspace of K-slice products (grown on demand).
+static tadm_status ensure_kpart(tadm_model* m, size_t floats) {
+  Workspace& s = m->ws;
+  if (s.kpart_cap >= floats) return TADM_OK;
+  if (s.kpart) HIPCHK(hipFree(s.kpart));
+  s.kpart = nullptr;
+  HIPCHK(hipMalloc((void**)&s.kpart, floats * 4));
+  s.kpart_cap = floats;
+  return TADM_OK;
+}
+
 // --------------------------------------------------------------- the layers ---
 struct KVTarget {
   void *k, *vt;
@@ -468,7 +481,12 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
     EpiParams e;
     e.resid = x;
     e.ldr = d;
-    TRY(prof_begin(m, TADM_STAGE_OPROJ));
+    const int S = m->dt == BF16 ? gemm_resid_slices(N, d, H * dh) : 1;
+    if (S > 1) {
+      TRY(ensure_kpart(m, (size_t)S * N * d));
+      e.part = s.kpart;
+    }
+    TRY(prof_begin(m, TADM_STAGE_OPROJ, S > 1));
     HIPCHK(gemm(m->dt, p, EPI_RESID, e, st));
     TRY(prof_end(m, TADM_STAGE_OPROJ));
   }
@@ -500,7 +518,12 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
     EpiParams e;
     e.resid = x;
     e.ldr = d;
-    TRY(prof_begin(m, TADM_STAGE_FFN_DOWN));
+    const int S = m->dt == BF16 ? gemm_resid_slices(N, d, F) : 1;
+    if (S > 1) {
+      TRY(ensure_kpart(m, (size_t)S * N * d));
+      e.part = s.kpart;
+    }
+    TRY(prof_begin(m, TADM_STAGE_FFN_DOWN, S > 1));
     HIPCHK(gemm(m->dt, p, EPI_RESID, e, st));
     TRY(prof_end(m, TADM_STAGE_FFN_DOWN));
   }
@@ -1165,13 +1188,7 @@ static tadm_status entropy_impl(tadm_model* m, const float* logits, const int32_
     e.row1 = s.rscale;
     const int S = m->dt == BF16 ? gemm_split_slices(rows, d, Vp) : 1;
     if (S > 1) {
-      const size_t need = (size_t)S * rows * d;
-      if (s.kpart_cap < need) {
-        if (s.kpart) HIPCHK(hipFree(s.kpart));
-        s.kpart = nullptr;
-        HIPCHK(hipMalloc((void**)&s.kpart, need * 4));
-        s.kpart_cap = need;
-      }
+      TRY(ensure_kpart(m, (size_t)S * rows * d));
       e.part = s.kpart;
     }
     HIPCHK(gemm(m->dt, p, EPI_SCALE_F32, e, m->stream));
