@@ -338,14 +338,24 @@ __global__ void resid_reduce_kernel(const float* part, int S, int M, int N, floa
 }
 
 // K slices of a residual product with a long K and fewer than two 128 x 128 tiles per
-// CU: double while the grid has fewer than 512 blocks and each slice keeps >= 16 K tiles
+// CU (512 resident blocks): the S in {2, 4, 8} (each slice >= 16 K tiles) whose grid
+// best fills whole rounds of 512 blocks, the smaller S on ties
 int resid_slices(int M, int N, int K) {
   const long tiles = (long)((M + 127) / 128) * ((N + 127) / 128);
   const int nk = K / 64;
   if (tiles >= 512 || nk < 64 || N % 4) return 1;
-  int S = 1;
-  while (S < 8 && tiles * S < 512 && nk % (2 * S) == 0 && nk / (2 * S) >= 16) S *= 2;
-  return S;
+  int best = 1;
+  double best_fill = 0.0;
+  for (int S = 2; S <= 8; S *= 2) {
+    if (nk % S || nk / S < 16) break;
+    const long blocks = tiles * S, rounds = (blocks + 511) / 512;
+    const double fill = (double)blocks / (512.0 * rounds);
+    if (fill > best_fill + 1e-9) {
+      best = S;
+      best_fill = fill;
+    }
+  }
+  return best;
 }
 
 }  // namespace
