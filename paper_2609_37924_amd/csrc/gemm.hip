@@ -259,7 +259,14 @@ hipError_t dispatch(DType dt, const GemmProblem& p, const EpiParams& e, hipStrea
   const long t256 = (long)((p.M + 255) / 256) * ((p.N + 255) / 256);
   const long t128 = (long)((p.M + 127) / 128) * ((p.N + 127) / 128);
   if ((p.M >= 4096 || p.N >= 16384) && t256 >= 128) return launch_bf16<256, 256, 2, 2, 4, 1, K>(p, e, s);
-  if (t128 >= 256) return launch_bf16<128, 128, 2, 2, 2, 2, K>(p, e, s);
+  if (t128 >= 256) {
+    // two blocks per CU run in rounds of 512; 192 x 128 tiles win when they need fewer
+    // rounds for the same rows (e.g. 768 tiles of 128 x 128 = 1.5 rounds -> 512 of 192 x 128)
+    const long t192 = (long)((p.M + 191) / 192) * ((p.N + 127) / 128);
+    const long cost128 = (t128 + 511) / 512 * 128 * 128, cost192 = (t192 + 511) / 512 * 192 * 128;
+    if (cost192 < cost128) return launch_bf16<192, 128, 2, 2, 2, 2, K>(p, e, s);
+    return launch_bf16<128, 128, 2, 2, 2, 2, K>(p, e, s);
+  }
   return launch_bf16<64, 64, 2, 2, 2, 3, K>(p, e, s);
 }
 
