@@ -146,15 +146,26 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
     }
     // s[ks][j] = score(query lane&15, key t*64 + ks*16 + 4*grp + j)
     float mt = -INFINITY;
+    if ((t + 1) * KT <= Lk) {  // a whole tile: no key is masked
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
+      for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int key = t * KT + ks * 16 + 4 * grp + j;
-        const float v = key < Lk ? s[ks][j] * scale_log2 : -INFINITY;
-        s[ks][j] = v;
-        mt = fmaxf(mt, v);
-      }
+        for (int j = 0; j < 4; ++j) {
+          const float v = s[ks][j] * scale_log2;
+          s[ks][j] = v;
+          mt = fmaxf(mt, v);
+        }
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int key = t * KT + ks * 16 + 4 * grp + j;
+          const float v = key < Lk ? s[ks][j] * scale_log2 : -INFINITY;
+          s[ks][j] = v;
+          mt = fmaxf(mt, v);
+        }
+    }
     mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
     const float m_new = fmaxf(m_run, mt);
