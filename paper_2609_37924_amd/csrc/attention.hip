@@ -169,13 +169,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
     mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
     const float m_new = fmaxf(m_run, mt);
-    const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
+    // raw v_exp_f32: results below 2^-126 flush to 0 (a probability that small adds nothing)
+    const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
     float ps = 0.f;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float p = exp2f(s[ks][j] - m_new);
+        const float p = __builtin_amdgcn_exp2f(s[ks][j] - m_new);
         s[ks][j] = p;
         ps += p;
       }
