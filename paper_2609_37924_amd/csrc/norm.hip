@@ -30,8 +30,9 @@ __global__ void embed_kernel(const int32_t* tok, int n_tok, const T* E, int d, i
   *reinterpret_cast<float4*>(out + (size_t)t * d + 4 * c) = load4(E + (size_t)row * d + 4 * c);
 }
 
-// y[r] = x[map(r)] * rsqrt(mean(x^2) + eps) * g
-template <class T>
+// y[r] = x[map(r)] * rsqrt(mean(x^2) + eps) * g.  NV > 0: d <= 256 NV and the row stays in
+// registers between the two passes (one read of x); NV = 0: any d, x read twice.
+template <class T, int NV>
 __global__ __launch_bounds__(256) void rms_kernel(const float* x, const float* g, float eps,
                                                   int n_rows, int d, int rows_per_b,
                                                   int in_stride_b, int in_off, T* y) {
@@ -39,18 +40,38 @@ __global__ __launch_bounds__(256) void rms_kernel(const float* x, const float* g
   if (r >= n_rows) return;
   const long src = (long)(r / rows_per_b) * in_stride_b + in_off + (r % rows_per_b);
   const float* xr = x + src * d;
-  float ss = 0.f;
-  for (int c = lane * 4; c < d; c += 256) {
-    const float4 v = *reinterpret_cast<const float4*>(xr + c);
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-  }
-  ss = wave_sum(ss);
-  const float rs = rsqrtf(ss / d + eps);
   T* yr = y + (size_t)r * d;
-  for (int c = lane * 4; c < d; c += 256) {
-    const float4 v = *reinterpret_cast<const float4*>(xr + c);
-    const float4 w = *reinterpret_cast<const float4*>(g + c);
-    store4(yr + c, v.x * rs * w.x, v.y * rs * w.y, v.z * rs * w.z, v.w * rs * w.w);
+  float ss = 0.f;
+  if constexpr (NV > 0) {
+    float4 v[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane * 4 + 256 * i;
+      v[i] = c < d ? *reinterpret_cast<const float4*>(xr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+    }
+    ss = wave_sum(ss);
+    const float rs = rsqrtf(ss / d + eps);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane * 4 + 256 * i;
+      if (c < d) {
+        const float4 w = *reinterpret_cast<const float4*>(g + c);
+        store4(yr + c, v[i].x * rs * w.x, v[i].y * rs * w.y, v[i].z * rs * w.z, v[i].w * rs * w.w);
+      }
+    }
+  } else {
+    for (int c = lane * 4; c < d; c += 256) {
+      const float4 v = *reinterpret_cast<const float4*>(xr + c);
+      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+    ss = wave_sum(ss);
+    const float rs = rsqrtf(ss / d + eps);
+    for (int c = lane * 4; c < d; c += 256) {
+      const float4 v = *reinterpret_cast<const float4*>(xr + c);
+      const float4 w = *reinterpret_cast<const float4*>(g + c);
+      store4(yr + c, v.x * rs * w.x, v.y * rs * w.y, v.z * rs * w.z, v.w * rs * w.w);
+    }
   }
 }
 
@@ -147,12 +168,25 @@ hipError_t embed_gather(DType dt, const int32_t* tok, int n_tok, const void* emb
 hipError_t rms_norm(DType dt, const float* x, const float* g, float eps, int n_rows, int d,
                     int rows_per_b, int in_stride_b, int in_off, void* y, hipStream_t s) {
   if (n_rows == 0) return hipSuccess;
-  if (dt == BF16)
-    hipLaunchKernelGGL(rms_kernel<bf16>, dim3(blocks(n_rows, 4)), dim3(256), 0, s, x, g, eps, n_rows,
-                       d, rows_per_b, in_stride_b, in_off, static_cast<bf16*>(y));
-  else
-    hipLaunchKernelGGL(rms_kernel<float>, dim3(blocks(n_rows, 4)), dim3(256), 0, s, x, g, eps, n_rows,
-                       d, rows_per_b, in_stride_b, in_off, static_cast<float*>(y));
+  const dim3 grid(blocks(n_rows, 4));
+  if (dt == BF16) {
+    bf16* yb = static_cast<bf16*>(y);
+    if (d <= 1024)
+      hipLaunchKernelGGL((rms_kernel<bf16, 4>), grid, dim3(256), 0, s, x, g, eps, n_rows, d, rows_per_b,
+                         in_stride_b, in_off, yb);
+    else if (d <= 2048)
+      hipLaunchKernelGGL((rms_kernel<bf16, 8>), grid, dim3(256), 0, s, x, g, eps, n_rows, d, rows_per_b,
+                         in_stride_b, in_off, yb);
+    else if (d <= 4608)
+      hipLaunchKernelGGL((rms_kernel<bf16, 18>), grid, dim3(256), 0, s, x, g, eps, n_rows, d, rows_per_b,
+                         in_stride_b, in_off, yb);
+    else
+      hipLaunchKernelGGL((rms_kernel<bf16, 0>), grid, dim3(256), 0, s, x, g, eps, n_rows, d, rows_per_b,
+                         in_stride_b, in_off, yb);
+  } else {
+    hipLaunchKernelGGL((rms_kernel<float, 0>), grid, dim3(256), 0, s, x, g, eps, n_rows, d, rows_per_b,
+                       in_stride_b, in_off, static_cast<float*>(y));
+  }
   return hipGetLastError();
 }
 
