@@ -26,6 +26,14 @@ __device__ __forceinline__ void store4(bf16* p, float a, float b, float c, float
   *reinterpret_cast<bf16x4*>(p) = v;
 }
 
+// Store 2 consecutive values (4 B for bf16, 8 B for float).
+__device__ __forceinline__ void store2(float* p, float a, float b) { *reinterpret_cast<float2*>(p) = make_float2(a, b); }
+__device__ __forceinline__ void store2(bf16* p, float a, float b) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 v = {(bf16)a, (bf16)b};
+  *reinterpret_cast<bf16x2*>(p) = v;
+}
+
 // Workgroups of a launch are dispatched round-robin over the 8 XCDs (id % 8), each with
 // its own L2.  Renumber ids so that XCD x runs one contiguous range of logical ids:
 // neighbouring work items that read the same data then share an L2.

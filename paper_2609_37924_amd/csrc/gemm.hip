@@ -147,10 +147,8 @@ struct Epi<EPI_QKV_ROPE, T> {
       T* row = slot < e.H
                    ? static_cast<T*>(e.q) + (((size_t)b * e.H + slot) * e.L + l) * e.dh
                    : static_cast<T*>(e.k) + (((size_t)b * e.Hkv + (slot - e.H)) * e.kv_cap + e.kv_off + l) * e.dh;
-      row[j] = from_f32<T>(a0);
-      row[j + 1] = from_f32<T>(a1);
-      row[j + half] = from_f32<T>(b0);
-      row[j + half + 1] = from_f32<T>(b1);
+      store2(row + j, a0, a1);  // j is even: 4-byte (bf16) or 8-byte (float) aligned pairs
+      store2(row + j + half, b0, b1);
     } else {
       T* col = static_cast<T*>(e.vt) + (((size_t)b * e.Hkv + (slot - e.H - e.Hkv)) * e.dh + c) * e.kv_cap +
                e.kv_off + l;

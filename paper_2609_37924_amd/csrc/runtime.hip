@@ -202,7 +202,7 @@ bool valid_config(const tadm_config* c, std::string& why) {
   if (c->n_shared < 0 || c->n_anchor < 0 || c->n_denoise < 0) { why = "layer counts"; return false; }
   if (c->vocab > SAMPLE_MAX_VOCAB) { why = "vocab above the sampler's 262144 entries"; return false; }
   if (c->n_heads % c->n_kv_heads) { why = "n_heads must be a multiple of n_kv_heads"; return false; }
-  if (c->head_dim % 2) { why = "odd head_dim"; return false; }
+  if (c->head_dim % 4) { why = "head_dim must be a multiple of 4"; return false; }
   if (c->ffn_kind < 0 || c->ffn_kind > 2) { why = "ffn_kind"; return false; }
   if (c->fusion_kind < 0 || c->fusion_kind > 1) { why = "fusion_kind"; return false; }
   if (c->fusion_kind == TADM_FUSION_PAIRED &&
