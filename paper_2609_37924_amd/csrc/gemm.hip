@@ -134,9 +134,12 @@ struct Epi<EPI_PAIRED, T> {
 template <class T>
 struct Epi<EPI_QKV_ROPE, T> {
   static constexpr bool kGlu = false;
+  __device__ static int fdiv(int n, uint32_t mul, int shift) {
+    return (int)((__umulhi((uint32_t)n, mul) + (uint32_t)n) >> shift);
+  }
   __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
-    const int b = m / e.L, l = m % e.L;
-    const int slot = n / e.dh, c = n % e.dh;  // c is a multiple of 4
+    const int b = fdiv(m, e.l_mul, e.l_shift), l = m - b * e.L;
+    const int slot = fdiv(n, e.dh_mul, e.dh_shift), c = n - slot * e.dh;  // c is a multiple of 4
     if (slot < e.H + e.Hkv) {
       // (v0, v1) = pair j, (v2, v3) = pair j + 1 with j = c / 2
       const int j = c >> 1, half = e.dh >> 1;
@@ -406,7 +409,12 @@ hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e
     case EPI_ADD_BOTH: return dispatch<EPI_ADD_BOTH>(dt, p, e, s);
     case EPI_ADD_SUB: return dispatch<EPI_ADD_SUB>(dt, p, e, s);
     case EPI_PAIRED: return dispatch<EPI_PAIRED>(dt, p, e, s);
-    case EPI_QKV_ROPE: return dispatch<EPI_QKV_ROPE>(dt, p, e, s);
+    case EPI_QKV_ROPE: {
+      EpiParams f = e;
+      fast_divider((uint32_t)e.L, f.l_mul, f.l_shift);
+      fast_divider((uint32_t)e.dh, f.dh_mul, f.dh_shift);
+      return dispatch<EPI_QKV_ROPE>(dt, p, f, s);
+    }
     case EPI_SAMPLE: break;  // head_sample
   }
   return hipErrorInvalidValue;

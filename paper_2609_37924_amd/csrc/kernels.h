@@ -81,6 +81,9 @@ struct EpiParams {
   // pair (j, j + dh/2).  Q [B, H, L, dh], K rows kv_off + l of [B, Hkv, kv_cap, dh],
   // V^T columns kv_off + l of [B, Hkv, dh, kv_cap].
   int L = 0, pos0 = 0, H = 0, Hkv = 0, dh = 0, kv_cap = 0, kv_off = 0;
+  // n / L and n / dh as (umulhi(n, mul) + n) >> shift (n < 2^31), set by gemm()
+  uint32_t l_mul = 0, dh_mul = 0;
+  int l_shift = 0, dh_shift = 0;
   const float* cos_t = nullptr;
   const float* sin_t = nullptr;
   void* q = nullptr;
@@ -107,6 +110,13 @@ struct SamplePart {
 };
 
 hipError_t gemm(DType dt, const GemmProblem& p, EpiKind epi, const EpiParams& e, hipStream_t s);
+// Division by a fixed d >= 1 as q = (umulhi(n, mul) + n) >> shift, exact for 0 <= n < 2^31
+// (Granlund-Montgomery; mul = floor(2^32 (2^shift - d) / d) + 1, shift = ceil(log2 d)).
+inline void fast_divider(uint32_t d, uint32_t& mul, int& shift) {
+  shift = 0;
+  while ((1ull << shift) < d) ++shift;
+  mul = (uint32_t)(((1ull << 32) * ((1ull << shift) - d)) / d + 1);
+}
 // K slices the bf16 EPI_SCALE_F32 product uses (1: no split); its part buffer needs
 // slices * M * N floats.
 int gemm_split_slices(int M, int N, int K);
