@@ -367,8 +367,8 @@ def main():
         render_counter_summary(*args.render_counters[:3], command=args.command)
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build runs the path on a single MI355X "
-              "(multi-GPU sharding is design only).", file=sys.stderr)
+        print("bench.py measures one GPU: the path runs on a single MI355X "
+              "(sharding over several GPUs is described, not implemented).", file=sys.stderr)
         sys.exit(2)
     import torch
 

@@ -41,7 +41,7 @@ typedef enum {
   TADM_ERR_OOM = 2,          /* device allocation failed                           */
   TADM_ERR_DEVICE = 3,       /* HIP runtime error                                  */
   TADM_ERR_STATE = 4,        /* object mismatch, weights missing, wrong model      */
-  TADM_ERR_UNSUPPORTED = 5   /* valid request this build does not implement        */
+  TADM_ERR_UNSUPPORTED = 5   /* valid request the library does not implement       */
 } tadm_status;
 
 enum { TADM_DTYPE_F32 = 0, TADM_DTYPE_BF16 = 1 };
