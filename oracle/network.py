@@ -14,15 +14,12 @@ feed-forward (GELU, SwiGLU or GeGLU), residual.
 Precision.  Weights are the stored values (bf16 or fp32) and all arithmetic is
 float64.  A bf16 model (config dtype "bf16") additionally takes every operand of a
 matrix product in bf16: activations are rounded to bf16 (round to nearest even)
-where they enter a product -- the input of each layer projection, Q and K after
+where they enter a product -- the normalised input of each projection, Q and K after
 the rotary embedding, V, the softmax probabilities, the attention output, the
 feed-forward hidden state, the fusion input u and hidden state, the head input --
 while accumulation, norms, softmax, residual stream and elementwise maths stay in
-float64.  The RMSNorm in front of a layer projection scales each row by one factor
-1/rms(x), so (x / rms(x) * g) W = (1/rms(x)) ((x * g) W): the bf16 operand is x * g
-and the row factor multiplies the product (``norm_operand``).  That is the
-mixed-precision bf16 model (bf16 operands, wide accumulation); a float32 model has
-no rounding.
+float64.  That is the mixed-precision bf16 model (bf16 operands, wide accumulation);
+a float32 model has no rounding.
 
 Each function works on one batch row (arrays [L, ...]); rows are independent.
 """
@@ -45,17 +42,6 @@ def operand(cfg, x):
 
 def rms_norm(x, g, eps):
     return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * g
-
-
-def norm_operand(cfg, x, g, eps):
-    """RMSNorm(x) * g as the operand of a layer projection.  float32 models: the norm
-    itself.  bf16 models: the row factor 1/rms(x) times the bf16 operand x * g, i.e. the
-    product of the rounded x * g with its rows scaled afterwards (the same value in
-    exact arithmetic, since the factor is one scalar per row)."""
-    if cfg.get("dtype") != "bf16":
-        return rms_norm(x, g, eps)
-    r = 1.0 / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
-    return r * round_bf16(x * g)
 
 
 def layer_norm(x, w, b, eps):
@@ -135,7 +121,7 @@ def transformer_layer(W, li, x, pos, ctx_kv=None):
     p = f"layer{li}."
     L = x.shape[0]
     op = lambda t: operand(cfg, t)  # noqa: E731
-    xn = norm_operand(cfg, x, W[p + "attn_norm"], eps)
+    xn = op(rms_norm(x, W[p + "attn_norm"], eps))
     q = (xn @ W[p + "wq"].T).reshape(L, H, dh)
     k = (xn @ W[p + "wk"].T).reshape(L, Hkv, dh)
     v = (xn @ W[p + "wv"].T).reshape(L, Hkv, dh)
@@ -147,7 +133,7 @@ def transformer_layer(W, li, x, pos, ctx_kv=None):
         k_all, v_all = k, v
     o = op(attention(q, k_all, v_all, op).reshape(L, H * dh))
     x = x + o @ W[p + "wo"].T
-    xn = norm_operand(cfg, x, W[p + "ffn_norm"], eps)
+    xn = op(rms_norm(x, W[p + "ffn_norm"], eps))
     kind = cfg["ffn_kind"]
     if kind == "gelu":
         f = gelu(xn @ W[p + "w_up"].T)

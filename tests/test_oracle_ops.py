@@ -139,20 +139,3 @@ def test_bf16_model_rounds_only_product_operands():
     assert 0 < np.abs(a - b).max() < 2e-2
     v = N.round_bf16(rng.normal(size=100))
     assert np.array_equal(N.operand(cfg16, v), v) and np.array_equal(N.operand(cfg32, x), x)
-
-
-def test_norm_operand_is_the_row_scaled_rounded_product():
-    """The bf16 norm operand: (r * bf16(x g)) W equals r * (bf16(x g) W) row by row, it
-    is the plain RMSNorm when x g is already a bf16 value, and float32 models take the
-    norm unrounded."""
-    cfg16 = synth.get_config("tiny", dtype="bf16")
-    cfg32 = synth.get_config("tiny", dtype="f32")
-    x, g, W = rng.normal(size=(9, 64)) * 3.0, 1.0 + 0.1 * rng.normal(size=64), rng.normal(size=(32, 64))
-    eps = 1e-6
-    r = 1.0 / np.sqrt((x * x).mean(axis=-1, keepdims=True) + eps)
-    xg16 = torch.from_numpy(x * g).to(torch.bfloat16).to(torch.float64).numpy()
-    np.testing.assert_allclose(N.norm_operand(cfg16, x, g, eps) @ W.T, r * (xg16 @ W.T), rtol=1e-12, atol=1e-12)
-    np.testing.assert_allclose(N.norm_operand(cfg32, x, g, eps), x * r * g, rtol=1e-14, atol=0)
-    ones = np.ones(64)
-    xb = N.round_bf16(x)
-    np.testing.assert_allclose(N.norm_operand(cfg16, xb, ones, eps), N.rms_norm(xb, ones, eps), rtol=1e-14, atol=0)
