@@ -66,40 +66,48 @@ struct Epi<EPI_SAMPLE, T> {
         }
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      // S_g: each rint(exp(l' - m_g) 2^40) <= 2^40 is split exactly into 20-bit halves
-      uint32_t hi = 0, lo = 0;
+      // S_g: each rint(exp(l' - m_g) 2^40) <= 2^40 is an integer, so float64 sums of up to
+      // 2^13 of them are exact
+      double S = 0.0;
       // screening: this lane's two best scores, with the best entry's l' and u
       float a1 = -INFINITY, a2 = -INFINITY, lp1 = 0.f, u1 = 0.5f;
       int v1 = 0x7FFFFFFF;
+      // one vocabulary entry; the first loop is for strips wholly inside the vocabulary
+      auto entry = [&](float l, float u, int v) {
+        S += (double)rintf(own_exp(l - mx) * 1099511627776.0f);  // * 2^40
+        const float sc = screen_score(l, u);
+        if (sc > a1) {
+          a2 = a1;
+          a1 = sc;
+          v1 = v;
+          lp1 = l;
+          u1 = u;
+        } else if (sc > a2) {
+          a2 = sc;
+        }
+      };
+      if (nb + TN * 16 <= p.N) {
 #pragma unroll
-      for (int a = 0; a < TN; ++a) {
-        const int n0 = nb + 16 * a + 4 * fq;
-        uint32_t c[4] = {(uint32_t)n0 >> 2, pos, brow, e.step_id};
-        philox4x32_10(c, e.k0, e.k1);
+        for (int a = 0; a < TN; ++a) {
+          const int n0 = nb + 16 * a + 4 * fq;
+          uint32_t c[4] = {(uint32_t)n0 >> 2, pos, brow, e.step_id};
+          philox4x32_10(c, e.k0, e.k1);
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          if (n0 + jj >= p.N) continue;
-          const float q = rintf(own_exp(lp[a][jj] - mx) * 1099511627776.0f);  // * 2^40
-          const float qh = floorf(q * 9.5367431640625e-07f);                      // * 2^-20
-          hi += (uint32_t)qh;
-          lo += (uint32_t)(q - qh * 1048576.0f);
-          const float u = uniform01(c[jj]);
-          const float sc = screen_score(lp[a][jj], u);
-          if (sc > a1) {
-            a2 = a1;
-            a1 = sc;
-            v1 = n0 + jj;
-            lp1 = lp[a][jj];
-            u1 = u;
-          } else if (sc > a2) {
-            a2 = sc;
-          }
+          for (int jj = 0; jj < 4; ++jj) entry(lp[a][jj], uniform01(c[jj]), n0 + jj);
+        }
+      } else {
+#pragma unroll
+        for (int a = 0; a < TN; ++a) {
+          const int n0 = nb + 16 * a + 4 * fq;
+          uint32_t c[4] = {(uint32_t)n0 >> 2, pos, brow, e.step_id};
+          philox4x32_10(c, e.k0, e.k1);
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+            if (n0 + jj < p.N) entry(lp[a][jj], uniform01(c[jj]), n0 + jj);
         }
       }
-      hi += __shfl_xor(hi, 16, 64);
-      hi += __shfl_xor(hi, 32, 64);
-      lo += __shfl_xor(lo, 16, 64);
-      lo += __shfl_xor(lo, 32, 64);
+      S += __shfl_xor(S, 16, 64);
+      S += __shfl_xor(S, 32, 64);
       float amax = fmaxf(a1, __shfl_xor(a1, 16, 64));
       amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
       const float delta = 1e-3f + 2.4e-6f * (fabsf(mx) + 32.f);  // screening error bound, x 100
@@ -130,7 +138,7 @@ struct Epi<EPI_SAMPLE, T> {
         r.score = best.score;
         r.lp = best.lp;
         r.v = best.v;
-        r.S = ((long long)hi << 20) + (long long)lo;
+        r.S = (long long)S;
         static_cast<SamplePart*>(e.part)[(size_t)m * e.n_groups + g] = r;
       }
     }
