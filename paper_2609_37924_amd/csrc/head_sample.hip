@@ -56,12 +56,13 @@ struct Epi<EPI_SAMPLE, T> {
       const uint32_t brow = (uint32_t)(ci / e.Lc), pos = (uint32_t)(e.pos_base + ci % e.Lc);
       float lp[TN][4];
       float mx = -INFINITY;
+      const bool whole = nb + TN * 16 <= p.N;  // the strip lies inside the vocabulary
 #pragma unroll
       for (int a = 0; a < TN; ++a)
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
           const int n = nb + 16 * a + 4 * fq + jj;
-          lp[a][jj] = n < p.N ? cb[a][jj] * e.inv_temp : -INFINITY;
+          lp[a][jj] = (whole || n < p.N) ? cb[a][jj] * e.inv_temp : -INFINITY;
           mx = fmaxf(mx, lp[a][jj]);
         }
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
@@ -74,19 +75,16 @@ struct Epi<EPI_SAMPLE, T> {
       int v1 = 0x7FFFFFFF;
       // one vocabulary entry; the first loop is for strips wholly inside the vocabulary
       auto entry = [&](float l, float u, int v) {
-        S += (double)rintf(own_exp(l - mx) * 1099511627776.0f);  // * 2^40
+        S += (double)rintf(own_exp_sel_2p40(l - mx));
         const float sc = screen_score(l, u);
-        if (sc > a1) {
-          a2 = a1;
-          a1 = sc;
-          v1 = v;
-          lp1 = l;
-          u1 = u;
-        } else if (sc > a2) {
-          a2 = sc;
-        }
+        const bool top = sc > a1;  // selects, not branches: the update runs on every lane
+        a2 = top ? a1 : fmaxf(a2, sc);
+        a1 = top ? sc : a1;
+        v1 = top ? v : v1;
+        lp1 = top ? l : lp1;
+        u1 = top ? u : u1;
       };
-      if (nb + TN * 16 <= p.N) {
+      if (whole) {
 #pragma unroll
         for (int a = 0; a < TN; ++a) {
           const int n0 = nb + 16 * a + 4 * fq;

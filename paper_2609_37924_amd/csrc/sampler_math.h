@@ -34,8 +34,10 @@ __device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32
   }
 }
 
+// (2 (x >> 9) + 1) 2^-24: the float 1 + (x >> 9) 2^-23 minus 1 - 2^-24, a subtraction
+// that is exact (Sterbenz: the operands are within a factor of two)
 __device__ __forceinline__ float uniform01(uint32_t x) {
-  return (float)((x >> 9) * 2u + 1u) * 5.9604644775390625e-8f;  // * 2^-24, exact
+  return __uint_as_float((x >> 9) | 0x3F800000u) - bits_f(0x3F7FFFFFu);
 }
 
 __device__ __forceinline__ float own_log(float x) {
@@ -85,6 +87,27 @@ __device__ __forceinline__ float own_exp_sel(float y) {
   const bool under = y < -30.0f;
   const float e = own_exp(under ? -30.0f : y);
   return under ? 0.0f : e;
+}
+
+// own_exp_sel(y) * 2^40 with the power of two folded into the exponent: the same value,
+// since both scalings by powers of two are exact in the normal range own_exp reaches
+// (its results lie in [e^-30, e^0.35] or are 0).
+__device__ __forceinline__ float own_exp_sel_2p40(float y) {
+  const bool under = y < -30.0f;
+  const float yy = under ? -30.0f : y;
+  const float LN2_HI = bits_f(0x3F317200u), LN2_LO = bits_f(0x35BFBE8Eu);
+  const float k = rintf(yy * bits_f(0x3FB8AA3Bu));
+  const float r = (yy - k * LN2_HI) - k * LN2_LO;
+  float p = bits_f(0x39500D01u);
+  p = p * r + bits_f(0x3AB60B61u);
+  p = p * r + bits_f(0x3C088889u);
+  p = p * r + bits_f(0x3D2AAAABu);
+  p = p * r + bits_f(0x3E2AAAABu);
+  p = p * r + 0.5f;
+  p = p * r + 1.0f;
+  p = p * r + 1.0f;
+  const float scale = __uint_as_float((uint32_t)((int)k + 127 + 40) << 23);
+  return under ? 0.0f : p * scale;
 }
 
 struct Best {
