@@ -58,11 +58,14 @@ __global__ __launch_bounds__(256) void rope_split_kernel(const T* qkv, int B, in
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 typedef const __attribute__((address_space(1))) void* gbl_ptr;
-constexpr int vmcnt_all() { return (7 << 4) | (15 << 8); }  // s_waitcnt vmcnt(0)
+// waitcnt immediate for "at most n vector-memory operations outstanding" (gfx9 encoding)
+constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
 
 // K tile: 64 keys x DH, stored as DH/64 planes of [64 keys][128 B]; V^T tile: DH rows x
-// 64 keys of 128 B.  Chunk c (8 bf16) of LDS row r sits in slot c ^ (r & 7).
-template <int DH>
+// 64 keys of 128 B.  Chunk c (8 bf16) of K row r sits in slot c ^ (r & 7), of V^T row r
+// in slot c ^ (r & 7) ^ ((r >> 3) & 1): the V^T fragments are read 8 bytes per lane, 32
+// lanes per LDS pass over rows r and r + 8, which the extra bit sends to other banks.
+template <int DH, int NS>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const bf16* K,
                                                            const bf16* Vt, bf16* O, int H, int Hkv,
                                                            int Lq, int Lk, int kv_cap,
@@ -70,7 +73,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
   constexpr int KT = 64;
   constexpr int KBYTES = KT * DH * 2, VBYTES = DH * KT * 2, STAGE = KBYTES + VBYTES;
   constexpr int LK = KBYTES / 1024 / 4, LV = VBYTES / 1024 / 4;  // load instructions per wave
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  constexpr int LPT = LK + LV;                                      // per wave per tile
+  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, grp = lane >> 4, fr = lane & 15;
   // one block per (64-query tile, head, batch row), query tiles fastest: the tiles of a
@@ -89,6 +93,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
   for (int kc = 0; kc < DH / 32; ++kc) qf[kc] = *reinterpret_cast<const bf16x8*>(Qr + 32 * kc + 8 * grp);
 
   const int lrow = lane >> 3, lchunk = (lane & 7) ^ (lane >> 3);
+  const int lchunk_v = lchunk ^ (wave & 1);  // V^T rows 8 g + lrow with g = wave + 4 j
   const int nt = (Lk + KT - 1) / KT;
   auto issue = [&](int t, int buf) {
     const int k0 = t * KT;
@@ -102,7 +107,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
 #pragma unroll
     for (int j = 0; j < LV; ++j) {  // 8-row groups of V^T
       const int g = wave + 4 * j, r = g * 8 + lrow;
-      const bf16* src = Vb + (size_t)r * kv_cap + k0 + lchunk * 8;  // k0 + 64 <= kv_cap
+      const bf16* src = Vb + (size_t)r * kv_cap + k0 + lchunk_v * 8;  // k0 + 64 <= kv_cap
       __builtin_amdgcn_global_load_lds((gbl_ptr)src, (lds_ptr)(sb + KBYTES + g * 1024), 16, 0, 0);
     }
   };
@@ -112,35 +117,51 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
   for (int d = 0; d < DH / 16; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  issue(0, 0);
+  // this lane's LDS byte offsets inside a stage, the same for every K tile: K row fr of
+  // each 16-key block, chunk 4 (kc & 1) + grp; V^T row fr of each 16-row block, the
+  // half chunks of keys 32 kc2 + 4 grp + [0, 4) (chunk 4 kc2 + grp / 2) and 16 keys on
+  const int vsw = (fr & 7) ^ (fr >> 3);
+  int kofs[2], vofs[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    kofs[i] = fr * 128 + (((4 * i + grp) ^ (fr & 7)) * 16);
+    const int c0 = 4 * i + (grp >> 1);
+    vofs[i][0] = KBYTES + fr * 128 + ((c0 ^ vsw) * 16) + (grp & 1) * 8;
+    vofs[i][1] = KBYTES + fr * 128 + (((c0 + 2) ^ vsw) * 16) + (grp & 1) * 8;
+  }
+
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nt) issue(s, s);
   for (int t = 0; t < nt; ++t) {
-    const int buf = t & 1;
-    __builtin_amdgcn_s_waitcnt(vmcnt_all());
+    const int buf = t % NS;
+    if (t + NS - 2 < nt)  // tile t is in once at most NS - 2 younger tiles are in flight
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * LPT));
+    else
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     __syncthreads();
     const char* sk = smem + buf * STAGE;
-    const char* sv = sk + KBYTES;
     if ((t + 1) * KT > Lk) {
       // last, partial tile: keys past the end get V = 0 so that p = 0 meets finite values
-      char* svw = const_cast<char*>(sv);
+      char* svw = const_cast<char*>(sk + KBYTES);
       for (int idx = tid; idx < DH * KT; idx += 256) {
         const int r = idx / KT, key = idx % KT;
         if (t * KT + key >= Lk) {
-          const int slot = (key >> 3) ^ (r & 7);
+          const int slot = (key >> 3) ^ (r & 7) ^ ((r >> 3) & 1);
           *reinterpret_cast<bf16*>(svw + r * 128 + slot * 16 + (key & 7) * 2) = (bf16)0.f;
         }
       }
       __syncthreads();
     }
-    if (t + 1 < nt) issue(t + 1, buf ^ 1);
+    // the buffer of tile t - 1, which every wave finished before the barrier above
+    if (t + NS - 1 < nt) issue(t + NS - 1, (t + NS - 1) % NS);
     f32x4 s[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       s[ks] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int r = ks * 16 + fr;
 #pragma unroll
       for (int kc = 0; kc < DH / 32; ++kc) {
-        const int plane = kc >> 1, c = (kc & 1) * 4 + grp;
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + plane * 8192 + r * 128 + ((c ^ (r & 7)) * 16));
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + (kc >> 1) * 8192 + ks * 2048 + kofs[kc & 1]);
         s[ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kc], s[ks], 0, 0, 0);
       }
     }
@@ -192,14 +213,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
         pf[j] = (bf16)s[2 * kc2][j];
         pf[4 + j] = (bf16)s[2 * kc2 + 1][j];
       }
-      // keys 32*kc2 + 4*grp + [0,4) and 32*kc2 + 16 + 4*grp + [0,4): chunks 4*kc2 + grp/2
-      // and 4*kc2 + 2 + grp/2, at byte (grp & 1) * 8 inside the chunk
-      const int c0 = 4 * kc2 + (grp >> 1), c1 = c0 + 2, inb = (grp & 1) * 8;
 #pragma unroll
       for (int d = 0; d < DH / 16; ++d) {
-        const int r = d * 16 + fr;
-        const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(sv + r * 128 + ((c0 ^ (r & 7)) * 16) + inb);
-        const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(sv + r * 128 + ((c1 ^ (r & 7)) * 16) + inb);
+        const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(sk + d * 2048 + vofs[kc2][0]);
+        const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(sk + d * 2048 + vofs[kc2][1]);
         const bf16x8 vf = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
         o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[d], 0, 0, 0);
       }
@@ -278,11 +295,11 @@ hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, voi
     const dim3 grid(((Lq + 63) / 64) * H * B);
     const float sl2 = 1.4426950408889634f / sqrtf((float)dh);
     if (dh == 64)
-      launch_timed(attn_bf16_kernel<64>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
+      launch_timed(attn_bf16_kernel<64, 2>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
                    static_cast<const bf16*>(K), static_cast<const bf16*>(Vt), static_cast<bf16*>(O), H, Hkv, Lq,
                    Lk, kv_cap, sl2);
     else if (dh == 128)
-      launch_timed(attn_bf16_kernel<128>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
+      launch_timed(attn_bf16_kernel<128, 2>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
                    static_cast<const bf16*>(K), static_cast<const bf16*>(Vt), static_cast<bf16*>(O), H, Hkv, Lq,
                    Lk, kv_cap, sl2);
     else
