@@ -38,7 +38,7 @@ PEAK_HBM_GBS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="small")
     ap.add_argument("--K", type=int, default=4, help="headline refresh interval")
@@ -157,6 +157,10 @@ def kernel_table(cfg, B, K, stages):
                     "launches": n, "launches_expected": expect, "achieved": achieved, "peak": peak,
                     "unit": unit, "frac": achieved / peak, "work_per_launch": w / expect})
     return sorted(out, key=lambda r: -r["ms_per_step"])
+
+
+# the stage launched right before a stage in every layer / step (when it is a stage)
+PRED = {"oproj": "attn", "ffn_down": "ffn_up", "attn": "qkv", "fusion2": "fusion1", "sample": "head"}
 
 
 def source_digest(source):
@@ -402,8 +406,8 @@ def main():
 
     def timed(K, steps, warmup, profile=0, profiled_steps=None):
         """Time `steps` generations.  profile: stage bit mask timed during the last
-        `profiled_steps` of them (all by default); the timers add GPU time per timed
-        launch, so the headline pass times only its last generation's dominant kernel."""
+        `profiled_steps` of them (all by default); the timers add a little GPU time per
+        timed launch, so the headline pass times only its last generation."""
         profiled_steps = steps if profiled_steps is None else profiled_steps
         for _ in range(warmup):
             gen(K)
@@ -440,9 +444,12 @@ def main():
     for k in kernels:
         print(f"[bench]   {k['ms_per_step']:8.3f} ms  {k['achieved']:8.1f} {k['unit']:7s} ({100 * k['frac']:.1f}% "
               f"of peak)  {k['launches']} launches  {k['kernel']}", file=sys.stderr, flush=True)
-    # 2. headline; the dominant kernel's launches of the last generation carry timers
+    # 2. headline; the dominant kernel's launches of its last generation carry timers,
+    # and so do the launches right before them (a kernel timed after an untimed one is
+    # charged part of its predecessor's tail)
     dom = kernels[0] if kernels else None
-    mask = sum(1 << tadm.STAGES.index(n) for n in dom["stages"]) if dom else 0
+    timed_stages = set(dom["stages"]) | {PRED[n] for n in dom["stages"] if n in PRED} if dom else set()
+    mask = sum(1 << tadm.STAGES.index(n) for n in timed_stages)
     ms, wall_ms, dom_stages = timed(K0, args.steps, 1, profile=mask, profiled_steps=1)
     value = tokens / (ms / 1e3)
     print(f"[bench] K={K0}: {ms:.3f} ms/generation ({wall_ms:.3f} wall) -> {value:.1f} tokens/s",
@@ -518,7 +525,7 @@ def main():
               f"{B * Ltr / (tms / 1e3):.1f} tokens/s", file=sys.stderr, flush=True)
     roof = None
     if dom:
-        live = kernel_table(cfg, B, K0, dom_stages)[0]
+        live = next(r for r in kernel_table(cfg, B, K0, dom_stages) if r["kernel"] == dom["kernel"])
         source = next(k[4] for k in KERNELS if k[0] == dom["kernel"])
         traffic = stored_traffic(args.config, K0, dom["stages"][0], source)
         avg_ms = live["ms_per_step"] / live["launches"]

@@ -313,9 +313,11 @@ struct tadm_context {
 };
 
 // ---------------------------------------------------------------- profiling ---
+// Timing-only events: no system-scope fence when they complete (no cache writeback and
+// invalidation between the timed kernels); they are read after the stream has drained.
 static tadm_status prof_event(tadm_model* m, hipEvent_t* e) {
   if (m->pool.empty()) {
-    HIPCHK(hipEventCreate(e));
+    HIPCHK(hipEventCreateWithFlags(e, hipEventDisableSystemFence));
   } else {
     *e = m->pool.back();
     m->pool.pop_back();
