@@ -134,9 +134,12 @@ struct Epi<EPI_PAIRED, T> {
 template <class T>
 struct Epi<EPI_QKV_ROPE, T> {
   static constexpr bool kGlu = false;
+  static constexpr bool kTileLds = true;  // bf16 kernel: staged through LDS (tile_lds)
   __device__ static int fdiv(int n, uint32_t mul, int shift) {
     return (int)((__umulhi((uint32_t)n, mul) + (uint32_t)n) >> shift);
   }
+  // one 4-feature fragment, stored directly (float32 kernel, and head widths whose
+  // slots a wave strip does not tile)
   __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
     const int b = fdiv(m, e.l_mul, e.l_shift), l = m - b * e.L;
     const int slot = fdiv(n, e.dh_mul, e.dh_shift), c = n - slot * e.dh;  // c is a multiple of 4
@@ -157,6 +160,111 @@ struct Epi<EPI_QKV_ROPE, T> {
                e.kv_off + l;
 #pragma unroll
       for (int t = 0; t < 4; ++t) col[(size_t)t * e.kv_cap] = from_f32<T>(v[t]);
+    }
+  }
+
+  // Byte offset of element (r, col) of a [rows][C] bf16 staging tile: the 16-byte chunks
+  // of row r rotated by r + r / 8, so that the fragment writes (16 rows of one chunk)
+  // and the chunk reads (whole rows) meet distinct LDS banks.
+  template <int C>
+  __device__ static int staged(int r, int col) {
+    constexpr int NCH = C / 8;
+    return r * (C * 2) + (((col >> 3) + r + (r >> 3)) % NCH) * 16 + (col & 7) * 2;
+  }
+
+  // The wave's WTM tokens x WTN features lie in one head slot (dh % WTN == 0).  Q and K
+  // strips are rotated in registers and staged token-major, with the pair halves j and
+  // j + dh/2 already apart, so that each token's run of the head row leaves as 16-byte
+  // stores; V strips are staged feature-major and leave as 16-byte runs of 8 tokens of a
+  // V^T row.  Two phases with a block barrier between them (every wave of the block runs
+  // this function; the barrier orders each wave's LDS writes before its reads).
+  template <int TN, int TM>
+  __device__ static void tile_lds(const EpiParams& e, const GemmProblem& p, const f32x4 (&acc)[TN][TM], int mb,
+                                  int nb, int lane, char* lds) {
+    constexpr int WTN = TN * 16, WTM = TM * 16;
+    const int fr = lane & 15, fq = lane >> 4;
+    if (e.dh % WTN != 0) {  // the same for every wave of the grid
+#pragma unroll
+      for (int a = 0; a < TN; ++a)
+#pragma unroll
+        for (int b = 0; b < TM; ++b) {
+          const int m = mb + 16 * b + fr, n = nb + 16 * a + 4 * fq;
+          if (m < p.M && n < p.N) apply(e, m, n, acc[a][b]);
+        }
+      return;
+    }
+    const bool live = nb < p.N;
+    const int slot = fdiv(nb, e.dh_mul, e.dh_shift), c0 = nb - slot * e.dh;  // strip offset in the head
+    const int half = e.dh >> 1, jbase = c0 >> 1;
+    const bool is_v = slot >= e.H + e.Hkv;
+    // phase 1: stage
+    if (live && !is_v) {
+#pragma unroll
+      for (int b = 0; b < TM; ++b) {
+        const int r = 16 * b + fr;
+        const int m = min(mb + r, p.M - 1);  // rows past M are staged but never stored
+        const int bb = fdiv(m, e.l_mul, e.l_shift), l = m - bb * e.L;
+        const float* cs = e.cos_t + (size_t)(e.pos0 + l) * half + jbase;
+        const float* sn = e.sin_t + (size_t)(e.pos0 + l) * half + jbase;
+#pragma unroll
+        for (int a = 0; a < TN; ++a) {
+          const int pl = 8 * a + 2 * fq;  // local pair index of (v0, v1); (v2, v3) is pl + 1
+          const f32x4 v = acc[a][b];
+          const float2 c2 = *reinterpret_cast<const float2*>(cs + pl);
+          const float2 s2 = *reinterpret_cast<const float2*>(sn + pl);
+          const float a0 = v[0] * c2.x - v[1] * s2.x, b0 = v[1] * c2.x + v[0] * s2.x;
+          const float a1 = v[2] * c2.y - v[3] * s2.y, b1 = v[3] * c2.y + v[2] * s2.y;
+          store2(reinterpret_cast<bf16*>(lds + staged<WTN>(r, pl)), a0, a1);
+          store2(reinterpret_cast<bf16*>(lds + staged<WTN>(r, WTN / 2 + pl)), b0, b1);
+        }
+      }
+    } else if (live) {
+#pragma unroll
+      for (int a = 0; a < TN; ++a)
+#pragma unroll
+        for (int b = 0; b < TM; ++b)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+            *reinterpret_cast<bf16*>(lds + staged<WTM>(16 * a + 4 * fq + jj, 16 * b + fr)) = (bf16)acc[a][b][jj];
+    }
+    __syncthreads();
+    // phase 2: 16-byte chunks to the attention layouts
+    if (live && !is_v) {
+      constexpr int NC = WTN / 8;
+      T* base = slot < e.H ? static_cast<T*>(e.q) : static_cast<T*>(e.k);
+#pragma unroll
+      for (int idx = lane; idx < WTM * NC; idx += 64) {
+        const int r = idx / NC, c = idx % NC, m = mb + r;
+        if (m >= p.M) continue;
+        const int bb = fdiv(m, e.l_mul, e.l_shift), l = m - bb * e.L;
+        const size_t row = slot < e.H ? ((size_t)bb * e.H + slot) * e.L + l
+                                      : ((size_t)bb * e.Hkv + (slot - e.H)) * e.kv_cap + e.kv_off + l;
+        const int col = c < NC / 2 ? jbase + 8 * c : jbase + half + 8 * (c - NC / 2);
+        *reinterpret_cast<bf16x8*>(base + row * e.dh + col) = *reinterpret_cast<const bf16x8*>(lds + staged<WTN>(r, 8 * c));
+      }
+    } else if (live) {
+      constexpr int NC = WTM / 8;
+      const int hv = slot - e.H - e.Hkv;
+#pragma unroll
+      for (int idx = lane; idx < WTN * NC; idx += 64) {
+        const int f = idx / NC, c = idx % NC, m0 = mb + 8 * c;
+        if (m0 >= p.M) continue;
+        const bf16x8 v = *reinterpret_cast<const bf16x8*>(lds + staged<WTM>(f, 8 * c));
+        T* vrow = static_cast<T*>(e.vt) + (((size_t)0 * e.Hkv + hv) * e.dh + c0 + f) * e.kv_cap + e.kv_off;
+        const int b0 = fdiv(m0, e.l_mul, e.l_shift), l0 = m0 - b0 * e.L;
+        const size_t bstride = (size_t)e.Hkv * e.dh * e.kv_cap;  // one batch row of V^T
+        if (m0 + 8 <= p.M && l0 + 8 <= e.L && ((e.kv_off + l0) & 7) == 0) {
+          *reinterpret_cast<bf16x8*>(vrow + b0 * bstride + l0) = v;
+        } else {
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const int m = m0 + u;
+            if (m >= p.M) break;
+            const int bb = fdiv(m, e.l_mul, e.l_shift), l = m - bb * e.L;
+            vrow[bb * bstride + l] = v[u];
+          }
+        }
+      }
     }
   }
 };

@@ -23,7 +23,9 @@ namespace {
 
 // Epi<K, T> supplies the epilogue of kind K for operand type T: either apply() per
 // 4-feature fragment (with kGlu for gate/up pairs), or, when it defines kTile, a
-// tile<TN, TM>() that receives the wave's whole accumulator tile.
+// tile<TN, TM>() that receives the wave's whole accumulator tile, or, when it defines
+// kTileLds, a tile_lds<TN, TM>() that also receives WTM x WTN x 2 bytes of LDS of its
+// own (the K tiles' ring, free once every wave has left the main loop).
 template <EpiKind K, class T>
 struct Epi;
 
@@ -31,6 +33,10 @@ template <class E, class = void>
 struct TileEpi : std::false_type {};
 template <class E>
 struct TileEpi<E, std::void_t<decltype(E::kTile)>> : std::true_type {};
+template <class E, class = void>
+struct TileLdsEpi : std::false_type {};
+template <class E>
+struct TileLdsEpi<E, std::void_t<decltype(E::kTileLds)>> : std::true_type {};
 
 // An epilogue that reads other tensors may define kPre (float4 loads per fragment),
 // pre() and apply_pre(): the kernel then issues those loads before the main loop,
@@ -177,7 +183,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
   const int mw = m0 + wm * WTM + fr;
   if constexpr (KIND == EPI_STORE_F32)
     if (p.ksplit > 1) ep.out = static_cast<float*>(ep.out) + (size_t)blockIdx.y * ep.split_stride;
-  if constexpr (TileEpi<E>::value) {  // the epilogue takes the wave's whole tile
+  if constexpr (TileLdsEpi<E>::value) {  // the wave's whole tile, staged through LDS
+    static_assert(BM * BN * 2 <= STAGES * STAGE_BYTES, "staging area larger than the ring");
+    __syncthreads();  // every wave has finished reading the K tiles
+    E::template tile_lds<TN, TM>(ep, p, acc, m0 + wm * WTM, n0 + wn * WTN, lane, smem + wave * (WTM * WTN * 2));
+  } else if constexpr (TileEpi<E>::value) {  // the epilogue takes the wave's whole tile
     E::template tile<TN, TM>(ep, p, acc, m0 + wm * WTM, n0 + wn * WTN, lane);
   } else if constexpr (E::kGlu) {
 #pragma unroll
