@@ -146,10 +146,10 @@ struct Epi<EPI_QKV_ROPE, T> {
     if (slot < e.H + e.Hkv) {
       // (v0, v1) = pair j, (v2, v3) = pair j + 1 with j = c / 2
       const int j = c >> 1, half = e.dh >> 1;
-      const float* cs = e.cos_t + (size_t)(e.pos0 + l) * half + j;
-      const float* sn = e.sin_t + (size_t)(e.pos0 + l) * half + j;
-      const float a0 = v[0] * cs[0] - v[1] * sn[0], b0 = v[1] * cs[0] + v[0] * sn[0];
-      const float a1 = v[2] * cs[1] - v[3] * sn[1], b1 = v[3] * cs[1] + v[2] * sn[1];
+      // (cos j, sin j, cos j+1, sin j+1): j is even, so the load is 16-byte aligned
+      const float4 r = *reinterpret_cast<const float4*>(e.rope + ((size_t)(e.pos0 + l) * half + j) * 2);
+      const float a0 = v[0] * r.x - v[1] * r.y, b0 = v[1] * r.x + v[0] * r.y;
+      const float a1 = v[2] * r.z - v[3] * r.w, b1 = v[3] * r.z + v[2] * r.w;
       T* row = slot < e.H
                    ? static_cast<T*>(e.q) + (((size_t)b * e.H + slot) * e.L + l) * e.dh
                    : static_cast<T*>(e.k) + (((size_t)b * e.Hkv + (slot - e.H)) * e.kv_cap + e.kv_off + l) * e.dh;
@@ -204,16 +204,14 @@ struct Epi<EPI_QKV_ROPE, T> {
         const int r = 16 * b + fr;
         const int m = min(mb + r, p.M - 1);  // rows past M are staged but never stored
         const int bb = fdiv(m, e.l_mul, e.l_shift), l = m - bb * e.L;
-        const float* cs = e.cos_t + (size_t)(e.pos0 + l) * half + jbase;
-        const float* sn = e.sin_t + (size_t)(e.pos0 + l) * half + jbase;
+        const float* rp = e.rope + ((size_t)(e.pos0 + l) * half + jbase) * 2;
 #pragma unroll
         for (int a = 0; a < TN; ++a) {
           const int pl = 8 * a + 2 * fq;  // local pair index of (v0, v1); (v2, v3) is pl + 1
           const f32x4 v = acc[a][b];
-          const float2 c2 = *reinterpret_cast<const float2*>(cs + pl);
-          const float2 s2 = *reinterpret_cast<const float2*>(sn + pl);
-          const float a0 = v[0] * c2.x - v[1] * s2.x, b0 = v[1] * c2.x + v[0] * s2.x;
-          const float a1 = v[2] * c2.y - v[3] * s2.y, b1 = v[3] * c2.y + v[2] * s2.y;
+          const float4 rr = *reinterpret_cast<const float4*>(rp + 2 * pl);  // cos, sin of pl and pl + 1
+          const float a0 = v[0] * rr.x - v[1] * rr.y, b0 = v[1] * rr.x + v[0] * rr.y;
+          const float a1 = v[2] * rr.z - v[3] * rr.w, b1 = v[3] * rr.z + v[2] * rr.w;
           store2(reinterpret_cast<bf16*>(lds + staged<WTN>(r, pl)), a0, a1);
           store2(reinterpret_cast<bf16*>(lds + staged<WTN>(r, WTN / 2 + pl)), b0, b1);
         }

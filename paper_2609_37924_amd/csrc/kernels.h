@@ -84,8 +84,7 @@ struct EpiParams {
   // n / L and n / dh as (umulhi(n, mul) + n) >> shift (n < 2^31), set by gemm()
   uint32_t l_mul = 0, dh_mul = 0;
   int l_shift = 0, dh_shift = 0;
-  const float* cos_t = nullptr;
-  const float* sin_t = nullptr;
+  const float* rope = nullptr;  // (cos, sin) of position p and rotary pair j at rope[2 (p dh/2 + j)]
   void* q = nullptr;
   void* k = nullptr;
   void* vt = nullptr;

@@ -271,7 +271,7 @@ struct tadm_model {
   Layout lay;
   char* arena = nullptr;
   std::vector<char> loaded;
-  float *rope_cos = nullptr, *rope_sin = nullptr;
+  float* rope = nullptr;  // rotary table [max_seq][dh/2][cos, sin]
   Workspace ws;
   bool taps = false;
   bool tap_final = false;  // TADM_TAP_FINAL holds every canvas row (full-logits step)
@@ -466,8 +466,7 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
     e.dh = dh;
     e.kv_cap = kv.cap;
     e.kv_off = kv.off;
-    e.cos_t = m->rope_cos;
-    e.sin_t = m->rope_sin;
+    e.rope = m->rope;
     e.q = s.q;
     e.k = kv.k;
     e.vt = kv.vt;
@@ -855,19 +854,18 @@ tadm_status tadm_model_create(const tadm_config* cfg, tadm_model** out) {
     return fail(e == hipErrorOutOfMemory ? TADM_ERR_OOM : TADM_ERR_DEVICE, "weight arena (%zu bytes): %s",
                 bytes, hipGetErrorString(e));
   }
-  // rotary tables [max_seq, dh/2], angles in double precision
+  // rotary table [max_seq, dh/2, (cos, sin)], angles in double precision; the pairs of
+  // one position are interleaved so that one 16-byte load fetches two rotary pairs
   const int half = cfg->head_dim / 2;
-  std::vector<float> cs((size_t)cfg->max_seq * half), sn(cs.size());
+  std::vector<float> cs((size_t)cfg->max_seq * half * 2);
   for (int p = 0; p < cfg->max_seq; ++p)
     for (int j = 0; j < half; ++j) {
       const double ang = p * std::pow((double)cfg->rope_theta, -2.0 * j / cfg->head_dim);
-      cs[(size_t)p * half + j] = (float)std::cos(ang);
-      sn[(size_t)p * half + j] = (float)std::sin(ang);
+      cs[((size_t)p * half + j) * 2] = (float)std::cos(ang);
+      cs[((size_t)p * half + j) * 2 + 1] = (float)std::sin(ang);
     }
-  e = hipMalloc((void**)&m->rope_cos, cs.size() * 4);
-  if (e == hipSuccess) e = hipMalloc((void**)&m->rope_sin, sn.size() * 4);
-  if (e == hipSuccess) e = hipMemcpy(m->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice);
-  if (e == hipSuccess) e = hipMemcpy(m->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice);
+  e = hipMalloc((void**)&m->rope, cs.size() * 4);
+  if (e == hipSuccess) e = hipMemcpy(m->rope, cs.data(), cs.size() * 4, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     tadm_model_destroy(m);
     return fail(TADM_ERR_DEVICE, "rope tables: %s", hipGetErrorString(e));
@@ -925,8 +923,7 @@ tadm_status tadm_model_destroy(tadm_model* m) {
   for (void* p : m->ws.allocs) (void)hipFree(p);
   if (m->ws.logits) (void)hipFree(m->ws.logits);
   if (m->arena) (void)hipFree(m->arena);
-  if (m->rope_cos) (void)hipFree(m->rope_cos);
-  if (m->rope_sin) (void)hipFree(m->rope_sin);
+  if (m->rope) (void)hipFree(m->rope);
   next_launch_events = LaunchEvents{};
   for (auto& o : m->open) {
     (void)hipEventDestroy(o.a);
