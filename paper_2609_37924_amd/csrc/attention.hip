@@ -187,8 +187,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
           mt = fmaxf(mt, v);
         }
     }
-    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    mt = fmaxf(mt, xor16(mt));
+    mt = fmaxf(mt, xor32(mt));
     const float m_new = fmaxf(m_run, mt);
     // raw v_exp_f32: results below 2^-126 flush to 0 (a probability that small adds nothing)
     const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
@@ -222,8 +222,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
       }
     }
   }
-  float l_tot = l_run + __shfl_xor(l_run, 16, 64);
-  l_tot += __shfl_xor(l_tot, 32, 64);
+  float l_tot = l_run + xor16(l_run);
+  l_tot += xor32(l_tot);
   const float inv = 1.f / l_tot;
   if (q < Lq) {
     bf16* orow = O + ((size_t)b * Lq + q) * H * DH + h * DH;

@@ -34,6 +34,32 @@ __device__ __forceinline__ void store2(bf16* p, float a, float b) {
   *reinterpret_cast<bf16x2*>(p) = v;
 }
 
+// The value held by lane l ^ 16 (xor16) or l ^ 32 (xor32) of the wave, exchanged with
+// v_permlane16_swap / v_permlane32_swap (a VALU operation; __shfl_xor goes through the
+// LDS crossbar).  A swap of v with itself leaves, in every lane, the value of the lower
+// and of the upper row (16 lanes) or half (32 lanes) of its pair; the lane takes the
+// other one.  Block sizes are multiples of 64, so bit 4 / 5 of threadIdx.x is the lane's.
+__device__ __forceinline__ uint32_t xor16(uint32_t v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return (threadIdx.x & 16) ? r[0] : r[1];
+}
+__device__ __forceinline__ uint32_t xor32(uint32_t v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return (threadIdx.x & 32) ? r[0] : r[1];
+}
+__device__ __forceinline__ float xor16(float v) { return __uint_as_float(xor16(__float_as_uint(v))); }
+__device__ __forceinline__ float xor32(float v) { return __uint_as_float(xor32(__float_as_uint(v))); }
+__device__ __forceinline__ int xor16(int v) { return (int)xor16((uint32_t)v); }
+__device__ __forceinline__ int xor32(int v) { return (int)xor32((uint32_t)v); }
+__device__ __forceinline__ double xor16(double v) {
+  const uint64_t b = __double_as_longlong(v);
+  return __longlong_as_double((long long)(((uint64_t)xor16((uint32_t)(b >> 32)) << 32) | xor16((uint32_t)b)));
+}
+__device__ __forceinline__ double xor32(double v) {
+  const uint64_t b = __double_as_longlong(v);
+  return __longlong_as_double((long long)(((uint64_t)xor32((uint32_t)(b >> 32)) << 32) | xor32((uint32_t)b)));
+}
+
 // Workgroups of a launch are dispatched round-robin over the 8 XCDs (id % 8), each with
 // its own L2.  Renumber ids so that XCD x runs one contiguous range of logical ids:
 // neighbouring work items that read the same data then share an L2.

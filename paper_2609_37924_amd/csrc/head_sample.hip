@@ -25,6 +25,8 @@ __device__ __forceinline__ Cand better_cand(Cand a, Cand b) {
 __device__ __forceinline__ Cand shfl_cand(Cand c, int o) {
   return Cand{__shfl_xor(c.score, o, 64), __shfl_xor(c.v, o, 64), __shfl_xor(c.lp, o, 64)};
 }
+__device__ __forceinline__ Cand cand_xor16(Cand c) { return Cand{xor16(c.score), xor16(c.v), xor16(c.lp)}; }
+__device__ __forceinline__ Cand cand_xor32(Cand c) { return Cand{xor32(c.score), xor32(c.v), xor32(c.lp)}; }
 
 template <class T>
 struct Epi<EPI_SAMPLE, T> {
@@ -65,8 +67,8 @@ struct Epi<EPI_SAMPLE, T> {
           lp[a][jj] = (whole || n < p.N) ? cb[a][jj] * e.inv_temp : -INFINITY;
           mx = fmaxf(mx, lp[a][jj]);
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      mx = fmaxf(mx, xor16(mx));
+      mx = fmaxf(mx, xor32(mx));
       // S_g: each rint(exp(l' - m_g) 2^40) <= 2^40 is an integer, so float64 sums of up to
       // 2^13 of them are exact
       double S = 0.0;
@@ -104,15 +106,15 @@ struct Epi<EPI_SAMPLE, T> {
             if (n0 + jj < p.N) entry(lp[a][jj], uniform01(c[jj]), n0 + jj);
         }
       }
-      S += __shfl_xor(S, 16, 64);
-      S += __shfl_xor(S, 32, 64);
-      float amax = fmaxf(a1, __shfl_xor(a1, 16, 64));
-      amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
+      S += xor16(S);
+      S += xor32(S);
+      float amax = fmaxf(a1, xor16(a1));
+      amax = fmaxf(amax, xor32(amax));
       const float delta = 1e-3f + 2.4e-6f * (fabsf(mx) + 32.f);  // screening error bound, x 100
       const float wlo = amax - 2.5f * delta;
       int multi = a2 >= wlo ? 1 : 0;
-      multi |= __shfl_xor(multi, 16, 64);
-      multi |= __shfl_xor(multi, 32, 64);
+      multi |= xor16(multi);
+      multi |= xor32(multi);
       Cand best{-INFINITY, 0x7FFFFFFF, 0.f};
       if (multi) {  // a second entry of some lane is in the window: score the group exactly
 #pragma unroll
@@ -128,8 +130,8 @@ struct Epi<EPI_SAMPLE, T> {
       } else if (a1 >= wlo && v1 < p.N) {
         best = Cand{exact_score_of(lp1, u1), v1, lp1};
       }
-      best = better_cand(best, shfl_cand(best, 16));
-      best = better_cand(best, shfl_cand(best, 32));
+      best = better_cand(best, cand_xor16(best));
+      best = better_cand(best, cand_xor32(best));
       if (fq == 0 && row_ok && nb < p.N) {
         SamplePart r;
         r.m = mx;
