@@ -141,6 +141,10 @@ hipError_t rms_norm_gather(DType dt, const float* x, const float* g, float eps, 
 // LayerNorm with affine; output as T (y_t) or float (y_f), whichever is non-null.
 hipError_t layer_norm(DType dt, const float* x, const float* w, const float* b, float eps,
                       int n_rows, int d, void* y_t, float* y_f, hipStream_t s);
+// x = LayerNorm(x) (affine w, b; in place), then y(T) = RMSNorm(x) * g: a layer_norm followed
+// by rms_norm of its result, with the same arithmetic, in one kernel.
+hipError_t layer_rms_norm(DType dt, float* x, const float* w, const float* b, float ln_eps, const float* g,
+                          float rms_eps, int n_rows, int d, void* y, hipStream_t s);
 hipError_t copy_f32(const float* src, float* dst, size_t n, hipStream_t s);
 hipError_t to_f32(DType dt, const void* src, float* dst, size_t n, hipStream_t s);
 // out[r, f] = act(pre[r, gate_row(f)]) * pre[r, up_row(f)] for the fp32 GLU path.

@@ -128,6 +128,91 @@ __global__ __launch_bounds__(256) void ln_kernel(const float* x, const float* w,
   }
 }
 
+// LayerNorm of x in place (float32), then the RMSNorm of its result into y (the next
+// layer's normalised input): the two kernels' arithmetic in one pass over the row.
+// NV > 0: d <= 256 NV and the row stays in registers; NV = 0: any d, rows re-read.
+template <class T, int NV>
+__global__ __launch_bounds__(256) void ln_rms_kernel(float* x, const float* w, const float* b, float ln_eps,
+                                                     const float* g, float rms_eps, int n_rows, int d, T* y) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= n_rows) return;
+  float* xr = x + (size_t)r * d;
+  T* yr = y + (size_t)r * d;
+  if constexpr (NV > 0) {
+    float4 v[NV];
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane * 4 + 256 * i;
+      v[i] = c < d ? *reinterpret_cast<const float4*>(xr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      s += v[i].x + v[i].y + v[i].z + v[i].w;
+    }
+    const float mu = wave_sum(s) / d;
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (lane * 4 + 256 * i < d) {
+        const float a = v[i].x - mu, bb = v[i].y - mu, cc = v[i].z - mu, dd = v[i].w - mu;
+        ss += a * a + bb * bb + cc * cc + dd * dd;
+      }
+    const float rs = rsqrtf(wave_sum(ss) / d + ln_eps);
+    float sq = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane * 4 + 256 * i;
+      if (c < d) {
+        const float4 ww = *reinterpret_cast<const float4*>(w + c);
+        const float4 bv = *reinterpret_cast<const float4*>(b + c);
+        v[i] = make_float4((v[i].x - mu) * rs * ww.x + bv.x, (v[i].y - mu) * rs * ww.y + bv.y,
+                           (v[i].z - mu) * rs * ww.z + bv.z, (v[i].w - mu) * rs * ww.w + bv.w);
+        *reinterpret_cast<float4*>(xr + c) = v[i];
+      } else {
+        v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      sq += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+    }
+    const float rr = rsqrtf(wave_sum(sq) / d + rms_eps);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane * 4 + 256 * i;
+      if (c < d) {
+        const float4 gg = *reinterpret_cast<const float4*>(g + c);
+        store4(yr + c, v[i].x * rr * gg.x, v[i].y * rr * gg.y, v[i].z * rr * gg.z, v[i].w * rr * gg.w);
+      }
+    }
+  } else {
+    float s = 0.f;
+    for (int c = lane * 4; c < d; c += 256) {
+      const float4 v = *reinterpret_cast<const float4*>(xr + c);
+      s += v.x + v.y + v.z + v.w;
+    }
+    const float mu = wave_sum(s) / d;
+    float ss = 0.f;
+    for (int c = lane * 4; c < d; c += 256) {
+      const float4 v = *reinterpret_cast<const float4*>(xr + c);
+      const float a = v.x - mu, bb = v.y - mu, cc = v.z - mu, dd = v.w - mu;
+      ss += a * a + bb * bb + cc * cc + dd * dd;
+    }
+    const float rs = rsqrtf(wave_sum(ss) / d + ln_eps);
+    float sq = 0.f;
+    for (int c = lane * 4; c < d; c += 256) {
+      const float4 v = *reinterpret_cast<const float4*>(xr + c);
+      const float4 ww = *reinterpret_cast<const float4*>(w + c);
+      const float4 bv = *reinterpret_cast<const float4*>(b + c);
+      const float4 o = make_float4((v.x - mu) * rs * ww.x + bv.x, (v.y - mu) * rs * ww.y + bv.y,
+                                   (v.z - mu) * rs * ww.z + bv.z, (v.w - mu) * rs * ww.w + bv.w);
+      *reinterpret_cast<float4*>(xr + c) = o;
+      sq += o.x * o.x + o.y * o.y + o.z * o.z + o.w * o.w;
+    }
+    const float rr = rsqrtf(wave_sum(sq) / d + rms_eps);
+    for (int c = lane * 4; c < d; c += 256) {  // this lane's own writes above
+      const float4 o = *reinterpret_cast<const float4*>(xr + c);
+      const float4 gg = *reinterpret_cast<const float4*>(g + c);
+      store4(yr + c, o.x * rr * gg.x, o.y * rr * gg.y, o.z * rr * gg.z, o.w * rr * gg.w);
+    }
+  }
+}
+
 __global__ void copy_kernel(const float4* src, float4* dst, size_t n4) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n4) dst[i] = src[i];
@@ -212,6 +297,24 @@ hipError_t layer_norm(DType dt, const float* x, const float* w, const float* b, 
   else
     hipLaunchKernelGGL(ln_kernel<float>, dim3(blocks(n_rows, 4)), dim3(256), 0, s, x, w, b, eps, n_rows,
                        d, static_cast<float*>(y_t), y_f);
+  return hipGetLastError();
+}
+
+hipError_t layer_rms_norm(DType dt, float* x, const float* w, const float* b, float ln_eps, const float* g,
+                          float rms_eps, int n_rows, int d, void* y, hipStream_t s) {
+  if (n_rows == 0) return hipSuccess;
+  const dim3 grid(blocks(n_rows, 4));
+  if (dt == BF16) {
+    if (d <= 1024)
+      hipLaunchKernelGGL((ln_rms_kernel<bf16, 4>), grid, dim3(256), 0, s, x, w, b, ln_eps, g, rms_eps, n_rows, d,
+                         static_cast<bf16*>(y));
+    else
+      hipLaunchKernelGGL((ln_rms_kernel<bf16, 0>), grid, dim3(256), 0, s, x, w, b, ln_eps, g, rms_eps, n_rows, d,
+                         static_cast<bf16*>(y));
+  } else {
+    hipLaunchKernelGGL((ln_rms_kernel<float, 0>), grid, dim3(256), 0, s, x, w, b, ln_eps, g, rms_eps, n_rows, d,
+                       static_cast<float*>(y));
+  }
   return hipGetLastError();
 }
 

@@ -447,14 +447,16 @@ struct KVTarget {
   int cap, off;
 };
 
-static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int pos0, KVTarget kv) {
+// One pre-norm layer on x [N, d]; prenormed: ws.xn already holds the attention norm of x.
+static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int pos0, KVTarget kv,
+                             bool prenormed = false) {
   const tadm_config& c = m->cfg;
   const LayerIdx& w = m->lay.layers[li];
   Workspace& s = m->ws;
   const int N = B * L, d = c.d_model, H = c.n_heads, Hk = c.n_kv_heads, dh = c.head_dim,
             F = c.d_ffn;
   const hipStream_t st = m->stream;
-  HIPCHK(rms_norm(m->dt, x, m->Wf(w.attn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
+  if (!prenormed) HIPCHK(rms_norm(m->dt, x, m->Wf(w.attn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
   {
     // q/k/v projection with the rotary embedding and head split in the epilogue
     GemmProblem p{N, (H + 2 * Hk) * dh, d, s.xn, d, d, nullptr, 0, m->W(w.wqkv), d};
@@ -536,9 +538,11 @@ static KVTarget kv_target(tadm_model* m, const tadm_context* ctx, int li) {
   return KVTarget{m->ws.k, m->ws.vt, m->ws.kv_cap, 0};
 }
 
+// prenormed: ws.xn already holds the first layer's attention norm of x
 static tadm_status run_part(tadm_model* m, int first, int count, float* x, int B, int L, int pos0,
-                            const tadm_context* ctx) {
-  for (int li = first; li < first + count; ++li) TRY(run_layer(m, li, x, B, L, pos0, kv_target(m, ctx, li)));
+                            const tadm_context* ctx, bool prenormed = false) {
+  for (int li = first; li < first + count; ++li)
+    TRY(run_layer(m, li, x, B, L, pos0, kv_target(m, ctx, li), prenormed && li == first));
   return TADM_OK;
 }
 
@@ -698,8 +702,12 @@ static tadm_status anchor_net(tadm_model* m, const tadm_context* ctx, int B, int
 }
 
 // h~ = Phi(c, cache) into ws.x.
-static tadm_status fusion(tadm_model* m, int B, int L, const float* c, const tadm_cache* cache) {
+// h~ = Phi(c, h') into ws.x.  With the gated MLP fusion and denoiser layers, its closing
+// LayerNorm also writes the first denoiser layer's attention norm to ws.xn (*prenormed).
+static tadm_status fusion(tadm_model* m, int B, int L, const float* c, const tadm_cache* cache,
+                          bool* prenormed) {
   const tadm_config& cf = m->cfg;
+  *prenormed = false;
   if (cf.fusion_kind == TADM_FUSION_PAIRED) return paired_fuse(m, B, L, c, cache);
   Workspace& s = m->ws;
   const int N = B * L, d = cf.d_model;
@@ -733,7 +741,13 @@ static tadm_status fusion(tadm_model* m, int B, int L, const float* c, const tad
     HIPCHK(gemm(m->dt, p, EPI_FUSION2, e, st));
     TRY(prof_end(m, TADM_STAGE_FUSION2));
   }
-  HIPCHK(layer_norm(m->dt, s.x, m->Wf(Y.ln_o_w), m->Wf(Y.ln_o_b), cf.ln_eps, N, d, nullptr, s.x, st));
+  if (cf.n_denoise > 0) {
+    const float* g0 = m->Wf(Y.layers[cf.n_shared + cf.n_anchor].attn_norm);
+    HIPCHK(layer_rms_norm(m->dt, s.x, m->Wf(Y.ln_o_w), m->Wf(Y.ln_o_b), cf.ln_eps, g0, cf.rms_eps, N, d, s.xn, st));
+    *prenormed = true;
+  } else {
+    HIPCHK(layer_norm(m->dt, s.x, m->Wf(Y.ln_o_w), m->Wf(Y.ln_o_b), cf.ln_eps, N, d, nullptr, s.x, st));
+  }
   return TADM_OK;
 }
 
@@ -1062,8 +1076,9 @@ static tadm_status context_append_impl(tadm_model* m, tadm_context* ctx, const i
   Workspace& s = m->ws;
   TRY(shared_net(m, ctx, tok, B, n, s.c));
   TRY(anchor_net(m, ctx, B, n, s.c, scratch));
-  TRY(fusion(m, B, n, s.c, scratch));
-  TRY(run_part(m, m->cfg.n_shared + m->cfg.n_anchor, m->cfg.n_denoise, s.x, B, n, ctx->len, ctx));
+  bool prenormed;
+  TRY(fusion(m, B, n, s.c, scratch, &prenormed));
+  TRY(run_part(m, m->cfg.n_shared + m->cfg.n_anchor, m->cfg.n_denoise, s.x, B, n, ctx->len, ctx, prenormed));
   ctx->len += n;
   return TADM_OK;
 }
@@ -1210,13 +1225,14 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
   TRY(shared_net(m, ctx, canvas, B, L, s.c, entropy ? a->sc_in : nullptr, off));
   TRY(prof_end(m, TADM_STAGE_EMBED));
   TRY(prof_begin(m, TADM_STAGE_FUSION));
-  TRY(fusion(m, B, L, s.c, cache));
+  bool prenormed;
+  TRY(fusion(m, B, L, s.c, cache, &prenormed));
   TRY(prof_end(m, TADM_STAGE_FUSION));
   if (m->taps) HIPCHK(copy_f32(s.x, s.ht, (size_t)B * L * d, m->stream));
   const bool full = logits != nullptr, all_rows = full || entropy;
   const int rows = all_rows ? B * Lc : std::min(max_masked, B * Lc);
   TRY(prof_begin(m, TADM_STAGE_DENOISE));
-  TRY(run_part(m, cf.n_shared + cf.n_anchor, cf.n_denoise, s.x, B, L, pos0, ctx));
+  TRY(run_part(m, cf.n_shared + cf.n_anchor, cf.n_denoise, s.x, B, L, pos0, ctx, prenormed));
   if (all_rows) {
     HIPCHK(rms_norm(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, B * Lc, d, Lc, L, off, s.xn, m->stream));
   } else {
@@ -1535,10 +1551,11 @@ tadm_status tadm_train_loss(tadm_model* m, const int32_t* x_dev, int32_t B, int3
   TRY(shared_net(m, nullptr, zt, B, L, s.c));
   TRY(prof_end(m, TADM_STAGE_EMBED));
   TRY(prof_begin(m, TADM_STAGE_FUSION));
-  TRY(fusion(m, B, L, s.c, cache));
+  bool prenormed;
+  TRY(fusion(m, B, L, s.c, cache, &prenormed));
   TRY(prof_end(m, TADM_STAGE_FUSION));
   TRY(prof_begin(m, TADM_STAGE_DENOISE));
-  TRY(run_part(m, cf.n_shared + cf.n_anchor, cf.n_denoise, s.x, B, L, 0, nullptr));
+  TRY(run_part(m, cf.n_shared + cf.n_anchor, cf.n_denoise, s.x, B, L, 0, nullptr, prenormed));
   HIPCHK(compact_masked(zt, B, L, 0, mask, s.cidx, s.row_map, s.count, m->stream));
   HIPCHK(rms_norm_gather(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, s.cidx, s.count, N, L, L, 0, d, s.xn,
                          m->stream));
