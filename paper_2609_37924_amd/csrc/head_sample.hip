@@ -201,9 +201,9 @@ __global__ __launch_bounds__(256) void finalize_kernel(const SamplePart* part, i
 
 hipError_t head_sample(const GemmProblem& p, const EpiParams& e, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
-  // 128 x 128 tiles on 2 x 2 waves (64-column wave strips), two blocks per CU: one
-  // block's VALU-heavy epilogue overlaps the other's MFMA main loop
-  return launch_bf16<128, 128, 2, 2, 2, 2, EPI_SAMPLE>(p, e, s);
+  // 128 x 64 tiles on 4 x 1 waves (64-column wave strips), three blocks per CU (48 KB of
+  // LDS each): a block's VALU-heavy epilogue overlaps the others' MFMA main loops
+  return launch_bf16<128, 64, 2, 4, 1, 3, EPI_SAMPLE>(p, e, s);
 }
 
 hipError_t sample_finalize(const SamplePart* part, int n_groups, int V, const int32_t* row_map,
