@@ -103,25 +103,36 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
   const int lrow = lane >> 3, lchunk = (lane & 7) ^ (lane >> 3);
 
   const int nk = p.K / 64 / p.ksplit, kt_base = blockIdx.y * nk;  // this block's K slice
+  // this lane's source rows, fixed over the K loop: a K tile only adds its offset.  A
+  // second operand A2 (K columns from K1 on) gets its own row pointers, shifted by -K1.
+  const bf16* arow1[LA];
+  const bf16* arow2[LA];
+  const bf16* wrow[LW];
+#pragma unroll
+  for (int j = 0; j < LA; ++j) {
+    const int r = min(m0 + (wave + NW * j) * 8 + lrow, p.M - 1);
+    arow1[j] = A1 + (size_t)r * p.lda1 + lchunk * 8;
+    arow2[j] = A2 ? A2 + (size_t)r * p.lda2 + lchunk * 8 - p.K1 : arow1[j];
+  }
+#pragma unroll
+  for (int j = 0; j < LW; ++j) {
+    const int r = min(n0 + (wave + NW * j) * 8 + lrow, p.N - 1);
+    wrow[j] = W + (size_t)r * p.ldw + lchunk * 8;
+  }
   auto issue = [&](int kt, int buf) {
     const int k0 = (kt_base + kt) * 64;
-    const bf16* Ab = A1;
-    int lda = p.lda1, kk = k0;
-    if (k0 >= p.K1) { Ab = A2; lda = p.lda2; kk = k0 - p.K1; }
+    const bool second = k0 >= p.K1;
     char* sb = smem + buf * STAGE_BYTES;
 #pragma unroll
     for (int j = 0; j < LA; ++j) {
-      const int g = wave + NW * j;              // 8-row group
-      const int r = min(m0 + g * 8 + lrow, p.M - 1);
-      const bf16* src = Ab + (size_t)r * lda + kk + lchunk * 8;
+      const int g = wave + NW * j;  // 8-row group
+      const bf16* src = (second ? arow2[j] : arow1[j]) + k0;
       __builtin_amdgcn_global_load_lds((gbl_ptr)src, (lds_ptr)(sb + g * 1024), 16, 0, 0);
     }
 #pragma unroll
     for (int j = 0; j < LW; ++j) {
       const int g = wave + NW * j;
-      const int r = min(n0 + g * 8 + lrow, p.N - 1);
-      const bf16* src = W + (size_t)r * p.ldw + k0 + lchunk * 8;
-      __builtin_amdgcn_global_load_lds((gbl_ptr)src, (lds_ptr)(sb + BM * ROW + g * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((gbl_ptr)(wrow[j] + k0), (lds_ptr)(sb + BM * ROW + g * 1024), 16, 0, 0);
     }
   };
 
