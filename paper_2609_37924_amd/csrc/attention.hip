@@ -76,7 +76,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
   constexpr int LPT = LK + LV;                                      // per wave per tile
   __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, grp = lane >> 4, fr = lane & 15;
+  // wave index as a scalar: the K/V tile destinations in LDS are formed in scalar registers
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), grp = lane >> 4,
+            fr = lane & 15;
   // one block per (64-query tile, head, batch row), query tiles fastest: the tiles of a
   // head, and the heads sharing a K/V head, run on one XCD and read K/V from its L2
   const int nqt = (Lq + 63) / 64;

@@ -84,7 +84,9 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
   static_assert(WTN % 32 == 0, "GLU pairs need 32-row weight blocks per wave");
   __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE_BYTES];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index as a wave-uniform (scalar) value: LDS destinations of the tile loads are
+  // then formed in scalar registers
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % WGM, wn = wave / WGM;
   const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
   int tmi, tni;
