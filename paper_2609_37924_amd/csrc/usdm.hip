@@ -60,11 +60,35 @@ __global__ __launch_bounds__(256) void entropy_kernel(const float* logits, int V
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float* lg = logits + (size_t)row * V;
 
-  // argmax of the raw logits, smallest index among equal maxima
+  // argmax of the raw logits, smallest index among equal maxima (each thread's entries in
+  // increasing order, so a strict > keeps its smallest; float4 granules when V % 4 == 0,
+  // four of them in flight)
+  const bool vec = (V & 3) == 0;  // whole float4 granules (then ldp % 4 == 0 too)
   Best am{-INFINITY, 0x7FFFFFFF};
-  for (int v = tid; v < V; v += 256) {
-    const float x = lg[v];
-    if (x > am.score) am = Best{x, v};
+  if (vec) {
+    const int nq = V >> 2;
+    for (int q0 = tid; q0 < nq; q0 += 4 * 256) {
+      float4 x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int q = q0 + 256 * u;
+        x[u] = q < nq ? *reinterpret_cast<const float4*>(lg + 4 * q)
+                      : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int v = 4 * (q0 + 256 * u);
+        if (x[u].x > am.score) am = Best{x[u].x, v};
+        if (x[u].y > am.score) am = Best{x[u].y, v + 1};
+        if (x[u].z > am.score) am = Best{x[u].z, v + 2};
+        if (x[u].w > am.score) am = Best{x[u].w, v + 3};
+      }
+    }
+  } else {
+    for (int v = tid; v < V; v += 256) {
+      const float x = lg[v];
+      if (x > am.score) am = Best{x, v};
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) am = better(am, Best{__shfl_xor(am.score, o, 64), __shfl_xor(am.v, o, 64)});
@@ -78,9 +102,10 @@ __global__ __launch_bounds__(256) void entropy_kernel(const float* logits, int V
   if (am.v >= V) am.v = 0;  // only with non-finite logits
   const float m = lg[am.v] * inv_temp;  // max l' (rounding is monotone)
 
-  long long A = 0, Bs = 0;
+  // A and B as float64 sums of their integer terms (each < 2^41, at most 2^8 of them per
+  // thread): exact, then converted once
+  double Ad = 0.0, Bd = 0.0;
   Top2 top;
-  const bool vec = (V & 3) == 0;  // whole float4 granules (then ldp % 4 == 0 too)
   for (int q = tid; 4 * q < V; q += 256) {
     float l[4];
     if (vec) {
@@ -102,9 +127,14 @@ __global__ __launch_bounds__(256) void entropy_kernel(const float* logits, int V
       const float y = lp - m;
       const float ex = own_exp(y);
       w[e] = ex;
-      A += (long long)rintf(ex * TWO40);
-      if (ex > 0.f) Bs += (long long)rintf(((-y) * ex) * TWO40);
-      top.add(screen_score(lp, uniform01(c[e])), v);
+      Ad += (double)rintf(ex * TWO40);
+      Bd += ex > 0.f ? (double)rintf(((-y) * ex) * TWO40) : 0.0;
+      // the running top two, by selects
+      const float sc = screen_score(lp, uniform01(c[e]));
+      const bool t1 = sc > top.a1;
+      top.a2 = t1 ? top.a1 : fmaxf(top.a2, sc);
+      top.v1 = t1 ? v : top.v1;
+      top.a1 = t1 ? sc : top.a1;
     }
     if (P) {
       PT* dst = P + (size_t)row * ldp + 4 * q;
@@ -116,6 +146,7 @@ __global__ __launch_bounds__(256) void entropy_kernel(const float* logits, int V
   }
   if (P)
     for (int v = V + tid; v < ldp; v += 256) store_weight(P + (size_t)row * ldp + v, 0.f);
+  long long A = (long long)Ad, Bs = (long long)Bd;
   float amax = top.a1;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
