@@ -115,9 +115,11 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
 #pragma unroll
       for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
       long long sg = 0;
-      if (g < ng) {
+      if (g < ng) {  // four integer terms below 2^41: exact in float64, converted once
+        double sd = 0.0;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) sg += (long long)rintf(own_exp(lp[e] - mx) * 1099511627776.0f);  // * 2^40
+        for (int e = 0; e < 4; ++e) sd += (double)rintf(own_exp(lp[e] - mx) * 1099511627776.0f);  // * 2^40
+        sg = (long long)sd;
       }
 #pragma unroll
       for (int o = 1; o < 16; o <<= 1) sg += __shfl_xor(sg, o, 64);

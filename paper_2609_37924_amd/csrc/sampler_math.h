@@ -135,14 +135,11 @@ __device__ __forceinline__ float screen_score(float lp, float u) {
 struct Top2 {
   float a1 = -INFINITY, a2 = -INFINITY;
   int v1 = 0x7FFFFFFF;
-  __device__ __forceinline__ void add(float a, int v) {
-    if (a > a1) {
-      a2 = a1;
-      a1 = a;
-      v1 = v;
-    } else if (a > a2) {
-      a2 = a;
-    }
+  __device__ __forceinline__ void add(float a, int v) {  // by selects: no divergent branches
+    const bool t = a > a1;
+    a2 = t ? a1 : fmaxf(a2, a);
+    v1 = t ? v : v1;
+    a1 = t ? a : a1;
   }
 };
 
