@@ -167,31 +167,27 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
         s[ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kc], s[ks], 0, 0, 0);
       }
     }
-    // s[ks][j] = score(query lane&15, key t*64 + ks*16 + 4*grp + j)
+    // s[ks][j] = score(query lane&15, key t*64 + ks*16 + 4*grp + j), unscaled: the
+    // softmax runs in base 2 on s * scale_log2, the scale folded into one FMA per score
     float mt = -INFINITY;
     if ((t + 1) * KT <= Lk) {  // a whole tile: no key is masked
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float v = s[ks][j] * scale_log2;
-          s[ks][j] = v;
-          mt = fmaxf(mt, v);
-        }
+        for (int j = 0; j < 4; ++j) mt = fmaxf(mt, s[ks][j]);
     } else {
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int key = t * KT + ks * 16 + 4 * grp + j;
-          const float v = key < Lk ? s[ks][j] * scale_log2 : -INFINITY;
-          s[ks][j] = v;
-          mt = fmaxf(mt, v);
+          if (key >= Lk) s[ks][j] = -INFINITY;
+          mt = fmaxf(mt, s[ks][j]);
         }
     }
     mt = fmaxf(mt, xor16(mt));
     mt = fmaxf(mt, xor32(mt));
-    const float m_new = fmaxf(m_run, mt);
+    const float m_new = fmaxf(m_run, mt * scale_log2);  // scale_log2 > 0: the max commutes
     // raw v_exp_f32: results below 2^-126 flush to 0 (a probability that small adds nothing)
     const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
     float ps = 0.f;
@@ -199,7 +195,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
     for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float p = __builtin_amdgcn_exp2f(s[ks][j] - m_new);
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[ks][j], scale_log2, -m_new));
         s[ks][j] = p;
         ps += p;
       }
