@@ -3,6 +3,8 @@
 Each test fixes weights so that the module reduces to a closed form stated by the
 paper (zero-initialised output projection, C = C0) or to library routines.
 """
+import math
+
 import numpy as np
 import torch
 import torch.nn.functional as F
@@ -140,3 +142,149 @@ def test_paired_matches_library_formulation():
     ref = H0 + g * sH * F.linear(M, Wt["fusion.w_up"])
     out = N.fusion_paired(W, C.numpy(), C0.numpy(), H0.numpy())
     np.testing.assert_allclose(out, ref.numpy(), rtol=1e-9, atol=1e-11)
+
+
+# ---------------------------------------------------------------------------
+# Pins with every fusion weight and bias non-zero.  The reference formulations below
+# are written with torch's library ops (F.linear with its bias, F.gelu, F.silu,
+# F.layer_norm, F.rms_norm, scaled_dot_product_attention, torch.cat in the order the
+# appendix prints), so a swapped concatenation, a wrong activation or a dropped bias
+# in the oracle makes them disagree.
+
+def _paired_all_random():
+    """Seeded weights with the gate MLP and the mixer FFN scaled up (std 0.02 -> 0.5), so
+    that at this small width both change the result by far more than the tolerance."""
+    cfg, W = _paired()
+    for k in ("fusion.w_g1", "fusion.w_g2", "fusion.w_f1", "fusion.w_f2"):
+        W.t[k] *= 25.0
+        assert np.count_nonzero(W[k]) == W[k].size
+    assert W["fusion.b_g"][0] != -3.0  # perturbed away from the paper's -3
+    return cfg, W
+
+
+def _paired_reference(W, C, C0, H0):
+    """App. C.1 written with library ops: s_C, s_H token-wise RMS of the cached C0, H0;
+    Z = (C/s_C) W_C, Z0 = (C0/s_C) W_C, U = (H0/s_H) W_H; J = [Z, U];
+    R = Z + MHA(J W_Q, J W_K, J W_V) W_O; phi = R + SiLU(R W_1) W_2;
+    M = phi(Z, U) - phi(Z0, U); F = [U; Z0; Z - Z0; M];
+    g = sigmoid(SiLU(F W_g1) W_g2 + b_g); H~ = H0 + g s_H (M W_up)."""
+    cfg = W.cfg
+    d, r, nh, eps = cfg["d_model"], cfg["fusion_rank"], cfg["paired_heads"], cfg["rms_eps"]
+    Wt = {k: T(v) for k, v in W.t.items()}
+    C, C0, H0 = T(C), T(C0), T(H0)
+    L = C.shape[0]
+    sC = torch.sqrt(torch.mean(C0 ** 2, -1, keepdim=True) + eps)
+    sH = torch.sqrt(torch.mean(H0 ** 2, -1, keepdim=True) + eps)
+    Z = F.linear(C / sC, Wt["fusion.w_c"])
+    Z0 = F.linear(F.rms_norm(C0, (d,), eps=eps), Wt["fusion.w_c"])
+    U = F.linear(F.rms_norm(H0, (d,), eps=eps), Wt["fusion.w_h"])
+
+    def phi(Zx):
+        J = torch.cat([Zx, U], dim=-1)
+        q, k, v = (F.linear(J, Wt[f"fusion.w_{n}"]).view(L, nh, r // nh).transpose(0, 1) for n in "qkv")
+        att = F.scaled_dot_product_attention(q, k, v).transpose(0, 1).reshape(L, r)
+        R = Zx + F.linear(att, Wt["fusion.w_o"])
+        return R + F.linear(F.silu(F.linear(R, Wt["fusion.w_f1"])), Wt["fusion.w_f2"])
+
+    M = phi(Z) - phi(Z0)
+    Fcat = torch.cat([U, Z0, Z - Z0, M], dim=-1)
+    g = torch.sigmoid(F.linear(F.silu(F.linear(Fcat, Wt["fusion.w_g1"])), Wt["fusion.w_g2"], Wt["fusion.b_g"]))
+    return (H0 + g * sH * F.linear(M, Wt["fusion.w_up"])).numpy(), g.numpy(), M, (U, Z0, Z - Z0)
+
+
+def test_paired_all_weights_nonzero_matches_library_formulation():
+    cfg, W = _paired_all_random()
+    d = cfg["d_model"]
+    C, C0, H0 = rng.normal(size=(12, d)), rng.normal(size=(12, d)), rng.normal(size=(12, d)) * 2
+    ref, g, _, _ = _paired_reference(W, C, C0, H0)
+    # the gate is a genuine function of the token here, not a constant
+    assert g.std() > 1e-3
+    np.testing.assert_allclose(N.fusion_paired(W, C, C0, H0), ref, rtol=1e-9, atol=1e-11)
+
+
+def test_paired_zero_gate_output_layer_gives_bias_gate():
+    """W_g2 = 0 => g = sigmoid(b_g) for every token, whatever W_g1 and F are."""
+    cfg, W = _paired_all_random()
+    d = cfg["d_model"]
+    W.t["fusion.w_g2"][:] = 0.0
+    C, C0, H0 = rng.normal(size=(12, d)), rng.normal(size=(12, d)), rng.normal(size=(12, d))
+    _, _, M, _ = _paired_reference(W, C, C0, H0)
+    sH = np.sqrt(np.mean(H0 ** 2, -1, keepdims=True) + cfg["rms_eps"])
+    g = 1.0 / (1.0 + np.exp(-W["fusion.b_g"][0]))
+    ref = H0 + g * sH * (M.numpy() @ W["fusion.w_up"].T)
+    np.testing.assert_allclose(N.fusion_paired(W, C, C0, H0), ref, rtol=1e-9, atol=1e-11)
+
+
+def test_paired_zero_mixer_output_gives_residual_branch():
+    """W_f2 = 0 => phi(Z, U) = R = Z + MHA(.) W_O: the result equals the formulation
+    whose mixer stops at R, with W_f1 left non-zero."""
+    cfg, W = _paired_all_random()
+    d = cfg["d_model"]
+    W.t["fusion.w_f2"][:] = 0.0
+    C, C0, H0 = rng.normal(size=(12, d)), rng.normal(size=(12, d)), rng.normal(size=(12, d))
+    ref, _, _, _ = _paired_reference(W, C, C0, H0)
+    W2 = N.Weights(cfg, [], [])
+    W2.t = {k: v.copy() for k, v in W.t.items()}
+    W2.t["fusion.w_f1"][:] = 0.0  # with W_f2 = 0, W_f1 must not matter
+    np.testing.assert_allclose(N.fusion_paired(W, C, C0, H0), N.fusion_paired(W2, C, C0, H0), rtol=0, atol=1e-13)
+    np.testing.assert_allclose(N.fusion_paired(W, C, C0, H0), ref, rtol=1e-9, atol=1e-11)
+
+
+def test_paired_gate_reads_the_four_blocks_in_order():
+    """W_g1 selects one r-wide block of F = [U; Z0; Z - Z0; M] (identity on that block,
+    zero elsewhere) and W_g2 = 1/r: then g = sigmoid(mean(SiLU(block)) + b_g), with the
+    block computed from its own definition.  Each block gives a different gate, so an
+    oracle that concatenates in another order fails."""
+    cfg, W = _paired_all_random()
+    d, r, eps = cfg["d_model"], cfg["fusion_rank"], cfg["rms_eps"]
+    C, C0, H0 = rng.normal(size=(12, d)), rng.normal(size=(12, d)), rng.normal(size=(12, d))
+    _, _, M, (U, Z0, dZ) = _paired_reference(W, C, C0, H0)
+    blocks = [U.numpy(), Z0.numpy(), dZ.numpy(), M.numpy()]
+    sH = np.sqrt(np.mean(H0 ** 2, -1, keepdims=True) + eps)
+    MWup = M.numpy() @ W["fusion.w_up"].T
+    gates = []
+    for j, blk in enumerate(blocks):
+        W.t["fusion.w_g1"][:] = 0.0
+        W.t["fusion.w_g1"][:, j * r:(j + 1) * r] = np.eye(r)
+        W.t["fusion.w_g2"][:] = 1.0 / r
+        silu = blk / (1.0 + np.exp(-blk))
+        g = 1.0 / (1.0 + np.exp(-(silu.mean(-1, keepdims=True) + W["fusion.b_g"][0])))
+        gates.append(g)
+        np.testing.assert_allclose(N.fusion_paired(W, C, C0, H0), H0 + g * sH * MWup, rtol=1e-9, atol=1e-11)
+    for a in range(4):
+        for b in range(a + 1, 4):
+            assert np.abs(gates[a] - gates[b]).max() > 1e-4
+
+
+def test_gated_all_weights_nonzero_matches_library_formulation():
+    """App. C.2 with every weight and bias non-zero (b1, b2, b_g, LN gains and biases
+    perturbed), against F.layer_norm / F.linear with bias / F.gelu / torch.sigmoid."""
+    cfg, W = _weights("tiny")
+    d = cfg["d_model"]
+    assert np.abs(W["fusion.b1"]).max() > 0.05 and np.abs(W["fusion.b2"]).max() > 0.05
+    Wt = {k: T(v) for k, v in W.t.items()}
+    c, h = rng.normal(size=(9, d)), rng.normal(size=(9, d)) * 2
+    u = torch.cat([_ln(W, c, "ln_s"), _ln(W, h, "ln_a")], dim=-1)
+    g = torch.sigmoid(F.linear(u, Wt["fusion.wg"], Wt["fusion.bg"]))
+    delta = F.linear(F.gelu(F.linear(u, Wt["fusion.w1"], Wt["fusion.b1"])), Wt["fusion.w2"], Wt["fusion.b2"])
+    ref = _ln(W, T(h) + g * delta, "ln_o")
+    np.testing.assert_allclose(N.fusion_gated_mlp(W, c, h), ref.numpy(), rtol=1e-11, atol=1e-12)
+
+
+def test_gated_hidden_bias_enters_before_the_gelu():
+    """W1 = 0, open gate: the hidden state is GELU(b1) for every token, so
+    h~ = LN_o(h + W2 GELU(b1) + b2).  A dropped b1 (GELU(0) = 0) or a b1 added after
+    the GELU gives a different value."""
+    cfg, W = _weights("tiny")
+    d = cfg["d_model"]
+    W.t["fusion.w1"][:] = 0.0
+    W.t["fusion.wg"][:] = 0.0
+    W.t["fusion.bg"][:] = 1e4
+    c, h = rng.normal(size=(9, d)), rng.normal(size=(9, d))
+    b1 = W["fusion.b1"]
+    hid = 0.5 * b1 * (1.0 + np.vectorize(math.erf)(b1 / math.sqrt(2.0)))
+    delta = W["fusion.w2"] @ hid + W["fusion.b2"]
+    ref = _ln(W, T(h + delta[None, :]), "ln_o").numpy()
+    np.testing.assert_allclose(N.fusion_gated_mlp(W, c, h), ref, rtol=1e-11, atol=1e-12)
+    wrong = _ln(W, T(h + (W["fusion.w2"] @ (hid * 0) + W["fusion.b2"])[None, :]), "ln_o").numpy()
+    assert np.abs(wrong - ref).max() > 1e-3
