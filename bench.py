@@ -38,12 +38,16 @@ PEAK_HBM_GBS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", default="small")
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="26b",
+                    help="workload: 26b (default, the largest that fits one GPU), 1b, block, small, tiny")
     ap.add_argument("--K", type=int, default=4, help="headline refresh interval")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-sweep", action="store_true", help="only the headline K")
+    ap.add_argument("--extras", action="store_true",
+                    help="also time the remasking, loop and entropy-bound samplers and the training forward")
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work in the CPU sample")
     ap.add_argument("--out", default=None, help="also write the JSON line to this file")
     ap.add_argument("--render-stats", metavar="DIR", default=None,
                     help="print a markdown summary of the rocprofv3 --stats output under DIR and exit")
@@ -299,67 +303,140 @@ def cpu_model():
 
 
 def cpu_baseline(cfg, K, budget_s=10.0):
-    """The oracle on whole rows of the workload's first block, one row at a time until
-    about budget_s seconds have passed: each row runs one refresh cycle (the first K
-    reverse steps: one refresh step, K - 1 stale steps), each step timed.  The mean
-    refresh and stale step times are scaled to the whole job: rows x blocks x
-    (ceil(T/K) refresh + the other stale steps).  Context prefill of block mode is not
-    part of the sample."""
+    """The oracle's own Algorithm 1 (oracle.loop.generate) on whole rows of the workload,
+    one row after another until about budget_s seconds have passed (at least one row):
+    complete generations, nothing extrapolated.  Rows are independent, so the rate of
+    the rows run is the job's rate.  Workloads whose full generation of one row fits
+    the budget at every refresh interval (the tiny one) also get each interval's rate."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     import synth
-    from oracle import loop, network as N, sampler as S
+    from oracle import loop, network as N
 
     specs = synth.weight_specs(cfg)
-    need = sum(int(np.prod([d for d in sp[1] if d])) for sp in specs) * 8
-    if need > 64e9:
-        raise RuntimeError(f"the oracle's float64 weights would need {need / 1e9:.0f} GB of host memory")
     print("[bench] cpu baseline: building the oracle's float64 weights", file=sys.stderr, flush=True)
     tensors = synth.make_weights(cfg)
     net = N.Network(N.Weights(cfg, [s[0] for s in specs], tensors))
     del tensors
     B, P, G, T, bl = cfg["batch"], cfg["prompt_len"], cfg["gen_len"], cfg["T"], cfg["block_len"]
-    single = bl == G
-    mask = synth.mask_id(cfg)
     prompts = synth.make_prompt(cfg).numpy() if P else np.zeros((B, 0), dtype=np.int64)
-    t_ref, t_stale = [], []
-    t_start = time.perf_counter()
-    rows = 0
-    for r in range(B):
-        if single:
-            seq = np.concatenate([prompts[r], np.full(G, mask)])
-            pos, off, ctx = np.arange(P + G), P, None
-        else:  # first block after the prompt; the prompt context is built outside the timing
-            seq = np.full(bl, mask)
-            pos, off = np.arange(P, P + bl), 0
-            ctx = net.fresh_kv(prompts[r], np.arange(P))
-        cache = None
-        for k in range(min(K, T)):
-            i = T - k
-            t0 = time.perf_counter()
-            c = net.shared(seq, pos, ctx)
-            if k == 0:
-                cache = net.anchor_cache(c, pos, ctx)
-            xf = net.denoise(net.fuse(c, cache), pos, ctx)
-            lg = net.head(xf[off:]).astype(np.float32)
-            seq[off:], _, _ = S.reverse_step(lg, seq[off:], mask, loop.unmask_count(bl, i, T), pos[0] + off, r,
-                                             T - i, cfg["sampler_seed"], np.float32(1.0))
-            (t_ref if k == 0 else t_stale).append(time.perf_counter() - t0)
-        rows += 1
-        if time.perf_counter() - t_start >= budget_s:
-            break
-    tr = float(np.mean(t_ref))
-    ts = float(np.mean(t_stale)) if t_stale else tr
-    n_ref = math.ceil(T / K)
-    job_s = B * (G // bl) * (n_ref * tr + (T - n_ref) * ts)
+
+    def rate(Kx):
+        t_start = time.perf_counter()
+        rows = 0
+        for r in range(B):
+            loop.generate(net, prompts[r:r + 1], G, T, Kx, bl, cfg["sampler_seed"], cfg["temperature"],
+                          synth.mask_id(cfg))
+            rows += 1
+            if time.perf_counter() - t_start >= budget_s:
+                break
+        el = time.perf_counter() - t_start
+        return rows * G / el, rows, el
+
+    value, rows, el = rate(K)
+    per_k = None
+    if el / rows * len(cfg["Ks"]) < budget_s:
+        per_k = {f"K={Kx}": rate(Kx)[0] for Kx in cfg["Ks"]}
     threads = max([t.get("num_threads", 1) for t in threadpool_info()] + [1])
-    return {"value": B * G / job_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+    return {"value": value, "unit": "tokens/s", "cores": threads, "kind": "oracle", "extrapolated": False,
             "cpu_model": cpu_model(), "host_cpus_available": len(os.sched_getaffinity(0)),
-            "sample": f"{rows} of {B} rows, first block, one refresh cycle each (1 refresh step, mean "
-                      f"{tr:.2f} s; {min(K, T) - 1} stale steps, mean {ts:.2f} s) at the full shape, "
-                      f"{time.perf_counter() - t_start:.1f} s in all; scaled to rows x blocks x ({n_ref} refresh + "
-                      f"{T - n_ref} stale steps) per block, context prefill excluded"}
+            "k_sweep": per_k,
+            "sample": f"{rows} of {B} rows, each a complete generation by the oracle's Algorithm 1 at K={K} "
+                      f"({G} positions, T={T}), {el:.1f} s in all; rate of those rows (rows are independent)"}
+
+
+STREAM_HEAD_ROWS = 16384  # vocabulary rows of the head in the streamed sample
+
+
+def cpu_baseline_streamed(cfg, K, tensors, budget_s=20.0):
+    """The oracle on a bounded sample of a workload whose float64 weights do not fit
+    (or take minutes to build on) the host: one transformer layer (the first anchor
+    layer, at the real per-row shape of one call: one block, or the whole canvas, with
+    its context keys), the fusion module, the vocabulary head on its first
+    STREAM_HEAD_ROWS rows and the reverse step on a few masked positions, each timed by
+    itself on one batch row.  A whole generation is then extrapolated from those times
+    over Algorithm 1's schedule: per block, ceil(T/K) refresh steps (anchor layers) and
+    T steps of denoiser layers, fusion, head and sampler over the positions still
+    masked, the prompt prefill and block appends as fresh passes; times the batch
+    (rows are independent).  Layer times are taken at the first block's context length;
+    the embedding gather is not timed.  The result is labelled as extrapolated."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import synth
+    from oracle import network as N, sampler as S
+
+    B, P, G, T, bl, V, d = (cfg[k] for k in ("batch", "prompt_len", "gen_len", "T", "block_len", "vocab",
+                                               "d_model"))
+    Hkv, dh = cfg["n_kv_heads"], cfg["head_dim"]
+    single = bl == G
+    L = P + G if single else bl
+    ctx_len = 0 if single else P
+    li = cfg["n_shared"]
+    names = list(tensors)
+    W = N.Weights(cfg, names, [tensors[n] for n in names])
+    rng = np.random.default_rng(cfg["input_seed"])
+    pos = np.arange(ctx_len, ctx_len + L)
+    ctx = None
+    if ctx_len:  # context K (rotary applied) and V of the prompt, random values of the right shape
+        ctx = (rng.standard_normal((ctx_len, Hkv, dh)), rng.standard_normal((ctx_len, Hkv, dh)))
+    x = rng.standard_normal((L, d)) * 0.02
+    t_start = time.perf_counter()
+
+    # every piece once, then again until the budget is spent; each piece keeps its best time
+    best = {}
+
+    def timed(key, fn):
+        t0 = time.perf_counter()
+        out = fn()
+        dt = time.perf_counter() - t0
+        best[key] = min(best.get(key, dt), dt)
+        return out
+
+    n_s = 4
+    cv = np.full(n_s, synth.mask_id(cfg), dtype=np.int64)
+    rounds = 0
+    while rounds == 0 or time.perf_counter() - t_start < budget_s:
+        h, _ = timed("layer", lambda: N.transformer_layer(W, li, x, pos, ctx))
+        ht = timed("fusion", lambda: N.fuse(W, x, {"h": h, "c": x + 0.01}))
+        xf = N.rms_norm(ht, W["final_norm"], cfg["rms_eps"])
+        lg_part = timed("head", lambda: N.operand(cfg, xf) @ W["w_out"].T)
+        # the reverse step on full-width logit rows, drawn like the head's output
+        lg = (rng.standard_normal((n_s, V)) * float(lg_part.std())).astype(np.float32)
+        timed("sampler", lambda: S.reverse_step(lg, cv, synth.mask_id(cfg), 1, ctx_len, 0, 0,
+                                                cfg["sampler_seed"], np.float32(1.0)))
+        rounds += 1
+    t_layer, t_fuse = best["layer"], best["fusion"]
+    t_head_row = best["head"] * (V / W["w_out"].shape[0]) / L
+    t_samp_row = best["sampler"] / n_s
+    sample_s = time.perf_counter() - t_start
+    # extrapolation over the schedule (one row)
+    La, Ld, Ls = cfg["n_anchor"], cfg["n_denoise"], cfg["n_shared"]
+    n_ref = math.ceil(T / K)
+    per_block = 0.0
+    for i in range(T, 0, -1):
+        masked = (G if single else bl) * i // T
+        per_block += (Ls + Ld) * t_layer + t_fuse + masked * (t_head_row + t_samp_row)
+    per_block += n_ref * La * t_layer
+    n_blocks = G // bl
+    fresh = (Ls + La + Ld) * t_layer + t_fuse  # a fresh pass over one block's positions
+    extra = 0.0 if single else (P / bl) * fresh + (n_blocks - 1) * fresh
+    row_s = n_blocks * per_block + extra
+    job_s = B * row_s
+    threads = max([t.get("num_threads", 1) for t in threadpool_info()] + [1])
+    return {"value": B * G / job_s, "unit": "tokens/s", "cores": threads, "kind": "oracle", "extrapolated": True,
+            "cpu_model": cpu_model(), "host_cpus_available": len(os.sched_getaffinity(0)),
+            "per_row_ms": {"layer": 1e3 * t_layer, "fusion": 1e3 * t_fuse, "head_per_position": 1e3 * t_head_row,
+                           "sampler_per_position": 1e3 * t_samp_row},
+            "sample": f"EXTRAPOLATED from a layer-streamed sample ({sample_s:.1f} s of oracle work, {rounds} rounds, "
+                      f"best of each): one transformer "
+                      f"layer on one row of {L} positions with {ctx_len} context keys ({1e3 * t_layer:.0f} ms), the "
+                      f"{cfg['fusion_kind']} fusion ({1e3 * t_fuse:.0f} ms), the head on {W['w_out'].shape[0]} of "
+                      f"{V} vocabulary rows (scaled), the reverse step on {n_s} masked positions; "
+                      f"scaled to B={B} rows x {n_blocks} blocks x ({n_ref} refresh + {T} denoiser steps), "
+                      f"prefill and appends as fresh passes; the real weights of those tensors, context K/V and "
+                      f"layer inputs random of the right shape; embedding gather not timed"}
 
 
 def main():
@@ -386,9 +463,17 @@ def main():
     m = tadm.tadm_model_create(tadm.make_config(cfg, max_batch=B, max_seq=P + G))
     tadm.tadm_set_stream(m, stream.cuda_stream)
     t_load = time.perf_counter()
+    # the layer-streamed oracle sample of the large workloads keeps float64 host copies of
+    # the tensors it runs: the fusion, the final norm, the first anchor layer and the first
+    # STREAM_HEAD_ROWS rows of the vocabulary head
+    streamed = {} if (not args.no_cpu and cfg["dtype"] == "bf16" and cfg["d_model"] >= 2048) else None
+    keep_layer = f"layer{cfg['n_shared']}."
     for i, spec in enumerate(synth.weight_specs(cfg)):  # one tensor at a time: bounded memory
         t = synth.make_tensor(cfg, i, spec, device=dev)
         tadm.tadm_model_load_weight(m, i, t)
+        if streamed is not None and (spec[0].startswith(("fusion.", keep_layer)) or spec[0] in ("final_norm", "w_out")):
+            src = t[:STREAM_HEAD_ROWS] if spec[0] == "w_out" else t
+            streamed[spec[0]] = src.to(torch.float64).cpu().numpy()
         del t
     torch.cuda.empty_cache()
     print(f"[bench] weights generated and loaded in {time.perf_counter() - t_load:.1f} s", file=sys.stderr,
@@ -454,17 +539,54 @@ def main():
     value = tokens / (ms / 1e3)
     print(f"[bench] K={K0}: {ms:.3f} ms/generation ({wall_ms:.3f} wall) -> {value:.1f} tokens/s",
           file=sys.stderr, flush=True)
-    sweep = {}
+    sweep = {f"K={K0}": {"tokens_per_s": value, "ms_per_step": ms}}
     if not args.no_sweep:
         for K in cfg["Ks"]:
-            kms, _, _ = timed(K, max(2, args.steps // 2), 1)
+            if K == K0:
+                continue
+            kms, _, _ = timed(K, max(1, args.steps // 2), 0 if T * (P + G) >= 2 ** 16 else 1)
             sweep[f"K={K}"] = {"tokens_per_s": tokens / (kms / 1e3), "ms_per_step": kms}
             print(f"[bench] K={K}: {kms:.3f} ms -> {tokens / (kms / 1e3):.1f} tokens/s", file=sys.stderr,
                   flush=True)
+    # per-step timing on canvases at random times (the 1B-class workload's per-step leg):
+    # t_b ~ U(0,1) per row, i_b = ceil(t_b T), floor(M0 i_b / T) positions masked; an anchor
+    # refresh on the canvas, then stale steps (S, fusion, D, head, reverse step) with each
+    # row's own unmask count
+    per_step = None
+    if cfg["name"] == "1b":
+        canvas, steps_b = synth.make_timing_canvas(cfg, T)
+        d_canvas = canvas.to(dev)
+        n_rows = torch.tensor([tadm.tadm_unmask_count(G, i, T) for i in steps_b], dtype=torch.int32, device=dev)
+        cache = tadm.tadm_cache_create(m, B, P + G)
+        nxt = torch.empty_like(d_canvas)
+        sargs = tadm.step_args(T // 2, T, 0, 7, cfg["sampler_seed"], 1.0, n_unmask_rows=n_rows)
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        tadm.tadm_anchor_forward(m, None, d_canvas, B, P + G, T, T, cache)
+        tadm.tadm_denoise_step(m, None, d_canvas, B, P + G, P, cache, sargs, None, nxt)
+        torch.cuda.synchronize()
+        reps = max(3, args.steps)
+        e0.record(stream)
+        for _ in range(reps):
+            tadm.tadm_anchor_forward(m, None, d_canvas, B, P + G, T, T, cache)
+        e1.record(stream)
+        for _ in range(reps):
+            tadm.tadm_denoise_step(m, None, d_canvas, B, P + G, P, cache, sargs, None, nxt)
+        e2.record(stream)
+        torch.cuda.synchronize()
+        a_ms, s_ms = e0.elapsed_time(e1) / reps, e1.elapsed_time(e2) / reps
+        masked = int(sum((G * i) // T for i in steps_b))
+        per_step = {"canvas": f"B={B} x {P + G} positions at t_b ~ U(0,1), {masked} masked in all",
+                    "anchor_refresh_ms": a_ms, "stale_step_ms": s_ms,
+                    "stale_step_tokens_per_s": B * (P + G) / (s_ms / 1e3),
+                    "what": "a stale step processes every position of the canvas; the head and sampler run on "
+                            "the masked ones"}
+        tadm.tadm_cache_destroy(cache)
+        print(f"[bench] random-t canvases: anchor refresh {a_ms:.3f} ms, stale step {s_ms:.3f} ms",
+              file=sys.stderr, flush=True)
     # the remasking posterior (capped sigma, eta = 0.04) without and with the nucleus p = 0.9
     # of the paper's ReMDM-Cap runs
     remask = None
-    if not args.no_sweep:
+    if args.extras:
         remask = {}
         for top_p in (0.0, 0.9):
             sampler[0] = tadm.remask_sampler(0.04, top_p)
@@ -501,7 +623,7 @@ def main():
     # the pretraining objective's forward pass (stale pair, anchor on z_t', denoiser on
     # z_t, 1/t-weighted masked cross-entropy) over B sequences of P + G tokens
     train_line = None
-    if not args.no_sweep:
+    if args.extras:
         Ltr = P + G
         xtr = torch.randint(0, cfg["vocab"], (B, Ltr), generator=torch.Generator().manual_seed(5),
                             dtype=torch.int32).to(dev)
@@ -537,7 +659,10 @@ def main():
     cpu = None
     if not args.no_cpu:
         try:
-            cpu = cpu_baseline(cfg, K0)
+            if streamed is not None:
+                cpu = cpu_baseline_streamed(cfg, K0, streamed, args.cpu_budget)
+            else:
+                cpu = cpu_baseline(cfg, K0, args.cpu_budget)
         except Exception as e:  # the GPU number stands on its own
             print(f"[bench] cpu baseline skipped: {e}", file=sys.stderr)
             cpu = {"value": None, "unit": "tokens/s", "kind": "oracle", "skipped": str(e)}
@@ -550,6 +675,10 @@ def main():
         "config": {"workload": workload_name(cfg), "global_batch": B, "seq_len": P + G, "K": K0,
                    "parallelism": "none (1 GPU)"},
         "k_sweep": sweep,
+        "k4_over_k1": (sweep["K=4"]["tokens_per_s"] / sweep["K=1"]["tokens_per_s"]
+                       if "K=4" in sweep and "K=1" in sweep else None),
+        "latency_ms_per_generation": {k: v["ms_per_step"] for k, v in sweep.items()},
+        "per_step_random_t": per_step,
         "samplers": remask,
         "train_forward": train_line,
         "stages_ms_per_step": {k: v["ms_per_step"] for k, v in stages.items()},

@@ -139,13 +139,31 @@ tadm_status tadm_cache_read(const tadm_cache* c, int32_t field, void* dst_dev, s
 int32_t tadm_cache_refresh_step(const tadm_cache* c);
 
 /* -------------------------------------------------------------- context ---- */
-/* Block diffusion: per-layer K, V of the prompt and finished blocks, attended by
- * later blocks (bidirectional within a block, causal across blocks). */
+/* Block diffusion with an encoder/decoder split (App. C.1, architecture details of the
+ * post-trained model): the encoder pass prefills a KV context from the prompt, the
+ * decoder denoises one block at a time attending to that context, and each finished
+ * block is appended to the context by the encoder.  Here the context holds per-layer
+ * K, V of the prompt and the finished blocks; attention is bidirectional within a
+ * block and causal across blocks (the prompt is block 0).
+ *
+ * tadm_context_create: a context for B rows and at most max_ctx positions
+ * (1 <= B <= max_batch, 1 <= max_ctx <= max_seq), owned by the caller and destroyed
+ * with tadm_context_destroy; device memory n_layers x 2 x B x Hkv x cap x head_dim
+ * elements of the model dtype (cap = max_ctx rounded up to 64).  TADM_ERR_INVALID for
+ * sizes outside those bounds, TADM_ERR_OOM when the allocation fails. */
 tadm_status tadm_context_create(tadm_model* m, int32_t B, int32_t max_ctx, tadm_context** out);
-/* Fresh pass (a refresh step: S, A, Phi with the fresh anchor, D) over n clean
- * tokens per row [B, n] at positions [len, len + n); appends every layer's K, V. */
+/* The encoder pass: a fresh pass (a refresh step: S, A, Phi with the fresh anchor, D)
+ * over n clean tokens per row, tokens_dev device int32 [B, n] (borrowed until the
+ * stream work completes), at positions [len, len + n), attending to the context and
+ * bidirectionally among themselves; appends every layer's K, V and advances len by n.
+ * Token ids are not read on the host: an id outside [0, vocab] is clamped into that
+ * range by the embedding gather (memory safety only; the result is then meaningless).
+ * TADM_ERR_INVALID when n < 1 or the positions exceed max_seq or the context's
+ * capacity; TADM_ERR_STATE for a context of another model or another B. */
 tadm_status tadm_context_append(tadm_model* m, tadm_context* ctx, const int32_t* tokens_dev,
                                 int32_t B, int32_t n);
+/* Committed positions (len); 0 after create or reset (and for NULL).  reset empties
+ * the context without freeing it.  destroy waits for the device, then frees it. */
 int32_t tadm_context_length(const tadm_context* ctx);
 tadm_status tadm_context_reset(tadm_context* ctx);
 tadm_status tadm_context_destroy(tadm_context* ctx);
@@ -294,6 +312,20 @@ void tadm_stale_times(int32_t B, uint64_t seed, uint32_t step, float eps, float*
 enum { TADM_TAP_EMBED = 0, TADM_TAP_FUSED = 1, TADM_TAP_FINAL = 2, TADM_TAP_CHOICE = 3, TADM_TAP_CONF = 4 };
 /* Keep a copy of h~ for TADM_TAP_FUSED (one extra [B, L, d] copy per step; off by default). */
 tadm_status tadm_debug_taps(tadm_model* m, int32_t enable);
+/* Per-layer capture for layer-by-layer checks: from now on every transformer layer li
+ * that runs (in any call) copies the residual stream entering it to slot 2 li and the
+ * stream leaving it to slot 2 li + 1 of dst_dev, each slot [B, L, d] float32 of that
+ * call (caller-owned, bytes = capacity; a layer whose slots do not fit is skipped).
+ * A slot holds the last call that ran the layer.  dst_dev = NULL turns capture off.
+ * Costs two device copies per layer; for tests. */
+tadm_status tadm_debug_layers(tadm_model* m, float* dst_dev, size_t bytes);
+/* Enqueues copies of one layer's context K [B, Hkv, cap, head_dim] (rotary embedding
+ * applied) and V transposed [B, Hkv, head_dim, cap], in the model dtype; positions
+ * [0, tadm_context_length) are committed.  bytes is the size of each array
+ * (TADM_ERR_INVALID otherwise). */
+tadm_status tadm_context_read(const tadm_context* ctx, int32_t layer, void* k_dev, void* vt_dev, size_t bytes);
+/* cap of a context: max_ctx rounded up to a multiple of 64 (0 for NULL). */
+int32_t tadm_context_capacity(const tadm_context* ctx);
 tadm_status tadm_debug_read(tadm_model* m, int32_t tap, float* dst_dev, size_t bytes);
 
 /* Per-stage timing on the model stream for each stage whose bit is set in stage_mask

@@ -95,6 +95,9 @@ _SIGS = {
                                C.POINTER(C.c_float)]),
     "tadm_debug_read": (_I, [_P, _I, _P, C.c_size_t]),
     "tadm_debug_taps": (_I, [_P, _I]),
+    "tadm_debug_layers": (_I, [_P, _P, C.c_size_t]),
+    "tadm_context_read": (_I, [_P, _I, _P, _P, C.c_size_t]),
+    "tadm_context_capacity": (_I, [_P]),
     "tadm_profile_enable": (_I, [_P, _I]),
     "tadm_profile_read": (_I, [_P, _I, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
     "tadm_profile_reset": (_I, [_P]),
@@ -348,3 +351,16 @@ def load_model(cfg, tensors, max_batch=None, max_seq=None, stream=None):
         tadm_model_destroy(m)
         raise
     return m
+
+
+def tadm_debug_layers(m, dst):
+    """dst: device float32 tensor of 2 * n_layers slots [B, L, d] (None turns capture off)."""
+    check(lib.tadm_debug_layers(m, ptr(dst), 0 if dst is None else dst.numel() * 4))
+
+
+def tadm_context_read(ctx, layer, k, vt):
+    check(lib.tadm_context_read(ctx, layer, ptr(k), ptr(vt), k.numel() * k.element_size()))
+
+
+def tadm_context_capacity(ctx):
+    return lib.tadm_context_capacity(ctx)

@@ -284,6 +284,9 @@ struct tadm_model {
   void* embT = nullptr;            // embedding rows [0, V) transposed, [d, round64(V)] (lazy)
   bool embT_valid = false;
   int tap_B = 0, tap_L = 0, tap_Lc = 0;
+  // per-layer capture (tadm_debug_layers): residual stream entering and leaving each layer
+  float* layer_cap = nullptr;
+  size_t layer_cap_bytes = 0;
   // profiling
   int32_t prof_mask = 0;  // bit s: record stage s
   std::vector<ProfRec> recs;
@@ -456,6 +459,11 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
   const int N = B * L, d = c.d_model, H = c.n_heads, Hk = c.n_kv_heads, dh = c.head_dim,
             F = c.d_ffn;
   const hipStream_t st = m->stream;
+  // capture slots: 2 li (entering layer li) and 2 li + 1 (leaving it), [N, d] float32 each
+  const size_t slot = (size_t)N * d;
+  const bool capture = m->layer_cap && (2 * (size_t)li + 2) * slot * 4 <= m->layer_cap_bytes;
+  if (capture)
+    HIPCHK(hipMemcpyAsync(m->layer_cap + 2 * (size_t)li * slot, x, slot * 4, hipMemcpyDeviceToDevice, st));
   if (!prenormed) HIPCHK(rms_norm(m->dt, x, m->Wf(w.attn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
   {
     // q/k/v projection with the rotary embedding and head split in the epilogue
@@ -530,6 +538,8 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
     HIPCHK(gemm(m->dt, p, EPI_RESID, e, st));
     TRY(prof_end(m, TADM_STAGE_FFN_DOWN));
   }
+  if (capture)
+    HIPCHK(hipMemcpyAsync(m->layer_cap + (2 * (size_t)li + 1) * slot, x, slot * 4, hipMemcpyDeviceToDevice, st));
   return TADM_OK;
 }
 
@@ -1619,6 +1629,27 @@ tadm_status tadm_debug_taps(tadm_model* m, int32_t enable) {
   m->taps = enable != 0;
   return TADM_OK;
 }
+
+tadm_status tadm_debug_layers(tadm_model* m, float* dst_dev, size_t bytes) {
+  if (!m) return fail(TADM_ERR_INVALID, "null model");
+  if (dst_dev && bytes == 0) return fail(TADM_ERR_INVALID, "empty capture buffer");
+  m->layer_cap = dst_dev;
+  m->layer_cap_bytes = dst_dev ? bytes : 0;
+  return TADM_OK;
+}
+
+tadm_status tadm_context_read(const tadm_context* ctx, int32_t layer, void* k_dev, void* vt_dev, size_t bytes) {
+  if (!ctx || !k_dev || !vt_dev) return fail(TADM_ERR_INVALID, "null argument");
+  const tadm_model* m = ctx->model;
+  if (layer < 0 || layer >= m->n_layers()) return fail(TADM_ERR_INVALID, "layer %d", layer);
+  const size_t n = (size_t)ctx->B * m->cfg.n_kv_heads * ctx->cap * m->cfg.head_dim * m->esz;
+  if (bytes != n) return fail(TADM_ERR_INVALID, "context layer has %zu bytes, got %zu", n, bytes);
+  HIPCHK(hipMemcpyAsync(k_dev, ctx->k[layer], n, hipMemcpyDeviceToDevice, m->stream));
+  HIPCHK(hipMemcpyAsync(vt_dev, ctx->vt[layer], n, hipMemcpyDeviceToDevice, m->stream));
+  return TADM_OK;
+}
+
+int32_t tadm_context_capacity(const tadm_context* ctx) { return ctx ? ctx->cap : 0; }
 
 tadm_status tadm_profile_enable(tadm_model* m, int32_t stage_mask) {
   if (!m) return fail(TADM_ERR_INVALID, "null model");

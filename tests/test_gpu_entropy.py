@@ -85,7 +85,9 @@ def test_selfcond_matches_oracle(name, overrides, rtol, atol):
         sync()
         E = tensors[[sp[0] for sp in synth.weight_specs(cfg)].index("embed")]
         ref = usdm.selfcond(logits.numpy(), np.float32(1.25), E.float().numpy())
-        rows_close(sc.cpu().numpy(), ref, rtol, atol, f"{name} self-conditioning", scale_atol=name != "tiny")
+        if name != "tiny":  # s is ~1e-2 in size: the bar's atol is taken relative to it (stricter)
+            atol = atol * float(np.sqrt((ref ** 2).mean()))
+        rows_close(sc.cpu().numpy(), ref, rtol, atol, f"{name} self-conditioning")
     finally:
         tadm.tadm_model_destroy(m)
 

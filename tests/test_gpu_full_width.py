@@ -1,14 +1,23 @@
-"""Full-width, full-batch parity of the benchmark workloads (GPU).
+"""Full-size parity of the benchmark workloads (GPU), layer by layer.
 
-The block-diffusion, 1B-class and 26B-class workloads at their full width, vocabulary,
-batch and sequence sizes, so that every kernel runs in the launch configuration the
-benchmark times (GEMM tile shapes follow the row count, attention the context length,
-the fused head the vocabulary), with one anchor and one denoiser layer so that the
-float64 oracle can follow a sampled row in seconds.  Per sampled row: the anchor
-state, the fused state, the final hidden state and the logits against the oracle,
-judged against the oracle's own bf16 noise floor at that shape (the spread between two
-equally valid bf16 evaluations of the row); over the whole batch: the step with the
-sampling epilogue equals, bit for bit, the step computed from the full logits.
+The block-diffusion and 1B-class workloads at their full depth (20 + 4 and 18 + 6
+layers), width, vocabulary, batch and sequence, and the 26B-class workload at its full
+width, vocabulary, batch, sequence and depth (40 + 6 layers) with five of its layers
+checked, so that every kernel runs in the launch configuration the benchmark times
+(GEMM tile shapes follow the row count, attention the context length, the fused head
+the vocabulary).
+
+Teacher forcing per layer: the GPU records the residual stream entering and leaving
+every transformer layer (tadm_debug_layers); for a sampled row the float64 oracle runs
+each checked layer on the GPU's own input to it (and, in block mode, on the GPU's own
+context K/V of that layer, tadm_context_read), the fusion on the GPU's c, h' (and c'),
+and the final norm and head on the GPU's last residual stream.  Every output must lie
+within rtol = atol = 2e-2 of the oracle's, element by element.  Chained over 24 layers
+without teacher forcing, two equally valid bf16 evaluations of these random-init
+models drift apart by far more than that (the design notes give the figures), so a
+whole-network comparison at this depth would measure that drift, not the kernels.
+Over the whole batch: the step with the sampling epilogue equals, bit for bit, the
+step computed from the full logits.
 """
 import numpy as np
 import pytest
@@ -16,30 +25,54 @@ import torch
 
 import paper_2609_37924_amd as tadm
 import synth
-from helpers import dev, gpu_model, oracle_net, unnormalised_attention, within_noise_floor
+from helpers import dev, gpu_generated_weights, rows_close
 from oracle import network as N
 
 pytestmark = pytest.mark.gpu
 
+BF16_TOL = dict(rtol=2e-2, atol=2e-2)
 
 
 def say(msg):
-    print(f"[full-width] {msg}", flush=True)
+    print(f"[full-size] {msg}", flush=True)
 
 
-def _full_width(name, rows):
-    cfg = synth.get_config(name, n_anchor=1, n_denoise=1)
+def _row(t, b):
+    return t[b].float().cpu().numpy().astype(np.float64)
+
+
+def _full_size(name, rows, layers=None):
+    """layers: the transformer layers checked (all when None)."""
+    cfg = synth.get_config(name)
     B, P, G, bl, V, d = (cfg[k] for k in ("batch", "prompt_len", "gen_len", "block_len", "vocab", "d_model"))
+    Hkv, dh = cfg["n_kv_heads"], cfg["head_dim"]
+    n_layers = cfg["n_shared"] + cfg["n_anchor"] + cfg["n_denoise"]
+    Ls, La = cfg["n_shared"], cfg["n_anchor"]
+    checked = list(range(n_layers)) if layers is None else layers
     single = bl == G
     Lw = P + G if single else bl          # positions of one call
     off = P if single else 0
     Lc = Lw - off
-    say(f"{name}: B={B} P={P} G={G} block={bl} d={d} V={V}; generating weights")
-    tensors = synth.make_weights(cfg, perturb=True)
-    m = gpu_model(cfg, tensors, B, P + G)
-    say("weights on the GPU")
+    say(f"{name}: {La} + {cfg['n_denoise']} layers (checking {len(checked)}), B={B} P={P} G={G} "
+        f"block={bl} d={d} V={V}")
+    keep = tuple(f"layer{li}." for li in checked) + ("fusion.", "final_norm", "w_out", "embed")
+    dev_t, host = gpu_generated_weights(cfg, keep=lambda n: n.startswith(keep))
+    m = tadm.load_model(cfg, dev_t, max_batch=B, max_seq=P + G, stream=torch.cuda.current_stream().cuda_stream)
+    del dev_t
+    W = N.Weights(cfg, list(host), [host[k] for k in host])
+    del host
+    say("weights on the GPU, checked layers on the host")
+    failures = []
+
+    def check(got, ref, what):
+        try:
+            rows_close(got, ref, what=f"{name} {what}", **BF16_TOL)
+        except AssertionError as e:
+            failures.append(str(e))
+
     try:
         tadm.tadm_debug_taps(m, 1)
+        cap = torch.empty(2 * n_layers, B, Lw, d, device=dev())
         prompt = synth.make_prompt(cfg, batch=B) if P else None
         ctx = None
         g = torch.Generator().manual_seed(5)
@@ -55,64 +88,91 @@ def _full_width(name, rows):
             z1[torch.rand(B, bl, generator=g) < 0.6] = V
             pos = np.arange(P, P + bl)
         T, i = 16, 11
+        # anchor refresh on z0, its layers captured
+        tadm.tadm_debug_layers(m, cap)
         cache = tadm.tadm_cache_create(m, B, Lw)
         tadm.tadm_anchor_forward(m, ctx, z0.to(dev()), B, Lw, T, T, cache)
         h_gpu = torch.empty(B, Lw, d, device=dev())
+        c0_gpu = torch.empty(B, Lw, d, device=dev())
         tadm.tadm_cache_read(cache, tadm.CACHE_H, h_gpu)
+        tadm.tadm_cache_read(cache, tadm.CACHE_C, c0_gpu)
+        torch.cuda.synchronize()
+        # (layer, row) -> float64 (entering, leaving) of the rows checked
+        layer_io = {(li, b): (_row(cap[2 * li], b), _row(cap[2 * li + 1], b))
+                    for li in checked if li < Ls + La for b in rows}
+        # stale step on z1, its layers captured
         args = tadm.step_args(i, T, tadm.tadm_unmask_count(Lc, i, T), T - i, 91, 1.0)
         d1 = z1.to(dev())
         logits = torch.empty(B, Lc, V, device=dev())
         nxt_full, nxt_fused = torch.empty_like(d1), torch.empty_like(d1)
         tadm.tadm_denoise_step(m, ctx, d1, B, Lw, off, cache, args, logits, nxt_full)
+        embed = torch.empty(B, Lw, d, device=dev())
         fused = torch.empty(B, Lw, d, device=dev())
         final = torch.empty(B, Lc, d, device=dev())
+        tadm.tadm_debug_read(m, tadm.TAP_EMBED, embed)
         tadm.tadm_debug_read(m, tadm.TAP_FUSED, fused)
         tadm.tadm_debug_read(m, tadm.TAP_FINAL, final)
+        torch.cuda.synchronize()
+        layer_io.update({(li, b): (_row(cap[2 * li], b), _row(cap[2 * li + 1], b))
+                         for li in checked if li >= Ls + La for b in rows})
+        last_out = {b: _row(cap[2 * (n_layers - 1) + 1], b) for b in rows}
+        tadm.tadm_debug_layers(m, None)
+        del cap
         tadm.tadm_denoise_step(m, ctx, d1, B, Lw, off, cache, args, None, nxt_fused)
         torch.cuda.synchronize()
         assert torch.equal(nxt_full, nxt_fused), "sampling epilogue differs from the full-logits step"
-        say("GPU step done; fused-head step equals the full-logits step")
-        net = oracle_net(cfg, tensors)
-        del tensors
-        orig = N.attention
-
-        def oracle_row(b, attention):
-            N.attention = attention
-            try:
-                kv = None if single else net.fresh_kv(prompt[b].numpy(), np.arange(P))
-                cache_ref = net.anchor_cache(net.shared(z0[b].numpy(), pos, kv), pos, kv)
-                ht = net.fuse(net.shared(z1[b].numpy(), pos, kv), cache_ref)
-                xf = net.denoise(ht, pos, kv)[off:]
-                return {"anchor h": cache_ref["h"], "fused": ht, "final": xf, "logits": net.head(xf)}
-            finally:
-                N.attention = orig
-
+        say("GPU steps done; fused-head step equals the full-logits step")
+        ctx_kv = {}
+        if ctx is not None:
+            capc = tadm.tadm_context_capacity(ctx)
+            for li in checked:
+                k = torch.empty(B, Hkv, capc, dh, dtype=torch.bfloat16, device=dev())
+                vt = torch.empty(B, Hkv, dh, capc, dtype=torch.bfloat16, device=dev())
+                tadm.tadm_context_read(ctx, li, k, vt)
+                ctx_kv[li] = (k, vt)
+            torch.cuda.synchronize()
         for b in rows:
-            say(f"oracle row {b} (two bf16 evaluations)")
-            ref, alt = oracle_row(b, orig), oracle_row(b, unnormalised_attention(orig))
-            got = {"anchor h": h_gpu[b], "fused": fused[b], "final": final[b], "logits": logits[b]}
-            for k in ref:
-                within_noise_floor(got[k].cpu().numpy(), ref[k], alt[k], f"{name} {k} row {b}")
+            say(f"row {b}")
+            if "embed" in W.t:
+                np.testing.assert_array_equal(_row(embed, b), W["embed"][z1[b].numpy()])
+            for li in checked:
+                x_in, x_out = layer_io[(li, b)]
+                kv = None
+                if ctx is not None:
+                    k, vt = ctx_kv[li]
+                    kv = (k[b, :, :P, :].permute(1, 0, 2).double().cpu().numpy(),
+                          vt[b, :, :, :P].permute(2, 0, 1).double().cpu().numpy())
+                ref, _ = N.transformer_layer(W, li, x_in, pos, kv)
+                check(x_out, ref, f"layer {li} row {b}")
+            ref_fused = N.fuse(W, _row(embed, b), {"h": _row(h_gpu, b), "c": _row(c0_gpu, b)})
+            check(_row(fused, b), ref_fused, f"fusion row {b}")
+            xf = N.rms_norm(last_out[b], W["final_norm"], cfg["rms_eps"])[off:]
+            check(_row(final, b), xf, f"final norm row {b}")
+            check(_row(logits, b), N.head(W, xf), f"logits row {b}")
         tadm.tadm_cache_destroy(cache)
         if ctx is not None:
             tadm.tadm_context_destroy(ctx)
     finally:
         tadm.tadm_model_destroy(m)
+    assert not failures, "\n".join(failures)
 
 
-def test_block_workload_full_width():
-    """Block diffusion: d=2048, 16 heads / 4 KV heads of 128, SwiGLU 8192, V=128256,
-    B=16, 512-token prompt prefilled into the context, 64-position blocks."""
-    _full_width("block", rows=[0, 15])
+def test_block_workload_full_depth():
+    """Block diffusion: 20 anchor + 4 denoiser layers, d=2048, 16 heads / 4 KV heads of
+    128, SwiGLU 8192, V=128256, B=16, 512-token prompt prefilled into the context,
+    64-position blocks; every layer checked on rows 0 and 15."""
+    _full_size("block", rows=[0, 15])
 
 
-def test_1b_workload_full_width():
-    """1B-class: d=2048, 16 heads of 128, GELU 8192, V=50304, B=32, 1024 positions."""
-    _full_width("1b", rows=[0, 31])
+def test_1b_workload_full_depth():
+    """1B-class: 18 anchor + 6 denoiser layers, d=2048, 16 heads of 128, GELU 8192,
+    V=50304, B=32, 1024 positions; every layer checked on rows 0 and 31."""
+    _full_size("1b", rows=[0, 31])
 
 
-def test_26b_workload_full_width():
-    """26B-class post-trained shape: d=4608, 32 heads / 16 KV heads of 128, GeGLU 36864,
-    paired-attention fusion of rank 256, V=262144, B=4, 1024-token prompt, 256-position
-    blocks."""
-    _full_width("26b", rows=[3])
+def test_26b_workload_full_depth():
+    """26B-class post-trained shape, 40 anchor + 6 denoiser layers: d=4608, 32 heads / 16
+    KV heads of 128, GeGLU 36864, paired-attention fusion of rank 256, V=262144, B=4,
+    1024-token prompt, 256-position blocks; the first, middle and last anchor layers and
+    the first and last denoiser layers checked on row 3."""
+    _full_size("26b", rows=[3], layers=[0, 20, 39, 40, 45])

@@ -21,10 +21,7 @@ if not torch.cuda.is_available():
     pytest.skip("no GPU", allow_module_level=True)
 
 FP32_TOL = dict(rtol=1e-4, atol=1e-4)
-# bf16: the bound rtol = atol = 2e-2 must hold for all but a 1e-5 tail of elements,
-# and every element within 4e-2 (two bf16 evaluations of one model diverge at the
-# rounding-noise level; tests/test_bf16_noise.py measures that floor on the CPU).
-BF16_TOL = dict(rtol=2e-2, atol=2e-2, tail=1e-5, max_err=4e-2)
+BF16_TOL = dict(rtol=2e-2, atol=2e-2)
 
 
 def sync():
@@ -264,17 +261,18 @@ def test_gelu_bf16_step_parity():
 @pytest.mark.parametrize("dh,H,Hkv", [(64, 12, 12), (128, 16, 16), (128, 16, 4)])
 def test_attention_dominated_layer(dh, H, Hkv):
     """One anchor layer whose output is dominated by attention (feed-forward off,
-    V and O projections scaled up), so that an attention error cannot hide behind
-    the residual stream.  Covers both head widths and grouped KV heads."""
+    V and O projections scaled up twofold: the attention output, rms ~1, is ~50 times
+    the embedding it is added to), so that an attention error cannot hide behind the
+    residual stream.  Covers both head widths and grouped KV heads."""
     cfg = synth.get_config("1b", n_anchor=1, n_denoise=1, vocab=512, n_heads=H, n_kv_heads=Hkv,
                            head_dim=dh, d_model=H * dh, prompt_len=30, gen_len=100)
     tensors = synth.make_weights(cfg, perturb=True)
     names = [s[0] for s in synth.weight_specs(cfg)]
     for li in range(2):
-        tensors[names.index(f"layer{li}.wv")] = (tensors[names.index(f"layer{li}.wv")].float() * 8).bfloat16()
-        tensors[names.index(f"layer{li}.wo")] = (tensors[names.index(f"layer{li}.wo")].float() * 8).bfloat16()
+        tensors[names.index(f"layer{li}.wv")] = (tensors[names.index(f"layer{li}.wv")].float() * 2).bfloat16()
+        tensors[names.index(f"layer{li}.wo")] = (tensors[names.index(f"layer{li}.wo")].float() * 2).bfloat16()
         tensors[names.index(f"layer{li}.w_down")] = torch.zeros_like(tensors[names.index(f"layer{li}.w_down")])
-    _teacher_step_parity(cfg, 2, dict(BF16_TOL, scale_atol=True), tensors=tensors)
+    _teacher_step_parity(cfg, 2, BF16_TOL, tensors=tensors)
 
 
 def test_tiny_fp32_paired_step_parity():
@@ -498,6 +496,78 @@ def test_bf16_generation_invariants():
     P = cfg["prompt_len"]
     assert np.array_equal(got[:, :P], prompt.numpy())
     assert (got >= 0).all() and (got < cfg["vocab"]).all()
+
+
+@pytest.mark.parametrize("block_len", [None, 16])
+def test_bf16_generation_step_by_step_matches_oracle_sampler(block_len):
+    """A whole bf16 generation (single canvas, and block mode with context KV), replayed
+    step by step through the C ABI with the product path (masked-only head with the
+    sampling epilogue, device-side row compaction): at every step the sampled tokens,
+    the confidences and the next canvas equal, bit for bit, the oracle's reverse step
+    on that step's GPU logits (the same step run once more with a logits buffer), and
+    the replay's final tokens equal tadm_generate's."""
+    cfg = synth.get_config("small", n_anchor=2, n_denoise=1, prompt_len=40, gen_len=48, T=12)
+    B, P, G, T, K, V = 3, 40, 48, 12, 4, cfg["vocab"]
+    bl = block_len or G
+    single = bl == G
+    seed, inv_temp = 0x51CE, 1.0
+    tensors = synth.make_weights(cfg, perturb=True)
+    prompt = synth.make_prompt(cfg, batch=B)
+    m = gpu_model(cfg, tensors, B, P + G)
+    try:
+        tadm.tadm_debug_taps(m, 1)
+        out = torch.empty(B, P + G, dtype=torch.int32, device=dev())
+        tadm.tadm_generate(m, prompt.to(dev()), B, P, G, T, K, bl, seed, inv_temp, out)
+        seq = torch.cat([prompt, torch.full((B, G), V, dtype=torch.int32)], 1).to(dev())
+        ctx = None
+        if not single:
+            ctx = tadm.tadm_context_create(m, B, P + G)
+            tadm.tadm_context_append(m, ctx, seq[:, :P].contiguous(), B, P)
+        windows = [(0, P, P + G)] if single else [(P + j * bl, P + j * bl, P + (j + 1) * bl) for j in range(G // bl)]
+        steps = 0
+        for j, (w0, c0, w1) in enumerate(windows):
+            Lw, off = w1 - w0, c0 - w0
+            Lc = w1 - c0
+            cache = tadm.tadm_cache_create(m, B, Lw)
+            for i in range(T, 0, -1):
+                z = seq[:, w0:w1].contiguous()
+                if (T - i) % K == 0:
+                    tadm.tadm_anchor_forward(m, ctx, z, B, Lw, i, T, cache)
+                n = tadm.tadm_unmask_count(Lc, i, T)
+                step_id = j * T + (T - i)
+                args = tadm.step_args(i, T, n, step_id, seed, inv_temp)
+                logits = torch.empty(B, Lc, V, device=dev())
+                nz_full = torch.empty_like(z)
+                tadm.tadm_denoise_step(m, ctx, z, B, Lw, off, cache, args, logits, nz_full)
+                nz = torch.empty_like(z)
+                tadm.tadm_denoise_step(m, ctx, z, B, Lw, off, cache, args, None, nz)
+                choice = torch.empty(B, Lc, dtype=torch.int32, device=dev())
+                conf = torch.empty(B, Lc, dtype=torch.float32, device=dev())
+                tadm.tadm_debug_read(m, tadm.TAP_CHOICE, choice)
+                tadm.tadm_debug_read(m, tadm.TAP_CONF, conf)
+                sync()
+                zc = z.cpu().numpy().astype(np.int64)
+                r_next, r_choice, r_conf = oracle_sample_rows(logits.cpu().numpy(), zc, V, n, c0 - off, off,
+                                                              step_id, seed, inv_temp)
+                masked = zc[:, off:] == V
+                np.testing.assert_array_equal(choice.cpu().numpy()[masked], r_choice[masked])
+                np.testing.assert_array_equal(conf.cpu().numpy().view(np.int32)[masked],
+                                              r_conf.view(np.int32)[masked])
+                np.testing.assert_array_equal(nz.cpu().numpy(), r_next, err_msg=f"block {j} step i={i}")
+                assert torch.equal(nz, nz_full)
+                seq[:, w0:w1] = nz
+                steps += 1
+            tadm.tadm_cache_destroy(cache)
+            if ctx is not None and j + 1 < len(windows):
+                tadm.tadm_context_append(m, ctx, seq[:, w0:w1].contiguous(), B, Lw)
+        sync()
+        assert steps == T * len(windows)
+        assert not (seq == V).any()
+        assert torch.equal(seq, out), "the step-by-step replay differs from tadm_generate"
+        if ctx is not None:
+            tadm.tadm_context_destroy(ctx)
+    finally:
+        tadm.tadm_model_destroy(m)
 
 
 # -------------------------------------------------------------- invariants
