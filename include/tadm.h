@@ -216,6 +216,24 @@ tadm_status tadm_sample(tadm_model* m, const float* logits_dev, const int32_t* c
                         const tadm_step_args* args, int32_t* next_canvas_dev,
                         int32_t* choice_dev, float* conf_dev);
 
+/* tadm_sample for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same arguments,
+ * results bit-identical to tadm_sample, but it calls no hipMalloc/hipFree and never
+ * touches the model's workspace: the per-position tokens, confidences and nucleus
+ * thresholds that pass between its kernels live in a fixed device array of the
+ * library, one per GPU (TADM_NOALLOC_MAX_POSITIONS entries, about 2 MB, held until the
+ * process ends; its address is looked up on the first call on each device).
+ * Limits: B * (L - canvas_off) <= TADM_NOALLOC_MAX_POSITIONS, else TADM_ERR_INVALID;
+ * ENTROPY mode returns TADM_ERR_UNSUPPORTED (its statistics need the workspace).  The
+ * stage timers are not used.  Every call on one GPU shares that array: calls that
+ * overlap on one GPU (on different streams, or from several threads) race and must be
+ * serialised by the caller; nothing in it needs clearing between calls. */
+#define TADM_NOALLOC_MAX_POSITIONS 65536
+tadm_status tadm_sample_noalloc(tadm_model* m, const float* logits_dev, const int32_t* canvas_dev,
+                                int32_t B, int32_t L, int32_t canvas_off, int32_t pos0,
+                                const tadm_step_args* args, int32_t* next_canvas_dev,
+                                int32_t* choice_dev, float* conf_dev);
+
 /* Whole generation (Algorithm 1 with the linear unmask schedule
  * n_i = floor(M0 i / T) - floor(M0 (i-1) / T)).  prompt_dev [B, P]; tokens_dev
  * [B, P + gen_len] receives prompt and generated tokens.  block_len == gen_len:

@@ -86,6 +86,7 @@ _SIGS = {
     "tadm_stale_times": (None, [_I, C.c_uint64, C.c_uint32, C.c_float, _P, _P, _P, _P, _P]),
     "tadm_denoise_step": (_I, [_P, _P, _P, _I, _I, _I, _P, C.POINTER(tadm_step_args), _P, _P]),
     "tadm_sample": (_I, [_P, _P, _P, _I, _I, _I, _I, C.POINTER(tadm_step_args), _P, _P, _P]),
+    "tadm_sample_noalloc": (_I, [_P, _P, _P, _I, _I, _I, _I, C.POINTER(tadm_step_args), _P, _P, _P]),
     "tadm_generate": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, C.c_uint64, C.c_float, _P]),
     "tadm_generate_sampler": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, C.c_uint64, C.c_float,
                                    C.POINTER(tadm_sampler), _P]),
@@ -108,6 +109,7 @@ for _name, (_res, _args) in _SIGS.items():
     _f.restype, _f.argtypes = _res, _args
 
 EXPORTED = sorted(_SIGS)
+NOALLOC_MAX_POSITIONS = 65536  # TADM_NOALLOC_MAX_POSITIONS
 
 
 def last_error():
@@ -263,6 +265,11 @@ def tadm_denoise_step(m, ctx, canvas, B, L, canvas_off, cache, args, logits, nex
 def tadm_sample(m, logits, canvas, B, L, canvas_off, pos0, args, next_canvas, choice=None, conf=None):
     check(lib.tadm_sample(m, ptr(logits), ptr(canvas), B, L, canvas_off, pos0, C.byref(args),
                           ptr(next_canvas), ptr(choice), ptr(conf)))
+
+
+def tadm_sample_noalloc(m, logits, canvas, B, L, canvas_off, pos0, args, next_canvas, choice=None, conf=None):
+    check(lib.tadm_sample_noalloc(m, ptr(logits), ptr(canvas), B, L, canvas_off, pos0, C.byref(args),
+                                  ptr(next_canvas), ptr(choice), ptr(conf)))
 
 
 def tadm_generate(m, prompt, B, P, gen_len, T, K, block_len, seed, temperature, tokens):

@@ -11,6 +11,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -49,6 +50,7 @@ static tadm_status fail(tadm_status st, const char* fmt, ...) {
   } while (0)
 
 static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+static constexpr size_t align_up_const(size_t x) { return (x + 255) & ~size_t(255); }
 static int round64(int x) { return (x + 63) / 64 * 64; }
 
 // ----------------------------------------------------------- weight specs ----
@@ -818,6 +820,43 @@ static tadm_status canvas_update(tadm_model* m, const int32_t* canvas, const int
   return TADM_OK;
 }
 
+// ------------------------------------------------- allocation-free sampler ---
+// Fixed device array of tadm_sample_noalloc: per canvas position the sampled token
+// (int32) and confidence (float32), then the nucleus thresholds.  In host code the
+// array's name stands for a host-side shadow, not a device address: the device copy
+// of each GPU is reached only through the address hipGetSymbolAddress returns with
+// that GPU current, kept per device below.
+namespace {
+constexpr size_t kNoAllocChoice = 0;
+constexpr size_t kNoAllocConf = kNoAllocChoice + (size_t)TADM_NOALLOC_MAX_POSITIONS * sizeof(int32_t);
+constexpr size_t kNoAllocThr = align_up_const(kNoAllocConf + (size_t)TADM_NOALLOC_MAX_POSITIONS * sizeof(float));
+constexpr size_t kNoAllocBytes = kNoAllocThr + (size_t)TADM_NOALLOC_MAX_POSITIONS * sizeof(NucleusThr);
+constexpr int kMaxDevices = 64;
+}  // namespace
+
+static __device__ __align__(256) char scratch[kNoAllocBytes];
+static std::mutex g_scratch_mutex;
+static char* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of `scratch` on `device`, looked up once per device with it current.
+static tadm_status noalloc_scratch(int device, char** out) {
+  if (device < 0 || device >= kMaxDevices) return fail(TADM_ERR_UNSUPPORTED, "device %d", device);
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_dev[device]) {
+    int prev = -1;
+    hipError_t e = hipGetDevice(&prev);
+    if (e == hipSuccess && prev != device) e = hipSetDevice(device);
+    void* ptr = nullptr;
+    if (e == hipSuccess) e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (prev >= 0 && prev != device) (void)hipSetDevice(prev);
+    if (e != hipSuccess || !ptr)
+      return fail(TADM_ERR_DEVICE, "scratch address on device %d: %s", device, hipGetErrorString(e));
+    g_scratch_dev[device] = static_cast<char*>(ptr);
+  }
+  *out = g_scratch_dev[device];
+  return TADM_OK;
+}
+
 // ============================================================== C ABI =========
 extern "C" {
 
@@ -1329,6 +1368,40 @@ tadm_status tadm_sample(tadm_model* m, const float* logits_dev, const int32_t* c
                         choice_dev ? choice_dev : m->ws.choice, conf_dev ? conf_dev : m->ws.conf);
   return sample_impl(m, logits_dev, nullptr, canvas_dev, B, L, canvas_off, pos0, args, next_canvas_dev,
                      choice_dev ? choice_dev : m->ws.choice, conf_dev ? conf_dev : m->ws.conf);
+}
+
+tadm_status tadm_sample_noalloc(tadm_model* m, const float* logits_dev, const int32_t* canvas_dev, int32_t B,
+                                int32_t L, int32_t canvas_off, int32_t pos0, const tadm_step_args* args,
+                                int32_t* next_canvas_dev, int32_t* choice_dev, float* conf_dev) {
+  if (!m) return fail(TADM_ERR_INVALID, "null model");
+  if (!logits_dev || !canvas_dev || !next_canvas_dev) return fail(TADM_ERR_INVALID, "null argument");
+  if (B < 1 || B > m->cfg.max_batch || L < 1 || L > m->cfg.max_seq || canvas_off < 0 || canvas_off >= L || pos0 < 0)
+    return fail(TADM_ERR_INVALID, "sample shape B=%d L=%d off=%d", B, L, canvas_off);
+  TRY(check_args(args, L - canvas_off));
+  if (args->mode == TADM_STEP_ENTROPY) return fail(TADM_ERR_UNSUPPORTED, "entropy mode needs the workspace");
+  const long long positions = (long long)B * (L - canvas_off);
+  if (positions > TADM_NOALLOC_MAX_POSITIONS)
+    return fail(TADM_ERR_INVALID, "%lld canvas positions exceed the %d of the fixed scratch", positions,
+                TADM_NOALLOC_MAX_POSITIONS);
+  char* base = nullptr;
+  TRY(noalloc_scratch(m->device, &base));
+  int32_t* choice = choice_dev ? choice_dev : reinterpret_cast<int32_t*>(base + kNoAllocChoice);
+  float* conf = conf_dev ? conf_dev : reinterpret_cast<float*>(base + kNoAllocConf);
+  NucleusThr* thr = reinterpret_cast<NucleusThr*>(base + kNoAllocThr);
+  const int mask = m->cfg.vocab;
+  const bool nucleus = args->top_p > 0.f && args->top_p < 1.f;
+  if (nucleus)
+    HIPCHK(nucleus_thresholds(logits_dev, nullptr, canvas_dev, B, L, canvas_off, m->cfg.vocab, mask, args->inv_temp,
+                              args->top_p, thr, m->stream));
+  HIPCHK(sample_tokens(logits_dev, nullptr, nucleus ? thr : nullptr, canvas_dev, B, L, canvas_off, m->cfg.vocab, mask,
+                       pos0, args->step_id, args->seed, args->inv_temp, choice, conf, m->stream));
+  if (args->mode == TADM_STEP_REMASK)
+    HIPCHK(remask_update(canvas_dev, choice, B, L, canvas_off, mask, pos0, args->step_id, args->seed, args->p_unmask,
+                         args->sigma, next_canvas_dev, m->stream));
+  else
+    HIPCHK(select_unmask(canvas_dev, choice, conf, B, L, canvas_off, mask, args->n_unmask, args->n_unmask_rows,
+                         next_canvas_dev, m->stream));
+  return TADM_OK;
 }
 
 // --------------------------------------------------------------- generate ---
