@@ -3,8 +3,11 @@
 //
 // WGM x WGN wave64s per block, block tile BM x BN, K tiles of 64.  Tiles move
 // global -> LDS with global_load_lds_dwordx4 (no register staging) through a
-// STAGES-deep ring of LDS buffers, so that STAGES-1 tiles are in flight while one is
-// multiplied.  LDS rows are 128 B (64 bf16); the 16-byte chunk c of row r is stored
+// two-stage ring of LDS buffers: the next K tile lands while one is multiplied.  Each
+// wave holds one set of MFMA fragments and reads the next 32-deep half's fragments in
+// their place as the products that use them issue (a rolling prefetch), so that its
+// LDS reads overlap its own MFMAs instead of all waves reading at once after each
+// barrier.  LDS rows are 128 B (64 bf16); the 16-byte chunk c of row r is stored
 // in slot c ^ (r & 7), which makes the MFMA fragment reads (16 rows x one chunk) hit
 // distinct banks; the permutation is applied through the global addresses because
 // each lane's 16 bytes land at a fixed LDS slot.  Products use
@@ -69,6 +72,20 @@ __device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int rm, int rn
   tn = b / tiles_m;
 }
 
+// MFMA on an accumulator held in four AGPRs, written in place (dst == srcC).  Keeping
+// the accumulator tied to one register quadruple over the whole K loop stops the
+// register allocator from rotating accumulators through VGPRs between iterations.
+// The chain of products on one accumulator needs no wait states (full-register srcC
+// overlap); the operands come from LDS reads, whose waits the compiler inserts.
+__device__ __forceinline__ void mfma_acc(f32x4& acc, const bf16x8& w, const bf16x8& a) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(w), "v"(a));
+}
+// The first product of an accumulator: srcC is the constant 0, so no VALU write
+// initialises the accumulator (a VALU write read by an MFMA would need wait states).
+__device__ __forceinline__ void mfma_first(f32x4& acc, const bf16x8& w, const bf16x8& a) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=a"(acc) : "v"(w), "v"(a));
+}
+
 // ------------------------------------------------------------ bf16 MFMA kernel
 template <int BM, int BN, int STAGES, int WGM, int WGN, int MINB, EpiKind KIND>
 __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmProblem p, EpiParams ep) {
@@ -78,7 +95,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
   constexpr int STAGE_BYTES = (BM + BN) * ROW;
   constexpr int LA = BM / 8 / NW, LW = BN / 8 / NW;  // load instructions per wave per stage
   static_assert(LA * 8 * NW == BM && LW * 8 * NW == BN, "tile rows must split evenly over waves");
-  constexpr int LPS = LA + LW;
+  static_assert(STAGES == 2, "the K loop is written for a two-stage ring");
   constexpr int WTM = BM / WGM, WTN = BN / WGN; // wave tile
   constexpr int TM = WTM / 16, TN = WTN / 16;   // 16x16 subtiles per wave
   static_assert(WTN % 32 == 0, "GLU pairs need 32-row weight blocks per wave");
@@ -139,10 +156,6 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
   };
 
   f32x4 acc[TN][TM];
-#pragma unroll
-  for (int a = 0; a < TN; ++a)
-#pragma unroll
-    for (int b = 0; b < TM; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // epilogue operands, loaded before the K tiles so that they are the oldest
   // vector-memory operations (the vmcnt waits below only ever wait for older ones)
@@ -160,37 +173,66 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
       }
   }
 
-#pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) issue(s, s);
-
   const int fr = lane & 15, fq = lane >> 4, sw = lane & 7;
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + STAGES - 2 < nk)
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm((STAGES - 2) * LPS));
-    else
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    __syncthreads();
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-    const char* sa = smem + (kt % STAGES) * STAGE_BYTES;
-    const char* swt = sa + BM * ROW;
+  const int aoff = (wm * WTM + fr) * ROW, woff = BM * ROW + (wn * WTN + fr) * ROW;
+  // fragment t of the 32-deep half kk of the K tile in LDS buffer buf
+  auto fa_at = [&](int buf, int kk, int t) {
+    return *reinterpret_cast<const bf16x8*>(smem + buf * STAGE_BYTES + aoff + t * 16 * ROW + ((kk * 4 + fq) ^ sw) * 16);
+  };
+  auto fw_at = [&](int buf, int kk, int t) {
+    return *reinterpret_cast<const bf16x8*>(smem + buf * STAGE_BYTES + woff + t * 16 * ROW + ((kk * 4 + fq) ^ sw) * 16);
+  };
+  bf16x8 fa[TM], fw[TN];
+  // the products of one 32-deep half; each fragment is replaced by the same fragment of
+  // the half (nbuf, nkk) as soon as its last product has issued
+  auto half = [&](auto first, auto prefetch, int nbuf, int nkk) {
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int slot = ((kk * 4 + fq) ^ sw) * 16;
-      bf16x8 fa[TM], fw[TN];
+    for (int a = 0; a < TN; ++a) {
 #pragma unroll
-      for (int t = 0; t < TM; ++t)
-        fa[t] = *reinterpret_cast<const bf16x8*>(sa + (wm * WTM + t * 16 + fr) * ROW + slot);
-#pragma unroll
-      for (int t = 0; t < TN; ++t)
-        fw[t] = *reinterpret_cast<const bf16x8*>(swt + (wn * WTN + t * 16 + fr) * ROW + slot);
-#pragma unroll
-      for (int a = 0; a < TN; ++a)
-#pragma unroll
-        for (int b = 0; b < TM; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[a], fa[b], acc[a][b], 0, 0, 0);
+      for (int b = 0; b < TM; ++b) {
+        if constexpr (decltype(first)::value)
+          mfma_first(acc[a][b], fw[a], fa[b]);
+        else
+          mfma_acc(acc[a][b], fw[a], fa[b]);
+        if constexpr (decltype(prefetch)::value)
+          if (a == TN - 1) fa[b] = fa_at(nbuf, nkk, b);
+      }
+      if constexpr (decltype(prefetch)::value) fw[a] = fw_at(nbuf, nkk, a);
     }
+  };
+  using Yes = std::true_type;
+  using No = std::false_type;
+
+  // K tile 0 landed and published, K tile 1 in flight, the first half's fragments read
+  issue(0, 0);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  __syncthreads();
+  if (nk > 1) issue(1, 1);
+#pragma unroll
+  for (int t = 0; t < TM; ++t) fa[t] = fa_at(0, 0, t);
+#pragma unroll
+  for (int t = 0; t < TN; ++t) fw[t] = fw_at(0, 0, t);
+  half(Yes{}, Yes{}, 0, 1);
+  // iteration kt: the second half of K tile kt, then the first half of K tile kt + 1
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    const int buf = kt & 1;
+    // every wave has read K tile kt's buffer (its last fragments are the ones in
+    // registers) and K tile kt + 1 has landed: the buffer can take K tile kt + 2
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __syncthreads();
+    if (kt + 2 < nk) issue(kt + 2, buf);
+    half(No{}, Yes{}, buf ^ 1, 0);
+    half(No{}, Yes{}, buf ^ 1, 1);
   }
+  half(No{}, No{}, 0, 0);
+  // the last products must be written before any accumulator is read back: wait
+  // states after the final MFMA, then every accumulator passes through an empty asm
+  // that is ordered after the wait, so no read can be scheduled before it
+  asm volatile("s_nop 15\n s_nop 15\n s_nop 15" ::: "memory");
+#pragma unroll
+  for (int a = 0; a < TN; ++a)
+#pragma unroll
+    for (int b = 0; b < TM; ++b) asm volatile("" : "+a"(acc[a][b]));
 
   // lane holds C[n = nb + 4*(lane>>4) + j][m = mb + (lane & 15)]
   const int mw = m0 + wm * WTM + fr;
