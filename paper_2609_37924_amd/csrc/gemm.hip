@@ -365,7 +365,16 @@ hipError_t dispatch(DType dt, const GemmProblem& p, const EpiParams& e, hipStrea
   // the narrow (N = d_model) projections 64 x 64 at three blocks per CU
   const long t256 = (long)((p.M + 255) / 256) * ((p.N + 255) / 256);
   const long t128 = (long)((p.M + 127) / 128) * ((p.N + 127) / 128);
-  if ((p.M >= 4096 || p.N >= 16384) && t256 >= 128) return launch_bf16<256, 256, 2, 2, 4, 1, K>(p, e, s);
+  if ((p.M >= 4096 || p.N >= 16384) && t256 >= 128) {
+    if constexpr (K == EPI_GLU_SILU || K == EPI_GLU_GELU) {
+      // one block per CU runs in rounds of 256: 256 x 192 tiles (waves 64 x 96) win when
+      // they fill the last round better (26B-class gate/up, 1024 x 73728: 1152 tiles of
+      // 256 x 256 = 4.5 rounds -> 1536 of 256 x 192 = 6 rounds: 747 -> 669 us)
+      const long t192 = (long)((p.M + 255) / 256) * ((p.N + 191) / 192);
+      if ((t192 + 255) / 256 * 192 < (t256 + 255) / 256 * 256) return launch_bf16<256, 192, 2, 4, 2, 1, K>(p, e, s);
+    }
+    return launch_bf16<256, 256, 2, 2, 4, 1, K>(p, e, s);
+  }
   if (t128 >= 256) {
     // two blocks per CU run in rounds of 512; 192 x 128 tiles win when they need fewer
     // rounds for the same rows (e.g. 768 tiles of 128 x 128 = 1.5 rounds -> 512 of 192 x 128)
@@ -451,6 +460,28 @@ __global__ void resid_reduce_kernel(const float* part, int S, int M, int N, floa
   *r = x;
 }
 
+// K slices of a residual product with a very long K (at least 128 K tiles: the FFN
+// down projections) on 256 x 256 tiles, one block per CU: the S in [2, 16] (each slice
+// >= 16 K tiles, slices as even as the tile count allows) that minimises the time of
+// the grid, rounds of 256 blocks x the K tiles per slice, the smaller S on ties; 1 when
+// no split beats the unsplit grid.  26B-class FFN down (1024 x 4608 x 36864): S = 7,
+// 504 blocks in two rounds (468 -> 354 us against 128 x 128 tiles in 8 slices).
+int resid_slices256(int M, int N, int K) {
+  const long tiles = (long)((M + 255) / 256) * ((N + 255) / 256);
+  const int nk = K / 64;
+  if (nk < 128 || N % 4) return 1;
+  int best = 1;
+  double best_t = (double)((tiles + 255) / 256);
+  for (int S = 2; S <= 16 && nk / S >= 16; ++S) {
+    const double t = (double)((tiles * S + 255) / 256) / S;
+    if (t < best_t - 1e-9) {
+      best = S;
+      best_t = t;
+    }
+  }
+  return best;
+}
+
 // K slices of a residual product with a long K and fewer than two 128 x 128 tiles per
 // CU (512 resident blocks): the S in {2, 4, 8} (each slice >= 16 K tiles) whose grid
 // best fills whole rounds of 512 blocks, the smaller S on ties
@@ -475,7 +506,10 @@ int resid_slices(int M, int N, int K) {
 }  // namespace
 
 int gemm_split_slices(int M, int N, int K) { return split_slices(M, N, K); }
-int gemm_resid_slices(int M, int N, int K) { return resid_slices(M, N, K); }
+int gemm_resid_slices(int M, int N, int K) {
+  const int S256 = resid_slices256(M, N, K);
+  return S256 > 1 ? S256 : resid_slices(M, N, K);
+}
 
 hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
@@ -484,7 +518,8 @@ hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e
     if (splitk_scale(p, e, s, &err)) return err;
   }
   if (kind == EPI_RESID && dt == BF16 && e.part && !p.M_dev && p.K1 == p.K) {
-    const int S = resid_slices(p.M, p.N, p.K);
+    const int S256 = resid_slices256(p.M, p.N, p.K);
+    const int S = S256 > 1 ? S256 : resid_slices(p.M, p.N, p.K);
     if (S > 1) {  // the slices' products to part [S, M, N], then an ordered sum into resid
       GemmProblem q = p;
       q.ksplit = S;
@@ -492,7 +527,8 @@ hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e
       f.out = e.part;
       f.ldo = p.N;
       f.split_stride = (size_t)p.M * p.N;
-      hipError_t err = launch_bf16<128, 128, 2, 2, 2, 2, EPI_STORE_F32>(q, f, s);
+      hipError_t err = S256 > 1 ? launch_bf16<256, 256, 2, 2, 4, 1, EPI_STORE_F32>(q, f, s)
+                                : launch_bf16<128, 128, 2, 2, 2, 2, EPI_STORE_F32>(q, f, s);
       if (err != hipSuccess) return err;
       const long total = (long)p.M * (p.N / 4);
       hipLaunchKernelGGL(resid_reduce_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,

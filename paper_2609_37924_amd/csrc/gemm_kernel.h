@@ -121,7 +121,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
   // this lane's source row inside an 8-row group and its swizzled chunk
   const int lrow = lane >> 3, lchunk = (lane & 7) ^ (lane >> 3);
 
-  const int nk = p.K / 64 / p.ksplit, kt_base = blockIdx.y * nk;  // this block's K slice
+  // this block's K slice: K tiles [kt_base, kt_base + nk), slices as even as the tile
+  // count allows (they differ by at most one tile)
+  const int NKT = p.K / 64, kt_base = (int)((long)blockIdx.y * NKT / p.ksplit);
+  const int nk = (int)((long)(blockIdx.y + 1) * NKT / p.ksplit) - kt_base;
   // this lane's source rows, fixed over the K loop: a K tile only adds its offset.  A
   // second operand A2 (K columns from K1 on) gets its own row pointers, shifted by -K1.
   const bf16* arow1[LA];
