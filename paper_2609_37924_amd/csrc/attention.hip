@@ -1,7 +1,9 @@
 // Rotary embedding + head split, and bidirectional softmax attention.
 //
-// bf16 attention: one workgroup = 64 queries of one (row, head); 4 wave64s with
-// 16 queries each.  K (64 keys x dh) and V^T (dh x 64 keys) tiles move global -> LDS
+// bf16 attention: one workgroup = 64 queries of one batch row for the G query heads
+// that share one K/V head (grouped-query attention: G = H / Hkv), 4 G wave64s with 16
+// queries of one head each, so that every K/V tile brought into LDS serves all G heads.
+// K (64 keys x dh) and V^T (dh x 64 keys) tiles move global -> LDS
 // with global_load_lds_dwordx4 into a 2-stage ring (16-byte chunks swizzled by row).  Scores are computed transposed, S^T = K Q^T with
 // v_mfma_f32_16x16x32_bf16, so that each lane owns one query: the online-softmax
 // statistics live in the lane and the probabilities feed the O^T = V^T P^T MFMA
@@ -65,29 +67,40 @@ constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >>
 // 64 keys of 128 B.  Chunk c (8 bf16) of K row r sits in slot c ^ (r & 7), of V^T row r
 // in slot c ^ (r & 7) ^ ((r >> 3) & 1): the V^T fragments are read 8 bytes per lane, 32
 // lanes per LDS pass over rows r and r + 8, which the extra bit sends to other banks.
-template <int DH, int NS>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const bf16* K,
-                                                           const bf16* Vt, bf16* O, int H, int Hkv,
-                                                           int Lq, int Lk, int kv_cap,
-                                                           float scale_log2) {
-  constexpr int KT = 64;
+// G = 0: one query head per block for any head ratio (its K/V head floor(h Hkv / H)).
+template <int DH, int NS, int G>
+__global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf16_kernel(
+    const bf16* Q, const bf16* K, const bf16* Vt, bf16* O, int H, int Hkv, int Lq, int Lk, int kv_cap,
+    float scale_log2) {
+  constexpr int KT = 64, NW = 4 * (G > 0 ? G : 1);  // waves per block: 4 query strips x G heads
   constexpr int KBYTES = KT * DH * 2, VBYTES = DH * KT * 2, STAGE = KBYTES + VBYTES;
-  constexpr int LK = KBYTES / 1024 / 4, LV = VBYTES / 1024 / 4;  // load instructions per wave
+  constexpr int LK = KBYTES / 1024 / NW, LV = VBYTES / 1024 / NW;  // load instructions per wave
+  static_assert(LK * 1024 * NW == KBYTES && LV * 1024 * NW == VBYTES, "tile rows must split over the waves");
   constexpr int LPT = LK + LV;                                      // per wave per tile
   __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
   // wave index as a scalar: the K/V tile destinations in LDS are formed in scalar registers
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), grp = lane >> 4,
             fr = lane & 15;
-  // one block per (64-query tile, head, batch row), query tiles fastest: the tiles of a
-  // head, and the heads sharing a K/V head, run on one XCD and read K/V from its L2
+  // one block per (64-query tile, K/V head, batch row), query tiles fastest: the tiles of
+  // a K/V head run on one XCD and read K/V from its L2
   const int nqt = (Lq + 63) / 64;
   const int id = xcd_contiguous(blockIdx.x, gridDim.x);
-  const int qt = id % nqt, h = (id / nqt) % H, b = id / (nqt * H);
-  const int hk = (h * Hkv) / H;
+  int qt, h, hk, b;
+  if constexpr (G > 0) {
+    qt = id % nqt;
+    hk = (id / nqt) % Hkv;
+    b = id / (nqt * Hkv);
+    h = hk * G + wave / 4;  // query heads hk G .. hk G + G - 1 read K/V head hk
+  } else {
+    qt = id % nqt;
+    h = (id / nqt) % H;
+    b = id / (nqt * H);
+    hk = (h * Hkv) / H;
+  }
   const bf16* Kb = K + ((size_t)b * Hkv + hk) * kv_cap * DH;
   const bf16* Vb = Vt + ((size_t)b * Hkv + hk) * DH * kv_cap;
-  const int q = qt * 64 + wave * 16 + fr;
+  const int q = qt * 64 + (wave % 4) * 16 + fr;
   const bf16* Qr = Q + (((size_t)b * H + h) * Lq + min(q, Lq - 1)) * DH;
 
   bf16x8 qf[DH / 32];
@@ -95,20 +108,20 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
   for (int kc = 0; kc < DH / 32; ++kc) qf[kc] = *reinterpret_cast<const bf16x8*>(Qr + 32 * kc + 8 * grp);
 
   const int lrow = lane >> 3, lchunk = (lane & 7) ^ (lane >> 3);
-  const int lchunk_v = lchunk ^ (wave & 1);  // V^T rows 8 g + lrow with g = wave + 4 j
+  const int lchunk_v = lchunk ^ (wave & 1);  // V^T rows 8 g + lrow with g = wave + NW j (NW even)
   const int nt = (Lk + KT - 1) / KT;
   auto issue = [&](int t, int buf) {
     const int k0 = t * KT;
     char* sb = smem + buf * STAGE;
 #pragma unroll
     for (int j = 0; j < LK; ++j) {  // 8-row groups of the K planes
-      const int g = wave + 4 * j, plane = g / 8, r = (g % 8) * 8 + lrow;
+      const int g = wave + NW * j, plane = g / 8, r = (g % 8) * 8 + lrow;
       const bf16* src = Kb + (size_t)min(k0 + r, Lk - 1) * DH + plane * 64 + lchunk * 8;
       __builtin_amdgcn_global_load_lds((gbl_ptr)src, (lds_ptr)(sb + g * 1024), 16, 0, 0);
     }
 #pragma unroll
     for (int j = 0; j < LV; ++j) {  // 8-row groups of V^T
-      const int g = wave + 4 * j, r = g * 8 + lrow;
+      const int g = wave + NW * j, r = g * 8 + lrow;
       const bf16* src = Vb + (size_t)r * kv_cap + k0 + lchunk_v * 8;  // k0 + 64 <= kv_cap
       __builtin_amdgcn_global_load_lds((gbl_ptr)src, (lds_ptr)(sb + KBYTES + g * 1024), 16, 0, 0);
     }
@@ -146,7 +159,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
     if ((t + 1) * KT > Lk) {
       // last, partial tile: keys past the end get V = 0 so that p = 0 meets finite values
       char* svw = const_cast<char*>(sk + KBYTES);
-      for (int idx = tid; idx < DH * KT; idx += 256) {
+      for (int idx = tid; idx < DH * KT; idx += 64 * NW) {
         const int r = idx / KT, key = idx % KT;
         if (t * KT + key >= Lk) {
           const int slot = (key >> 3) ^ (r & 7) ^ ((r >> 3) & 1);
@@ -187,7 +200,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
     }
     mt = fmaxf(mt, xor16(mt));
     mt = fmaxf(mt, xor32(mt));
-    const float m_new = fmaxf(m_run, mt * scale_log2);  // scale_log2 > 0: the max commutes
+    // The probabilities are taken relative to a reference m_run that only moves when the
+    // tile's maximum exceeds it by more than 2^8 (in base 2): until then they stay below
+    // 256 (exact in bf16's exponent range) and the accumulators need no rescaling; the
+    // row sum l_run uses the same reference, so o / l is unchanged.
+    const float mt2 = mt * scale_log2;  // scale_log2 > 0: the max commutes
+    const bool move = mt2 > m_run + 8.f;  // also true on the first tile (m_run = -inf)
+    const float m_new = move ? mt2 : m_run;
     // raw v_exp_f32: results below 2^-126 flush to 0 (a probability that small adds nothing)
     const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
     float ps = 0.f;
@@ -201,8 +220,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q, const 
       }
     l_run = l_run * alpha + ps;
     m_run = m_new;
+    if (__builtin_amdgcn_ballot_w64(move))  // some lane of the wave moved its reference
 #pragma unroll
-    for (int d = 0; d < DH / 16; ++d) o[d] *= alpha;
+      for (int d = 0; d < DH / 16; ++d) o[d] *= alpha;
 #pragma unroll
     for (int kc2 = 0; kc2 < 2; ++kc2) {
       bf16x8 pf;
@@ -290,19 +310,28 @@ hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, voi
                      int Hkv, int Lq, int Lk, int kv_cap, int dh, hipStream_t s) {
   if (B * Lq == 0) return hipSuccess;
   if (dt == BF16) {
-    const dim3 grid(((Lq + 63) / 64) * H * B);
     const float sl2 = 1.4426950408889634f / sqrtf((float)dh);
-    if (dh == 64)
-      launch_timed(attn_bf16_kernel<64, 2>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
-                   static_cast<const bf16*>(K), static_cast<const bf16*>(Vt), static_cast<bf16*>(O), H, Hkv, Lq,
-                   Lk, kv_cap, sl2);
-    else if (dh == 128)
-      launch_timed(attn_bf16_kernel<128, 2>, grid, dim3(256), 0, s, static_cast<const bf16*>(Q),
-                   static_cast<const bf16*>(K), static_cast<const bf16*>(Vt), static_cast<bf16*>(O), H, Hkv, Lq,
-                   Lk, kv_cap, sl2);
-    else
-      return hipErrorInvalidValue;
-    return hipGetLastError();
+    const int nqt = (Lq + 63) / 64, G = H % Hkv == 0 ? H / Hkv : 0;
+    auto go = [&](auto kernel, int g) {
+      const dim3 grid(nqt * (g > 0 ? Hkv : H) * B), block(256 * (g > 0 ? g : 1));
+      launch_timed(kernel, grid, block, 0, s, static_cast<const bf16*>(Q), static_cast<const bf16*>(K),
+                   static_cast<const bf16*>(Vt), static_cast<bf16*>(O), H, Hkv, Lq, Lk, kv_cap, sl2);
+      return hipGetLastError();
+    };
+    // The query heads sharing a K/V head go to one block (G = 2 or 4 of them, the K/V
+    // tile split over the 4 G waves) only when the packed grid still gives every CU two
+    // blocks: packing divides the block count by G, and at the benchmark's shapes that
+    // leaves CUs idle (block workload, G = 4: 64 blocks of 16 waves, attention 47.8 ->
+    // 94.7 ms per generation; 26B-class, G = 2: 256 blocks of 8 waves, no faster).
+    const bool pack = (long)nqt * Hkv * B >= 512;
+    if (dh == 64) return G == 1 ? go(attn_bf16_kernel<64, 2, 1>, 1) : go(attn_bf16_kernel<64, 2, 0>, 0);
+    if (dh == 128) {
+      if (G == 1) return go(attn_bf16_kernel<128, 2, 1>, 1);
+      if (pack && G == 2) return go(attn_bf16_kernel<128, 2, 2>, 2);
+      if (pack && G == 4) return go(attn_bf16_kernel<128, 2, 4>, 4);
+      return go(attn_bf16_kernel<128, 2, 0>, 0);
+    }
+    return hipErrorInvalidValue;
   }
   const dim3 grid((Lq + 3) / 4, H, B);
   launch_timed(attn_f32_kernel, grid, dim3(256), (uint32_t)(4 * Lk * sizeof(float)), s,

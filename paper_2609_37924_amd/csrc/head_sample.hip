@@ -201,8 +201,12 @@ __global__ __launch_bounds__(256) void finalize_kernel(const SamplePart* part, i
 
 hipError_t head_sample(const GemmProblem& p, const EpiParams& e, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
-  // 128 x 64 tiles on 4 x 1 waves (64-column wave strips), three blocks per CU (48 KB of
-  // LDS each): a block's VALU-heavy epilogue overlaps the others' MFMA main loops
+  // Large vocabularies: 128 x 128 tiles on 2 x 2 waves (64 x 64 per wave, a third less
+  // LDS traffic per product), two blocks per CU; 26B-class head (V = 262144): 507 -> 407
+  // ms per generation against the tiles below.  Smaller ones: 128 x 64 tiles on 4 x 1
+  // waves, three blocks per CU (48 KB of LDS each), so that a block's VALU-heavy
+  // epilogue overlaps the others' MFMA main loops (1 % ahead on V = 32768).
+  if (p.N >= 65536) return launch_bf16<128, 128, 2, 2, 2, 2, EPI_SAMPLE>(p, e, s);
   return launch_bf16<128, 64, 2, 4, 1, 3, EPI_SAMPLE>(p, e, s);
 }
 
