@@ -55,7 +55,8 @@ def build(jobs=8, verbose=False):
             if e:
                 print(e)
     tmp = OUT + ".tmp"
-    cmd = [hipcc(), "-shared", "-o", tmp, "--offload-arch=gfx950"] + [o for o, _ in results]
+    cmd = [hipcc(), "-shared", "-o", tmp, "--offload-arch=gfx950"] + [o for o, _ in results] + \
+        ["-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx", "-Wl,-rpath,/opt/rocm/lib"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stderr)
@@ -63,6 +64,37 @@ def build(jobs=8, verbose=False):
     return OUT
 
 
+# Host-side sanitizer build: the same sources with the host code instrumented by
+# AddressSanitizer and UndefinedBehaviorSanitizer (the device code is not), for running
+# the library's argument validation on the CPU under the sanitizers.
+SAN_OUT = os.path.join(ROOT, "_build", "san", "libtadm_san.so")
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address,undefined", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def build_host_sanitized(jobs=8):
+    objdir = os.path.join(ROOT, "_build", "san")
+    os.makedirs(objdir, exist_ok=True)
+
+    def one(src):
+        obj = os.path.join(objdir, src.replace(".hip", ".o"))
+        cmd = [hipcc(), "-c", os.path.join(HERE, src), "-o", obj] + flags() + EXTRA.get(src, []) + SAN_FLAGS
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc (host sanitizers) failed on {src}:\n{r.stderr}")
+        return obj
+
+    with ThreadPoolExecutor(max_workers=jobs) as ex:
+        objs = list(ex.map(one, SOURCES))
+    cmd = [hipcc(), "-shared", "-o", SAN_OUT, "--offload-arch=gfx950"] + objs + SAN_FLAGS + \
+        ["-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx", "-Wl,-rpath,/opt/rocm/lib"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("link (host sanitizers) failed:\n" + r.stderr)
+    return SAN_OUT
+
+
 if __name__ == "__main__":
     jobs = int(sys.argv[sys.argv.index("--jobs") + 1]) if "--jobs" in sys.argv else 8
     print(build(jobs, verbose=True))
+    if "--sanitize" in sys.argv:
+        print(build_host_sanitized(jobs))

@@ -154,7 +154,9 @@ __global__ __launch_bounds__(256) void finalize_kernel(const SamplePart* part, i
   __shared__ Cand s_c[4];
   __shared__ long long s_S[4];
   const int j = blockIdx.x, b = blockIdx.y, row = b * Lc + j;
-  if (canvas[(size_t)b * L + off + j] != mask_id) {
+  // not masked, or masked beyond the rows the head computed (row_map -1): not sampled,
+  // so the selection leaves it masked; no partial of another step is ever read
+  if (canvas[(size_t)b * L + off + j] != mask_id || row_map[row] < 0) {
     if (threadIdx.x == 0) {
       choice[row] = -1;
       conf[row] = -INFINITY;

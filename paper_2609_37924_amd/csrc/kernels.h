@@ -178,8 +178,9 @@ hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, voi
 
 // ---- sampler (sampler.hip)
 // List of masked canvas positions: idx[r] = b * Lc + j for the r-th masked entry
-// (row-major order), row_map[b * Lc + j] = r or -1, *count = number of entries.
-hipError_t compact_masked(const int32_t* canvas, int B, int L, int canvas_off, int mask_id,
+// (row-major order), row_map[b * Lc + j] = r or -1, *count = number of entries; only
+// the first `bound` masked entries get a row (the rest row_map -1, count <= bound).
+hipError_t compact_masked(const int32_t* canvas, int B, int L, int canvas_off, int mask_id, int bound,
                           int32_t* idx, int32_t* row_map, int* count, hipStream_t s);
 // Vocabulary projection of the masked rows with the sampler in the epilogue (bf16):
 // p is the head GEMM (M = compacted masked rows, M_dev their device count, N = V);

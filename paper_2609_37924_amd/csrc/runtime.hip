@@ -15,6 +15,8 @@
 #include <string>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "../../include/tadm.h"
 #include "kernels.h"
 
@@ -340,7 +342,25 @@ static bool single_kernel_stage(int stage) {
 // Stages nest (a kernel stage inside a layer stage); each end closes the latest begin.
 // multi: a single-kernel stage that this time launches more than one kernel (events
 // are recorded around its launches instead)
+// The method's parts (S, A, Phi, D, head, sampler, selection, context pass) also open a
+// roctx range, so that a trace of the host thread (rocprofv3 --marker-trace) shows where
+// each part of a step was enqueued; the per-kernel stages do not.
+static const char* range_name(int stage) {
+  switch (stage) {
+    case TADM_STAGE_EMBED: return "tadm S: shared network";
+    case TADM_STAGE_ANCHOR: return "tadm A: anchor network";
+    case TADM_STAGE_FUSION: return "tadm Phi: fusion";
+    case TADM_STAGE_DENOISE: return "tadm D: denoiser";
+    case TADM_STAGE_HEAD: return "tadm head";
+    case TADM_STAGE_SAMPLE: return "tadm sampler";
+    case TADM_STAGE_SELECT: return "tadm unmask";
+    case TADM_STAGE_CONTEXT: return "tadm context pass";
+    default: return nullptr;
+  }
+}
+
 static tadm_status prof_begin(tadm_model* m, int stage, bool multi = false) {
+  if (const char* r = range_name(stage)) roctxRangePushA(r);
   if (!((m->prof_mask >> stage) & 1)) return TADM_OK;
   OpenStage o{stage, nullptr, nullptr};
   TRY(prof_event(m, &o.a));
@@ -355,6 +375,7 @@ static tadm_status prof_begin(tadm_model* m, int stage, bool multi = false) {
 }
 
 static tadm_status prof_end(tadm_model* m, int stage) {
+  if (range_name(stage)) roctxRangePop();
   if (!((m->prof_mask >> stage) & 1) || m->open.empty() || m->open.back().stage != stage) return TADM_OK;
   OpenStage o = m->open.back();
   m->open.pop_back();
@@ -1285,7 +1306,7 @@ static tadm_status denoise_impl(tadm_model* m, const tadm_context* ctx, const in
   if (all_rows) {
     HIPCHK(rms_norm(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, B * Lc, d, Lc, L, off, s.xn, m->stream));
   } else {
-    HIPCHK(compact_masked(canvas, B, L, off, cf.vocab, s.cidx, s.row_map, s.count, m->stream));
+    HIPCHK(compact_masked(canvas, B, L, off, cf.vocab, rows, s.cidx, s.row_map, s.count, m->stream));
     HIPCHK(rms_norm_gather(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, s.cidx, s.count, rows, Lc, L,
                            off, d, s.xn, m->stream));
   }
@@ -1639,7 +1660,7 @@ tadm_status tadm_train_loss(tadm_model* m, const int32_t* x_dev, int32_t B, int3
   TRY(prof_end(m, TADM_STAGE_FUSION));
   TRY(prof_begin(m, TADM_STAGE_DENOISE));
   TRY(run_part(m, cf.n_shared + cf.n_anchor, cf.n_denoise, s.x, B, L, 0, nullptr, prenormed));
-  HIPCHK(compact_masked(zt, B, L, 0, mask, s.cidx, s.row_map, s.count, m->stream));
+  HIPCHK(compact_masked(zt, B, L, 0, mask, B * L, s.cidx, s.row_map, s.count, m->stream));
   HIPCHK(rms_norm_gather(m->dt, s.x, m->Wf(m->lay.final_norm), cf.rms_eps, s.cidx, s.count, N, L, L, 0, d, s.xn,
                          m->stream));
   TRY(prof_end(m, TADM_STAGE_DENOISE));

@@ -14,6 +14,8 @@
 //    rint(exp(l'_v - m_g) 2^40), S = sum_g rint(float(S_g) exp(m_g - m)); every sum is
 //    over integers, so any reduction order (and any tiling) gives the same bits.
 //  * ranking: confidence descending, then position ascending.
+#include <cfloat>
+
 #include "common.h"
 #include "kernels.h"
 #include "sampler_math.h"
@@ -58,7 +60,8 @@ __global__ __launch_bounds__(256) void sample_kernel(const float* logits, const 
   __shared__ long long s_sum[4];
   const int j = blockIdx.x, b = blockIdx.y;
   const int row = b * Lc + j;
-  if (canvas[(size_t)b * L + off + j] != mask_id) {
+  // not masked, or masked without a logits row (beyond the rows computed): not sampled
+  if (canvas[(size_t)b * L + off + j] != mask_id || (row_map && row_map[row] < 0)) {
     if (threadIdx.x == 0) {
       choice[row] = -1;
       conf[row] = -INFINITY;
@@ -237,7 +240,7 @@ __global__ __launch_bounds__(NUC_THREADS) void nucleus_kernel(const float* logit
   __shared__ unsigned long long s_u[NW];
   __shared__ unsigned long long s_sel[3];
   const int j = blockIdx.x, b = blockIdx.y, row = b * Lc + j;
-  if (canvas[(size_t)b * L + off + j] != mask_id) return;
+  if (canvas[(size_t)b * L + off + j] != mask_id || (row_map && row_map[row] < 0)) return;
   const float* lg = logits + (size_t)(row_map ? row_map[row] : row) * V;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // cached entry i of this thread: v = 4 (tid + NUC_THREADS (i / 4)) + i % 4
@@ -388,8 +391,11 @@ __global__ __launch_bounds__(NUC_THREADS) void nucleus_kernel(const float* logit
 }
 
 // One workgroup of 1024 threads scans every canvas entry in row-major order.
+// Masked canvas positions in order get rows 0, 1, ... (idx: row -> position, row_map:
+// position -> row or -1); rows from `bound` on are not assigned (row_map -1): a caller
+// that sized its work for `bound` rows never reads a row it did not compute.
 __global__ __launch_bounds__(1024) void compact_kernel(const int32_t* canvas, int B, int L, int off,
-                                                       int mask_id, int32_t* idx, int32_t* row_map,
+                                                       int mask_id, int bound, int32_t* idx, int32_t* row_map,
                                                        int* count) {
   __shared__ int wsum[16];
   __shared__ int base;
@@ -409,8 +415,9 @@ __global__ __launch_bounds__(1024) void compact_kernel(const int32_t* canvas, in
     for (int w = 0; w < wave; ++w) woff += wsum[w];
     const int r = base + woff + before;
     if (c < n) {
-      row_map[c] = m ? r : -1;
-      if (m) idx[r] = c;
+      const bool kept = m && r < bound;
+      row_map[c] = kept ? r : -1;
+      if (kept) idx[r] = c;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -420,7 +427,7 @@ __global__ __launch_bounds__(1024) void compact_kernel(const int32_t* canvas, in
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) *count = base;
+  if (threadIdx.x == 0) *count = min(base, bound);
 }
 
 // One workgroup of 1024 threads per row; rank by (conf desc, position asc) among the
@@ -440,9 +447,11 @@ __global__ __launch_bounds__(SELECT_THREADS) void select_kernel(const int32_t* c
   const int b = blockIdx.x, tid = threadIdx.x;
   const int Lc16 = (Lc + 15) & ~15, quarter = Lc16 / 4;  // each quarter: whole float4s
   float cnt = 0.f;
+  // the candidates are the masked positions that were sampled (choice >= 0); a
+  // candidate's confidence is at least -FLT_MAX, so it ranks ahead of every other slot
   for (int p = tid; p < Lc16; p += SELECT_THREADS) {
-    const bool m = p < Lc && canvas[(size_t)b * L + off + p] == mask_id;
-    sc[p] = m ? conf[(size_t)b * Lc + p] : -INFINITY;
+    const bool m = p < Lc && canvas[(size_t)b * L + off + p] == mask_id && choice[(size_t)b * Lc + p] >= 0;
+    sc[p] = m ? fmaxf(conf[(size_t)b * Lc + p], -FLT_MAX) : -INFINITY;
     cnt += m ? 1.f : 0.f;
   }
   const int n_masked = (int)block_sum(cnt, red);  // exact: counts < 2^24; ends with a barrier
@@ -452,7 +461,7 @@ __global__ __launch_bounds__(SELECT_THREADS) void select_kernel(const int32_t* c
     const int l = l0 + (tid >> 2), p = l - off;
     const bool mine = l < L;
     const int t = mine ? canvas[(size_t)b * L + l] : 0;
-    const bool cand = mine && p >= 0 && p < Lc && t == mask_id && n > 0;
+    const bool cand = mine && p >= 0 && p < Lc && t == mask_id && n > 0 && sc[p] != -INFINITY;
     int rank = 0;
     if (__any(cand)) {
       const float cp = cand ? sc[p] : 0.f;
@@ -502,9 +511,9 @@ hipError_t remask_update(const int32_t* canvas, const int32_t* choice, int B, in
   return hipGetLastError();
 }
 
-hipError_t compact_masked(const int32_t* canvas, int B, int L, int canvas_off, int mask_id,
+hipError_t compact_masked(const int32_t* canvas, int B, int L, int canvas_off, int mask_id, int bound,
                           int32_t* idx, int32_t* row_map, int* count, hipStream_t s) {
-  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, s, canvas, B, L, canvas_off, mask_id, idx,
+  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, s, canvas, B, L, canvas_off, mask_id, bound, idx,
                      row_map, count);
   return hipGetLastError();
 }

@@ -102,8 +102,9 @@ __global__ __launch_bounds__(256) void entropy_kernel(const float* logits, int V
   if (am.v >= V) am.v = 0;  // only with non-finite logits
   const float m = lg[am.v] * inv_temp;  // max l' (rounding is monotone)
 
-  // A and B as float64 sums of their integer terms (each < 2^41, at most 2^8 of them per
-  // thread): exact, then converted once
+  // A and B as float64 sums of their integer terms (each < 2^41, V / 256 of them per
+  // thread: 1024 at V = 262144, so every partial sum stays below 2^51 < 2^53): exact,
+  // then converted once
   double Ad = 0.0, Bd = 0.0;
   Top2 top;
   for (int q = tid; 4 * q < V; q += 256) {
