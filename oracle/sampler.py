@@ -93,15 +93,23 @@ LN2_HI = _f(0x3F317200)      # 0.693145751953125 (15 significant bits)
 LN2_LO = _f(0x35BFBE8E)      # ln 2 - LN2_HI
 INV_LN2 = _f(0x3FB8AA3B)     # 1/ln 2
 SQRT2_BITS = 0x3FB504F3      # float32 nearest sqrt(2)
-# log: s * (2 + 2/3 z + 2/5 z^2 + 2/7 z^3 + 2/9 z^4 + 2/11 z^5), z = s^2
+# log: 2 atanh(s) = 2 s + s R(z), z = s^2, R = 2/3 z + 2/5 z^2 + 2/7 z^3 + 2/9 z^4 + 2/11 z^5
+# (the atanh series), coefficients from the highest down
 LOG_C = [_f(0x3E3A2E8C), _f(0x3E638E39), _f(0x3E924925), _f(0x3ECCCCCD), _f(0x3F2AAAAB)]
-# exp: 1 + r + r^2/2 + ... + r^7/7!
-EXP_C = [_f(0x39500D01), _f(0x3AB60B61), _f(0x3C088889), _f(0x3D2AAAAB), _f(0x3E2AAAAB)]
+# exp: e^r = 1 + r + r^2 c(r), c = 1/2 + r/6 + ... + r^5/7! (Taylor), from the highest down
+EXP_C = [_f(0x39500D01), _f(0x3AB60B61), _f(0x3C088889), _f(0x3D2AAAAB), _f(0x3E2AAAAB), F32(0.5)]
 EXP_CUTOFF = F32(-30.0)
 
 
 def log32(x):
-    """Natural log of positive normal float32 values, in float32 arithmetic."""
+    """Natural log of positive normal float32 values, in float32 arithmetic (within
+    1 ulp: the exhaustive sweep of the tests).
+
+    x = 2^e m with m in [sqrt(1/2), sqrt(2)), f = m - 1 (exact), s = f / (2 + f), and
+    log(1 + f) = 2 atanh(s) = 2 s + s R(s^2).  Since 2 s = f - s f and
+    s f = f^2 / 2 - s f^2 / 2, the sum is taken as f - (f^2/2 - s (f^2/2 + R)): the exact
+    f leads and every rounded term is small beside it (the arrangement of Sun's fdlibm
+    logarithm).  e ln 2 is added in two parts (Cody-Waite)."""
     x = np.asarray(x, dtype=F32)
     bits = x.view(U32)
     e = (bits >> U32(23)).astype(np.int32) - 127
@@ -113,27 +121,34 @@ def log32(x):
     f = m - F32(1.0)
     s = f / (F32(2.0) + f)
     z = s * s
-    p = LOG_C[0]
-    for c in LOG_C[1:]:
-        p = p * z + c
-    p = p * z + F32(2.0)
-    t = s * p
+    c = LOG_C[0]
+    for k in LOG_C[1:]:
+        c = c * z + k
+    R = z * c
+    hfsq = F32(0.5) * f * f
     ef = e.astype(F32)
-    return (ef * LN2_HI + (ef * LN2_LO + t)).astype(F32)
+    return (ef * LN2_HI - ((hfsq - (s * (hfsq + R) + ef * LN2_LO)) - f)).astype(F32)
 
 
 def exp32(y):
-    """exp(y) for float32 y <= 0, in float32 arithmetic; 0 below -30."""
+    """exp(y) for float32 y <= 0, in float32 arithmetic (within 1 ulp: the exhaustive
+    sweep of the tests); 0 below -30.
+
+    k = rint(y / ln 2), r = y - k ln 2 with ln 2 in two parts (Cody-Waite): rh = y - k
+    ln2_hi is exact, r = rh - k ln2_lo.  e^r = 1 + r + r^2 c(r), summed as
+    1 + (rh + (r^2 c(r) - k ln2_lo)) so that the rounding of r does not enter the linear
+    term; then times 2^k (exact)."""
     y = np.asarray(y, dtype=F32)
     yc = np.maximum(y, EXP_CUTOFF)
     k = np.rint(yc * INV_LN2).astype(F32)
-    r = (yc - k * LN2_HI) - k * LN2_LO
-    p = EXP_C[0]
-    for c in EXP_C[1:]:
-        p = p * r + c
-    p = p * r + F32(0.5)
-    p = p * r + F32(1.0)
-    p = p * r + F32(1.0)
+    rh = yc - k * LN2_HI
+    kl = k * LN2_LO
+    r = rh - kl
+    c = EXP_C[0]
+    for q in EXP_C[1:]:
+        c = c * r + q
+    q = (r * r) * c
+    p = F32(1.0) + (rh + (q - kl))
     scale = ((k.astype(np.int32) + 127).astype(U32) << U32(23)).view(F32)
     return np.where(y < EXP_CUTOFF, F32(0.0), p * scale).astype(F32)
 

@@ -40,6 +40,10 @@ __device__ __forceinline__ float uniform01(uint32_t x) {
   return __uint_as_float((x >> 9) | 0x3F800000u) - bits_f(0x3F7FFFFFu);
 }
 
+// log(x) for positive normal x (within 1 ulp): x = 2^e m, m in [sqrt(1/2), sqrt(2)),
+// f = m - 1 (exact), s = f / (2 + f), log(1 + f) = 2 atanh(s) = 2 s + s R(s^2) with R
+// the atanh series; taken as f - (f^2/2 - s (f^2/2 + R)) so that the exact f leads (the
+// arrangement of Sun's fdlibm logarithm), e ln 2 added in two parts (Cody-Waite).
 __device__ __forceinline__ float own_log(float x) {
   const float LN2_HI = bits_f(0x3F317200u), LN2_LO = bits_f(0x35BFBE8Eu);
   const uint32_t bits = __float_as_uint(x);
@@ -53,32 +57,41 @@ __device__ __forceinline__ float own_log(float x) {
   const float f = m - 1.0f;
   const float s = f / (2.0f + f);
   const float z = s * s;
-  float p = bits_f(0x3E3A2E8Cu);       // 2/11
-  p = p * z + bits_f(0x3E638E39u);     // 2/9
-  p = p * z + bits_f(0x3E924925u);     // 2/7
-  p = p * z + bits_f(0x3ECCCCCDu);     // 2/5
-  p = p * z + bits_f(0x3F2AAAABu);     // 2/3
-  p = p * z + 2.0f;
-  const float t = s * p;
+  float c = bits_f(0x3E3A2E8Cu);       // 2/11
+  c = c * z + bits_f(0x3E638E39u);     // 2/9
+  c = c * z + bits_f(0x3E924925u);     // 2/7
+  c = c * z + bits_f(0x3ECCCCCDu);     // 2/5
+  c = c * z + bits_f(0x3F2AAAABu);     // 2/3
+  const float R = z * c;
+  const float hfsq = 0.5f * f * f;
   const float ef = (float)e;
-  return ef * LN2_HI + (ef * LN2_LO + t);
+  return ef * LN2_HI - ((hfsq - (s * (hfsq + R) + ef * LN2_LO)) - f);
+}
+
+// e^r = 1 + r + r^2 c(r) with c the Taylor series to r^5/7!, r = y - k ln 2 (Cody-Waite:
+// rh = y - k ln2_hi exact, r = rh - k ln2_lo), summed as 1 + (rh + (r^2 c - k ln2_lo)) so
+// that the rounding of r does not enter the linear term (within 1 ulp for y in [-30, 0]).
+__device__ __forceinline__ float own_exp_core(float y, int bias) {
+  const float LN2_HI = bits_f(0x3F317200u), LN2_LO = bits_f(0x35BFBE8Eu);
+  const float k = rintf(y * bits_f(0x3FB8AA3Bu));
+  const float rh = y - k * LN2_HI;
+  const float kl = k * LN2_LO;
+  const float r = rh - kl;
+  float c = bits_f(0x39500D01u);       // 1/5040
+  c = c * r + bits_f(0x3AB60B61u);     // 1/720
+  c = c * r + bits_f(0x3C088889u);     // 1/120
+  c = c * r + bits_f(0x3D2AAAABu);     // 1/24
+  c = c * r + bits_f(0x3E2AAAABu);     // 1/6
+  c = c * r + 0.5f;
+  const float q = (r * r) * c;
+  const float p = 1.0f + (rh + (q - kl));
+  const float scale = __uint_as_float((uint32_t)((int)k + 127 + bias) << 23);
+  return p * scale;
 }
 
 __device__ __forceinline__ float own_exp(float y) {
   if (y < -30.0f) return 0.0f;
-  const float LN2_HI = bits_f(0x3F317200u), LN2_LO = bits_f(0x35BFBE8Eu);
-  const float k = rintf(y * bits_f(0x3FB8AA3Bu));
-  const float r = (y - k * LN2_HI) - k * LN2_LO;
-  float p = bits_f(0x39500D01u);       // 1/5040
-  p = p * r + bits_f(0x3AB60B61u);     // 1/720
-  p = p * r + bits_f(0x3C088889u);     // 1/120
-  p = p * r + bits_f(0x3D2AAAABu);     // 1/24
-  p = p * r + bits_f(0x3E2AAAABu);     // 1/6
-  p = p * r + 0.5f;
-  p = p * r + 1.0f;
-  p = p * r + 1.0f;
-  const float scale = __uint_as_float((uint32_t)((int)k + 127) << 23);
-  return p * scale;
+  return own_exp_core(y, 0);
 }
 
 // own_exp without a branch: the same rounded operations for y >= -30 (and NaN), and 0 below,
@@ -94,20 +107,8 @@ __device__ __forceinline__ float own_exp_sel(float y) {
 // (its results lie in [e^-30, e^0.35] or are 0).
 __device__ __forceinline__ float own_exp_sel_2p40(float y) {
   const bool under = y < -30.0f;
-  const float yy = under ? -30.0f : y;
-  const float LN2_HI = bits_f(0x3F317200u), LN2_LO = bits_f(0x35BFBE8Eu);
-  const float k = rintf(yy * bits_f(0x3FB8AA3Bu));
-  const float r = (yy - k * LN2_HI) - k * LN2_LO;
-  float p = bits_f(0x39500D01u);
-  p = p * r + bits_f(0x3AB60B61u);
-  p = p * r + bits_f(0x3C088889u);
-  p = p * r + bits_f(0x3D2AAAABu);
-  p = p * r + bits_f(0x3E2AAAABu);
-  p = p * r + 0.5f;
-  p = p * r + 1.0f;
-  p = p * r + 1.0f;
-  const float scale = __uint_as_float((uint32_t)((int)k + 127 + 40) << 23);
-  return under ? 0.0f : p * scale;
+  const float e = own_exp_core(under ? -30.0f : y, 40);
+  return under ? 0.0f : e;
 }
 
 struct Best {
