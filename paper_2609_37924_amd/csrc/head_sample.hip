@@ -208,7 +208,7 @@ hipError_t head_sample(const GemmProblem& p, const EpiParams& e, hipStream_t s) 
   // ms per generation against the tiles below.  Smaller ones: 128 x 64 tiles on 4 x 1
   // waves, three blocks per CU (48 KB of LDS each), so that a block's VALU-heavy
   // epilogue overlaps the others' MFMA main loops (1 % ahead on V = 32768).
-  if (p.N >= 65536) return launch_bf16<128, 128, 2, 2, 2, 2, EPI_SAMPLE>(p, e, s);
+  if (p.N >= 40000) return launch_bf16<128, 128, 2, 2, 2, 2, EPI_SAMPLE>(p, e, s);
   return launch_bf16<128, 64, 2, 4, 1, 3, EPI_SAMPLE>(p, e, s);
 }
 
