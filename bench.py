@@ -55,6 +55,8 @@ def parse():
                     help="print per-kernel HBM traffic from two rocprofv3 --pmc runs (FETCH_SIZE, then "
                          "WRITE_SIZE) and, given a third run with MfmaUtil, the MFMA busy share; then exit")
     ap.add_argument("--command", default="", help="command line quoted in a rendered summary")
+    ap.add_argument("--run-args", action="store_true",
+                    help="print the workload as key=value arguments of the native tadm_run program and exit")
     return ap.parse_args()
 
 
@@ -283,6 +285,21 @@ def render_counter_summary(fetch_dir, write_dir, mfma_dir=None, command=""):
         print(f"      ({desc}: {len(fk)} dispatches, {b / 1e6:.3f} MB per launch)")
 
 
+def run_args(config, K):
+    """The workload as key=value arguments of paper_2609_37924_amd/tadm_run, the native
+    program that runs generations through the C ABI (no Python in the process)."""
+    import synth
+
+    cfg = synth.get_config(config)
+    enums = {"ffn_kind": {"gelu": 0, "swiglu": 1, "geglu": 2}, "fusion_kind": {"gated_mlp": 0, "paired": 1},
+             "dtype": {"f32": 0, "bf16": 1}}
+    keys = ("vocab", "d_model", "n_heads", "n_kv_heads", "head_dim", "d_ffn", "ffn_kind", "n_shared", "n_anchor",
+            "n_denoise", "fusion_kind", "fusion_rank", "paired_heads", "dtype", "rms_eps", "ln_eps", "rope_theta",
+            "batch", "prompt_len", "gen_len", "block_len", "T")
+    out = [f"{k}={enums[k][cfg[k]] if k in enums else cfg[k]}" for k in keys]
+    return out + [f"K={K}", f"seed={cfg['sampler_seed']}", f"temperature={cfg['temperature']}"]
+
+
 def workload_name(cfg):
     return (f"{cfg['name']}: d{cfg['d_model']} {cfg['n_heads']}x{cfg['head_dim']} heads "
             f"({cfg['n_kv_heads']} kv) {cfg['ffn_kind']}{cfg['d_ffn']} V{cfg['vocab']}, "
@@ -454,6 +471,9 @@ def main():
         return
     if args.render_counters:
         render_counter_summary(*args.render_counters[:3], command=args.command)
+        return
+    if args.run_args:
+        print(" ".join(run_args(args.config, args.K)))
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: the path runs on a single MI355X "

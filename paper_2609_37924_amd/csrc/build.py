@@ -61,7 +61,24 @@ def build(jobs=8, verbose=False):
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stderr)
     os.replace(tmp, OUT)
+    build_run()
     return OUT
+
+
+# tadm_run: a native program that runs whole generations through the C ABI (linked
+# against the library next to it)
+RUN_OUT = os.path.join(PKG, "tadm_run")
+
+
+def build_run():
+    tmp = RUN_OUT + ".tmp"
+    cmd = [hipcc(), os.path.join(HERE, "tadm_run.hip"), "-o", tmp] + flags() + \
+        ["-L", PKG, "-l:libtadm.so", "-Wl,-rpath,$ORIGIN"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed on tadm_run.hip:\n" + r.stderr)
+    os.replace(tmp, RUN_OUT)
+    return RUN_OUT
 
 
 # Host-side sanitizer build: the same sources with the host code instrumented by

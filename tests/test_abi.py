@@ -132,3 +132,22 @@ def test_loop_sampler_rejects_bad_schedules():
         st = tadm.lib.tadm_generate_sampler(None, None, 1, 0, 8, 4, 1, 8, 0, 1.0, C.byref(smp), None)
         assert st != 0
         assert re.search(rb"loop schedule|eta", tadm.lib.tadm_last_error()), bad
+
+
+RUN = os.path.join(os.path.dirname(os.path.dirname(__file__)), "paper_2609_37924_amd", "tadm_run")
+
+
+def test_native_driver_rejects_bad_arguments_before_device_work():
+    """tadm_run (the native program over the C ABI) checks its arguments before it
+    touches the GPU: these run on a host without one."""
+    import subprocess
+
+    if not os.path.exists(RUN):
+        pytest.skip("tadm_run not built")
+    for argv, msg in (([], "missing batch"), (["foo"], "bad argument"),
+                      (["batch=1", "prompt_len=0", "gen_len=8", "T=0", "vocab=8", "d_model=8", "n_heads=1",
+                        "head_dim=8", "d_ffn=8", "n_anchor=1", "n_denoise=1"], "must be positive"),
+                      (["batch=x"], "bad value")):
+        r = subprocess.run([RUN] + argv, capture_output=True, text=True, timeout=60)
+        assert r.returncode == 1, (argv, r.returncode, r.stderr)
+        assert msg in r.stderr, (argv, r.stderr)
