@@ -68,7 +68,10 @@ constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >>
 // in slot c ^ (r & 7) ^ ((r >> 3) & 1): the V^T fragments are read 8 bytes per lane, 32
 // lanes per LDS pass over rows r and r + 8, which the extra bit sends to other banks.
 // G = 0: one query head per block for any head ratio (its K/V head floor(h Hkv / H)).
-template <int DH, int NS, int G>
+// QS: query strips of 16 per wave; the block's query tile is 64 QS queries (strip s of
+// wave w: queries 64 s + 16 w + [0, 16)), and every K and V^T fragment read from LDS
+// feeds QS products, so a wave reads the K/V tile once for 16 QS queries.
+template <int DH, int NS, int G, int QS>
 __global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf16_kernel(
     const bf16* Q, const bf16* K, const bf16* Vt, bf16* O, int H, int Hkv, int Lq, int Lk, int kv_cap,
     float scale_log2) {
@@ -84,7 +87,7 @@ __global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf
             fr = lane & 15;
   // one block per (64-query tile, K/V head, batch row), query tiles fastest: the tiles of
   // a K/V head run on one XCD and read K/V from its L2
-  const int nqt = (Lq + 63) / 64;
+  const int nqt = (Lq + 64 * QS - 1) / (64 * QS);
   const int id = xcd_contiguous(blockIdx.x, gridDim.x);
   int qt, h, hk, b;
   if constexpr (G > 0) {
@@ -100,12 +103,15 @@ __global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf
   }
   const bf16* Kb = K + ((size_t)b * Hkv + hk) * kv_cap * DH;
   const bf16* Vb = Vt + ((size_t)b * Hkv + hk) * DH * kv_cap;
-  const int q = qt * 64 + (wave % 4) * 16 + fr;
-  const bf16* Qr = Q + (((size_t)b * H + h) * Lq + min(q, Lq - 1)) * DH;
-
-  bf16x8 qf[DH / 32];
+  int q[QS];
+  bf16x8 qf[QS][DH / 32];
 #pragma unroll
-  for (int kc = 0; kc < DH / 32; ++kc) qf[kc] = *reinterpret_cast<const bf16x8*>(Qr + 32 * kc + 8 * grp);
+  for (int u = 0; u < QS; ++u) {
+    q[u] = qt * 64 * QS + u * 64 + (wave % 4) * 16 + fr;
+    const bf16* Qr = Q + (((size_t)b * H + h) * Lq + min(q[u], Lq - 1)) * DH;
+#pragma unroll
+    for (int kc = 0; kc < DH / 32; ++kc) qf[u][kc] = *reinterpret_cast<const bf16x8*>(Qr + 32 * kc + 8 * grp);
+  }
 
   const int lrow = lane >> 3, lchunk = (lane & 7) ^ (lane >> 3);
   const int lchunk_v = lchunk ^ (wave & 1);  // V^T rows 8 g + lrow with g = wave + NW j (NW even)
@@ -127,10 +133,15 @@ __global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf
     }
   };
 
-  f32x4 o[DH / 16];
+  f32x4 o[QS][DH / 16];
+  float m_run[QS], l_run[QS];
 #pragma unroll
-  for (int d = 0; d < DH / 16; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
+  for (int u = 0; u < QS; ++u) {
+#pragma unroll
+    for (int d = 0; d < DH / 16; ++d) o[u][d] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m_run[u] = -INFINITY;
+    l_run[u] = 0.f;
+  }
 
   // this lane's LDS byte offsets inside a stage, the same for every K tile: K row fr of
   // each 16-key block, chunk 4 (kc & 1) + grp; V^T row fr of each 16-row block, the
@@ -170,84 +181,95 @@ __global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf
     }
     // the buffer of tile t - 1, which every wave finished before the barrier above
     if (t + NS - 1 < nt) issue(t + NS - 1, (t + NS - 1) % NS);
-    f32x4 s[4];
+    f32x4 s[QS][4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      s[ks] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u < QS; ++u) s[u][ks] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kc = 0; kc < DH / 32; ++kc) {
         const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + (kc >> 1) * 8192 + ks * 2048 + kofs[kc & 1]);
-        s[ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kc], s[ks], 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < QS; ++u) s[u][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[u][kc], s[u][ks], 0, 0, 0);
       }
     }
-    // s[ks][j] = score(query lane&15, key t*64 + ks*16 + 4*grp + j), unscaled: the
-    // softmax runs in base 2 on s * scale_log2, the scale folded into one FMA per score
-    float mt = -INFINITY;
-    if ((t + 1) * KT <= Lk) {  // a whole tile: no key is masked
+    bf16x8 pf[QS][2];
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
+    for (int u = 0; u < QS; ++u) {
+      // s[u][ks][j] = score(query q[u], key t*64 + ks*16 + 4*grp + j), unscaled: the
+      // softmax runs in base 2 on s * scale_log2, the scale folded into one FMA per score
+      float mt = -INFINITY;
+      if ((t + 1) * KT <= Lk) {  // a whole tile: no key is masked
 #pragma unroll
-        for (int j = 0; j < 4; ++j) mt = fmaxf(mt, s[ks][j]);
-    } else {
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) mt = fmaxf(mt, s[u][ks][j]);
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int key = t * KT + ks * 16 + 4 * grp + j;
+            if (key >= Lk) s[u][ks][j] = -INFINITY;
+            mt = fmaxf(mt, s[u][ks][j]);
+          }
+      }
+      mt = fmaxf(mt, xor16(mt));
+      mt = fmaxf(mt, xor32(mt));
+      // The probabilities are taken relative to a reference m_run that only moves when the
+      // tile's maximum exceeds it by more than 2^8 (in base 2): until then they stay below
+      // 256 (exact in bf16's exponent range) and the accumulators need no rescaling; the
+      // row sum l_run uses the same reference, so o / l is unchanged.
+      const float mt2 = mt * scale_log2;  // scale_log2 > 0: the max commutes
+      const bool move = mt2 > m_run[u] + 8.f;  // also true on the first tile (m_run = -inf)
+      const float m_new = move ? mt2 : m_run[u];
+      // raw v_exp_f32: results below 2^-126 flush to 0 (a probability that small adds nothing)
+      const float alpha = m_run[u] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[u] - m_new);
+      float ps = 0.f;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int key = t * KT + ks * 16 + 4 * grp + j;
-          if (key >= Lk) s[ks][j] = -INFINITY;
-          mt = fmaxf(mt, s[ks][j]);
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[u][ks][j], scale_log2, -m_new));
+          s[u][ks][j] = p;
+          ps += p;
+        }
+      l_run[u] = l_run[u] * alpha + ps;
+      m_run[u] = m_new;
+      if (__builtin_amdgcn_ballot_w64(move))  // some lane of the wave moved its reference
+#pragma unroll
+        for (int d = 0; d < DH / 16; ++d) o[u][d] *= alpha;
+#pragma unroll
+      for (int kc2 = 0; kc2 < 2; ++kc2)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          pf[u][kc2][j] = (bf16)s[u][2 * kc2][j];
+          pf[u][kc2][4 + j] = (bf16)s[u][2 * kc2 + 1][j];
         }
     }
-    mt = fmaxf(mt, xor16(mt));
-    mt = fmaxf(mt, xor32(mt));
-    // The probabilities are taken relative to a reference m_run that only moves when the
-    // tile's maximum exceeds it by more than 2^8 (in base 2): until then they stay below
-    // 256 (exact in bf16's exponent range) and the accumulators need no rescaling; the
-    // row sum l_run uses the same reference, so o / l is unchanged.
-    const float mt2 = mt * scale_log2;  // scale_log2 > 0: the max commutes
-    const bool move = mt2 > m_run + 8.f;  // also true on the first tile (m_run = -inf)
-    const float m_new = move ? mt2 : m_run;
-    // raw v_exp_f32: results below 2^-126 flush to 0 (a probability that small adds nothing)
-    const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-    float ps = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[ks][j], scale_log2, -m_new));
-        s[ks][j] = p;
-        ps += p;
-      }
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
-    if (__builtin_amdgcn_ballot_w64(move))  // some lane of the wave moved its reference
-#pragma unroll
-      for (int d = 0; d < DH / 16; ++d) o[d] *= alpha;
 #pragma unroll
     for (int kc2 = 0; kc2 < 2; ++kc2) {
-      bf16x8 pf;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        pf[j] = (bf16)s[2 * kc2][j];
-        pf[4 + j] = (bf16)s[2 * kc2 + 1][j];
-      }
 #pragma unroll
       for (int d = 0; d < DH / 16; ++d) {
         const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(sk + d * 2048 + vofs[kc2][0]);
         const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(sk + d * 2048 + vofs[kc2][1]);
         const bf16x8 vf = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-        o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[d], 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < QS; ++u) o[u][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[u][kc2], o[u][d], 0, 0, 0);
       }
     }
   }
-  float l_tot = l_run + xor16(l_run);
-  l_tot += xor32(l_tot);
-  const float inv = 1.f / l_tot;
-  if (q < Lq) {
-    bf16* orow = O + ((size_t)b * Lq + q) * H * DH + h * DH;
 #pragma unroll
-    for (int d = 0; d < DH / 16; ++d)
-      store4(orow + d * 16 + 4 * grp, o[d][0] * inv, o[d][1] * inv, o[d][2] * inv, o[d][3] * inv);
+  for (int u = 0; u < QS; ++u) {
+    float l_tot = l_run[u] + xor16(l_run[u]);
+    l_tot += xor32(l_tot);
+    const float inv = 1.f / l_tot;
+    if (q[u] < Lq) {
+      bf16* orow = O + ((size_t)b * Lq + q[u]) * H * DH + h * DH;
+#pragma unroll
+      for (int d = 0; d < DH / 16; ++d)
+        store4(orow + d * 16 + 4 * grp, o[u][d][0] * inv, o[u][d][1] * inv, o[u][d][2] * inv, o[u][d][3] * inv);
+    }
   }
 }
 
@@ -312,8 +334,9 @@ hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, voi
   if (dt == BF16) {
     const float sl2 = 1.4426950408889634f / sqrtf((float)dh);
     const int nqt = (Lq + 63) / 64, G = H % Hkv == 0 ? H / Hkv : 0;
-    auto go = [&](auto kernel, int g) {
-      const dim3 grid(nqt * (g > 0 ? Hkv : H) * B), block(256 * (g > 0 ? g : 1));
+    auto go = [&](auto kernel, int g, int qs) {
+      const int tiles = (Lq + 64 * qs - 1) / (64 * qs);
+      const dim3 grid(tiles * (g > 0 ? Hkv : H) * B), block(256 * (g > 0 ? g : 1));
       launch_timed(kernel, grid, block, 0, s, static_cast<const bf16*>(Q), static_cast<const bf16*>(K),
                    static_cast<const bf16*>(Vt), static_cast<bf16*>(O), H, Hkv, Lq, Lk, kv_cap, sl2);
       return hipGetLastError();
@@ -324,12 +347,18 @@ hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, voi
     // leaves CUs idle (block workload, G = 4: 64 blocks of 16 waves, attention 47.8 ->
     // 94.7 ms per generation; 26B-class, G = 2: 256 blocks of 8 waves, no faster).
     const bool pack = (long)nqt * Hkv * B >= 512;
-    if (dh == 64) return G == 1 ? go(attn_bf16_kernel<64, 2, 1>, 1) : go(attn_bf16_kernel<64, 2, 0>, 0);
+    // Two query strips per wave (128 queries per block) halve the LDS reads per product
+    // (each K / V^T fragment feeds two MFMAs), when the grid keeps two blocks per CU.
+    const bool two = (long)((Lq + 127) / 128) * H * B >= 512;
+    if (dh == 64) {
+      if (G == 1) return two ? go(attn_bf16_kernel<64, 2, 1, 2>, 1, 2) : go(attn_bf16_kernel<64, 2, 1, 1>, 1, 1);
+      return two ? go(attn_bf16_kernel<64, 2, 0, 2>, 0, 2) : go(attn_bf16_kernel<64, 2, 0, 1>, 0, 1);
+    }
     if (dh == 128) {
-      if (G == 1) return go(attn_bf16_kernel<128, 2, 1>, 1);
-      if (pack && G == 2) return go(attn_bf16_kernel<128, 2, 2>, 2);
-      if (pack && G == 4) return go(attn_bf16_kernel<128, 2, 4>, 4);
-      return go(attn_bf16_kernel<128, 2, 0>, 0);
+      if (G == 1) return two ? go(attn_bf16_kernel<128, 2, 1, 2>, 1, 2) : go(attn_bf16_kernel<128, 2, 1, 1>, 1, 1);
+      if (pack && G == 2) return go(attn_bf16_kernel<128, 2, 2, 1>, 2, 1);
+      if (pack && G == 4) return go(attn_bf16_kernel<128, 2, 4, 1>, 4, 1);
+      return two ? go(attn_bf16_kernel<128, 2, 0, 2>, 0, 2) : go(attn_bf16_kernel<128, 2, 0, 1>, 0, 1);
     }
     return hipErrorInvalidValue;
   }
