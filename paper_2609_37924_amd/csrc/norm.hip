@@ -43,22 +43,22 @@ __global__ __launch_bounds__(256) void rms_kernel(const float* x, const float* g
   T* yr = y + (size_t)r * d;
   float ss = 0.f;
   if constexpr (NV > 0) {
-    float4 v[NV];
+    // the gains are loaded with the row, so that their latency overlaps the row's
+    float4 v[NV], w[NV];
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int c = lane * 4 + 256 * i;
       v[i] = c < d ? *reinterpret_cast<const float4*>(xr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
-      ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+      w[i] = c < d ? *reinterpret_cast<const float4*>(g + c) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
+#pragma unroll
+    for (int i = 0; i < NV; ++i) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
     ss = wave_sum(ss);
     const float rs = rsqrtf(ss / d + eps);
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int c = lane * 4 + 256 * i;
-      if (c < d) {
-        const float4 w = *reinterpret_cast<const float4*>(g + c);
-        store4(yr + c, v[i].x * rs * w.x, v[i].y * rs * w.y, v[i].z * rs * w.z, v[i].w * rs * w.w);
-      }
+      if (c < d) store4(yr + c, v[i].x * rs * w[i].x, v[i].y * rs * w[i].y, v[i].z * rs * w[i].z, v[i].w * rs * w[i].w);
     }
   } else {
     for (int c = lane * 4; c < d; c += 256) {
