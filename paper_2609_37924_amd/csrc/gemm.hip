@@ -460,20 +460,25 @@ __global__ void resid_reduce_kernel(const float* part, int S, int M, int N, floa
   *r = x;
 }
 
-// K slices of a residual product with a very long K (at least 128 K tiles: the FFN
-// down projections) on 256 x 256 tiles, one block per CU: the S in [2, 16] (each slice
-// >= 16 K tiles, slices as even as the tile count allows) that minimises the time of
-// the grid, rounds of 256 blocks x the K tiles per slice, the smaller S on ties; 1 when
-// no split beats the unsplit grid.  26B-class FFN down (1024 x 4608 x 36864): S = 7,
-// 504 blocks in two rounds (468 -> 354 us against 128 x 128 tiles in 8 slices).
+// K slices of a residual product on 256 x 256 tiles, one block per CU: the S in
+// [2, 16] (each slice >= 8 K tiles, slices as even as the tile count allows) that
+// minimises the modelled time, in K-step units: rounds of 256 blocks x (K tiles per
+// slice + 2 for a block's prologue and epilogue), plus 1.5 per slice for the ordered
+// reduction's read of the slice's [M, N] partial; 1 when no split beats the unsplit
+// grid.  Products with fewer than 128 K tiles are split only from 64 output tiles on:
+// smaller ones run sooner on the 64 x 64 or 128 x 128 tiles at two or three blocks per CU
+// (block workload's attention output, 1024 x 2048 x 2048, and the small workload's FFN
+// down, 3072 x 768 x 2048: 2.5 % and 6.6 % slower per generation when split).  26B-class
+// FFN down (1024 x 4608 x 36864): S = 7, 504 blocks in two rounds (468 -> 354 us against
+// 128 x 128 tiles in 8 slices); its attention output (1024 x 4608 x 4096): S = 3.
 int resid_slices256(int M, int N, int K) {
   const long tiles = (long)((M + 255) / 256) * ((N + 255) / 256);
   const int nk = K / 64;
-  if (nk < 128 || N % 4) return 1;
+  if (N % 4 || nk < 32 || (nk < 128 && tiles < 64)) return 1;
   int best = 1;
-  double best_t = (double)((tiles + 255) / 256);
-  for (int S = 2; S <= 16 && nk / S >= 16; ++S) {
-    const double t = (double)((tiles * S + 255) / 256) / S;
+  double best_t = (double)((tiles + 255) / 256) * (nk + 2);
+  for (int S = 2; S <= 16 && nk / S >= 8; ++S) {
+    const double t = (double)((tiles * S + 255) / 256) * ((double)nk / S + 2) + 1.5 * S;
     if (t < best_t - 1e-9) {
       best = S;
       best_t = t;
