@@ -258,12 +258,15 @@ def test_gelu_bf16_step_parity():
     _teacher_step_parity(cfg, 2, BF16_TOL)
 
 
-@pytest.mark.parametrize("dh,H,Hkv", [(64, 12, 12), (128, 16, 16), (128, 16, 4)])
-def test_attention_dominated_layer(dh, H, Hkv):
+@pytest.mark.parametrize("dh,H,Hkv,B", [(64, 12, 12, 2), (128, 16, 16, 2), (128, 16, 4, 2), (128, 16, 16, 16),
+                                         (64, 12, 12, 24)])
+def test_attention_dominated_layer(dh, H, Hkv, B):
     """One anchor layer whose output is dominated by attention (feed-forward off,
     V and O projections scaled up twofold: the attention output, rms ~1, is ~50 times
     the embedding it is added to), so that an attention error cannot hide behind the
-    residual stream.  Covers both head widths and grouped KV heads."""
+    residual stream.  Covers both head widths and grouped KV heads; at B = 16 / 24 the
+    grid is large enough for two 16-query strips per wave (128-query blocks), and the
+    130 positions leave a ragged second block of 2 queries."""
     cfg = synth.get_config("1b", n_anchor=1, n_denoise=1, vocab=512, n_heads=H, n_kv_heads=Hkv,
                            head_dim=dh, d_model=H * dh, prompt_len=30, gen_len=100)
     tensors = synth.make_weights(cfg, perturb=True)
@@ -272,7 +275,7 @@ def test_attention_dominated_layer(dh, H, Hkv):
         tensors[names.index(f"layer{li}.wv")] = (tensors[names.index(f"layer{li}.wv")].float() * 2).bfloat16()
         tensors[names.index(f"layer{li}.wo")] = (tensors[names.index(f"layer{li}.wo")].float() * 2).bfloat16()
         tensors[names.index(f"layer{li}.w_down")] = torch.zeros_like(tensors[names.index(f"layer{li}.w_down")])
-    _teacher_step_parity(cfg, 2, BF16_TOL, tensors=tensors)
+    _teacher_step_parity(cfg, B, BF16_TOL, tensors=tensors, rows=None if B == 2 else [0, B - 1])
 
 
 def test_tiny_fp32_paired_step_parity():
