@@ -146,6 +146,11 @@ KERNELS = [
 ]
 
 
+# The fp32 K-slice products of split residual products (the only fp32-output products
+# on the bf16 workloads' layer path; the kernel_bench programs run nothing else of that kind)
+SLICE_PATTERN = r"gemm_bf16_kernel<(256, 256|128, 128).*EpiKind\)1>"
+
+
 def kernel_table(cfg, B, K, stages):
     """Per kernel group: time per generation, launches, algorithmic work and roofline."""
     work, launches = schedule_work(cfg, B, K)
@@ -277,12 +282,23 @@ def render_counter_summary(fetch_dir, write_dir, mfma_dir=None, command=""):
         rx = re.compile(pat)
         fk = [r for r in fetch if rx.search(r["Kernel_Name"])]
         wk = [r for r in write if rx.search(r["Kernel_Name"])]
+        calls = len(fk)
+        if "oproj" in names:
+            # a residual product split over K is two kernels, the fp32 slices and their
+            # ordered reduction: its bytes are both kernels', and it is one launch of the
+            # stage (the reduction marks it)
+            red = [r for r in fetch if "resid_reduce_kernel" in r["Kernel_Name"]]
+            if red:
+                sx = re.compile(SLICE_PATTERN)
+                fk += red + [r for r in fetch if sx.search(r["Kernel_Name"])]
+                wk += [r for r in write if "resid_reduce_kernel" in r["Kernel_Name"] or sx.search(r["Kernel_Name"])]
+                calls += len(red)
         if not fk or len(fk) != len(wk):
             continue
         b = (sum(float(r["Counter_Value"]) for r in fk) * sf + sum(float(r["Counter_Value"]) for r in wk) * sw) \
-            * 1024.0 / len(fk)
+            * 1024.0 / calls
         print(f"    traffic stage={names[0]} bytes_per_launch={b:.0f} sources={source_digest(source)}")
-        print(f"      ({desc}: {len(fk)} dispatches, {b / 1e6:.3f} MB per launch)")
+        print(f"      ({desc}: {calls} launches, {len(fk)} dispatches, {b / 1e6:.3f} MB per launch)")
 
 
 def run_args(config, K):

@@ -65,19 +65,23 @@ def build(jobs=8, verbose=False):
     return OUT
 
 
-# tadm_run: a native program that runs whole generations through the C ABI (linked
-# against the library next to it)
+# Native programs linked against the library next to them: tadm_run (whole generations
+# through the C ABI) and kernel_bench (one denoiser pass's kernels through the library's
+# launchers, the program hardware counters are taken on).
+PROGRAMS = ["tadm_run", "kernel_bench"]
 RUN_OUT = os.path.join(PKG, "tadm_run")
 
 
 def build_run():
-    tmp = RUN_OUT + ".tmp"
-    cmd = [hipcc(), os.path.join(HERE, "tadm_run.hip"), "-o", tmp] + flags() + \
-        ["-L", PKG, "-l:libtadm.so", "-Wl,-rpath,$ORIGIN"]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError("hipcc failed on tadm_run.hip:\n" + r.stderr)
-    os.replace(tmp, RUN_OUT)
+    for name in PROGRAMS:
+        out = os.path.join(PKG, name)
+        tmp = out + ".tmp"
+        cmd = [hipcc(), os.path.join(HERE, name + ".hip"), "-o", tmp] + flags() + \
+            ["-L", PKG, "-l:libtadm.so", "-Wl,-rpath,$ORIGIN"]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc failed on {name}.hip:\n" + r.stderr)
+        os.replace(tmp, out)
     return RUN_OUT
 
 

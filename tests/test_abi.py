@@ -137,6 +137,22 @@ def test_loop_sampler_rejects_bad_schedules():
 RUN = os.path.join(os.path.dirname(os.path.dirname(__file__)), "paper_2609_37924_amd", "tadm_run")
 
 
+def test_kernel_bench_rejects_bad_arguments_before_device_work():
+    import subprocess
+
+    kb = os.path.join(os.path.dirname(RUN), "kernel_bench")
+    if not os.path.exists(kb):
+        pytest.skip("kernel_bench not built")
+    for argv, msg in (([], "missing batch"), (["foo"], "bad argument"),
+                      (["batch=1", "prompt_len=0", "gen_len=8", "d_model=64", "n_heads=1", "head_dim=32",
+                        "d_ffn=64"], "unsupported shape"),
+                      (["batch=2", "prompt_len=0", "gen_len=8", "d_model=64", "n_heads=1", "head_dim=64",
+                        "d_ffn=64", "dtype=0"], "bf16 workloads only")):
+        r = subprocess.run([kb] + argv, capture_output=True, text=True, timeout=60)
+        assert r.returncode == 1, (argv, r.returncode, r.stderr)
+        assert msg in r.stderr, (argv, r.stderr)
+
+
 def test_native_driver_rejects_bad_arguments_before_device_work():
     """tadm_run (the native program over the C ABI) checks its arguments before it
     touches the GPU: these run on a host without one."""
