@@ -316,7 +316,10 @@ inline void xcd_patch(int rm, int rn, int BM, int BN, int R, int& gm, int& gn) {
     const int n = R / m;
     if (rm % m || rn % n) continue;
     const long cost = (long)m * BM + (long)n * BN;
-    if (cost < best) {
+    // on a tie, a patch as wide as the region: each A panel is then streamed once per
+    // region (the 1B-class FFN down, 32 768 x 2 048 x 8 192, region 16 x 8: 4 x 8 rather
+    // than 8 x 4, whose two patches per row band read each 4 MB A panel twice)
+    if (cost < best || (cost == best && gm > 0 && n == rn)) {
       best = cost;
       gm = m;
       gn = n;
