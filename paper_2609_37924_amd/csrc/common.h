@@ -111,3 +111,34 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
 __device__ __forceinline__ float sigmoidf_(float x) { return 1.f / (1.f + __expf(-x)); }
 __device__ __forceinline__ float siluf_(float x) { return x * sigmoidf_(x); }
+
+// Activations of products whose results are stored in bf16 (relative resolution 2^-8):
+// GELU as x Phi(x) with erfc(z), z = |x| / sqrt(2), from Abramowitz & Stegun 7.1.26
+// (Hastings' rational approximation, absolute error <= 1.5e-7), Phi(x) = erfc(z) / 2 for
+// x < 0 and 1 - erfc(z) / 2 otherwise; the sigmoid with the hardware reciprocal (1 ulp).
+// About a third of the instructions of the library erf and the IEEE division.
+__device__ __forceinline__ float gelu_bf16out(float x) {
+  const float z = fabsf(x) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(__builtin_fmaf(0.3275911f, z, 1.0f));
+  const float poly =
+      t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+  const float erfc = poly * __builtin_amdgcn_exp2f(-1.4426950408889634f * z * z);
+  return x * (x < 0.f ? 0.5f * erfc : 1.0f - 0.5f * erfc);
+}
+__device__ __forceinline__ float sigmoid_bf16out(float x) { return __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
+__device__ __forceinline__ float silu_bf16out(float x) { return x * sigmoid_bf16out(x); }
+// T = the product's operand type: float32 models keep the library erf and IEEE division
+template <class T>
+__device__ __forceinline__ float gelu_act(float x) {
+  if constexpr (sizeof(T) == 2) return gelu_bf16out(x);
+  else return gelu_erf(x);
+}
+template <class T>
+__device__ __forceinline__ float sigmoid_act(float x) {
+  if constexpr (sizeof(T) == 2) return sigmoid_bf16out(x);
+  else return sigmoidf_(x);
+}
+template <class T>
+__device__ __forceinline__ float silu_act(float x) {
+  return x * sigmoid_act<T>(x);
+}

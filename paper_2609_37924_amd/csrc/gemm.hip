@@ -55,8 +55,8 @@ template <class T>
 struct Epi<EPI_GELU, T> {
   static constexpr bool kGlu = false;
   __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
-    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + n, gelu_erf(v[0]), gelu_erf(v[1]),
-           gelu_erf(v[2]), gelu_erf(v[3]));
+    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + n, gelu_act<T>(v[0]), gelu_act<T>(v[1]),
+           gelu_act<T>(v[2]), gelu_act<T>(v[3]));
   }
 };
 template <class T>
@@ -65,11 +65,11 @@ struct Epi<EPI_FUSION1, T> {
   __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
     const float4 b = *reinterpret_cast<const float4*>(e.bias + n);
     if (n < e.split) {
-      store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + n, gelu_erf(v[0] + b.x),
-             gelu_erf(v[1] + b.y), gelu_erf(v[2] + b.z), gelu_erf(v[3] + b.w));
+      store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + n, gelu_act<T>(v[0] + b.x),
+             gelu_act<T>(v[1] + b.y), gelu_act<T>(v[2] + b.z), gelu_act<T>(v[3] + b.w));
     } else {
-      store4(e.out2 + (size_t)m * e.ldo2 + (n - e.split), sigmoidf_(v[0] + b.x),
-             sigmoidf_(v[1] + b.y), sigmoidf_(v[2] + b.z), sigmoidf_(v[3] + b.w));
+      store4(e.out2 + (size_t)m * e.ldo2 + (n - e.split), sigmoid_act<T>(v[0] + b.x),
+             sigmoid_act<T>(v[1] + b.y), sigmoid_act<T>(v[2] + b.z), sigmoid_act<T>(v[3] + b.w));
     }
   }
 };
@@ -88,8 +88,8 @@ template <class T>
 struct Epi<EPI_SILU, T> {
   static constexpr bool kGlu = false;
   __device__ static void apply(const EpiParams& e, int m, int n, f32x4 v) {
-    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + n, siluf_(v[0]), siluf_(v[1]), siluf_(v[2]),
-           siluf_(v[3]));
+    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + n, silu_act<T>(v[0]), silu_act<T>(v[1]),
+           silu_act<T>(v[2]), silu_act<T>(v[3]));
   }
 };
 template <class T>
@@ -270,16 +270,16 @@ template <class T>
 struct Epi<EPI_GLU_SILU, T> {
   static constexpr bool kGlu = true;
   __device__ static void glu(const EpiParams& e, int m, int f, f32x4 g, f32x4 u) {
-    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + f, siluf_(g[0]) * u[0], siluf_(g[1]) * u[1],
-           siluf_(g[2]) * u[2], siluf_(g[3]) * u[3]);
+    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + f, silu_act<T>(g[0]) * u[0],
+           silu_act<T>(g[1]) * u[1], silu_act<T>(g[2]) * u[2], silu_act<T>(g[3]) * u[3]);
   }
 };
 template <class T>
 struct Epi<EPI_GLU_GELU, T> {
   static constexpr bool kGlu = true;
   __device__ static void glu(const EpiParams& e, int m, int f, f32x4 g, f32x4 u) {
-    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + f, gelu_erf(g[0]) * u[0],
-           gelu_erf(g[1]) * u[1], gelu_erf(g[2]) * u[2], gelu_erf(g[3]) * u[3]);
+    store4(static_cast<T*>(e.out) + (size_t)m * e.ldo + f, gelu_act<T>(g[0]) * u[0],
+           gelu_act<T>(g[1]) * u[1], gelu_act<T>(g[2]) * u[2], gelu_act<T>(g[3]) * u[3]);
   }
 };
 
