@@ -71,11 +71,17 @@ constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >>
 // QS: query strips of 16 per wave; the block's query tile is 64 QS queries (strip s of
 // wave w: queries 64 s + 16 w + [0, 16)), and every K and V^T fragment read from LDS
 // feeds QS products, so a wave reads the K/V tile once for 16 QS queries.
-template <int DH, int NS, int G, int QS>
-__global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf16_kernel(
+// KS = 2: the keys of each K/V tile are split between two groups of 4 waves (keys 0-31 and
+// 32-63), each with its own running maximum, sum and output, merged in LDS at the end:
+// twice the waves per block for the same LDS, when the grid alone leaves the SIMDs short
+// of waves.
+template <int DH, int NS, int G, int QS, int KS>
+__global__ __launch_bounds__(256 * (G > 0 ? G : 1) * KS, G == 4 ? 1 : 2) void attn_bf16_kernel(
     const bf16* Q, const bf16* K, const bf16* Vt, bf16* O, int H, int Hkv, int Lq, int Lk, int kv_cap,
     float scale_log2) {
-  constexpr int KT = 64, NW = 4 * (G > 0 ? G : 1);  // waves per block: 4 query strips x G heads
+  static_assert(KS == 1 || (KS == 2 && G <= 1), "key split: one query head per wave");
+  constexpr int KT = 64, NW = 4 * (G > 0 ? G : 1) * KS;  // waves per block: 4 query strips x G heads x KS
+  constexpr int KB = 4 / KS;                              // 16-key blocks of a tile per wave
   constexpr int KBYTES = KT * DH * 2, VBYTES = DH * KT * 2, STAGE = KBYTES + VBYTES;
   constexpr int LK = KBYTES / 1024 / NW, LV = VBYTES / 1024 / NW;  // load instructions per wave
   static_assert(LK * 1024 * NW == KBYTES && LV * 1024 * NW == VBYTES, "tile rows must split over the waves");
@@ -85,6 +91,7 @@ __global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf
   // wave index as a scalar: the K/V tile destinations in LDS are formed in scalar registers
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), grp = lane >> 4,
             fr = lane & 15;
+  const int kh = KS > 1 ? wave / 4 : 0;  // this wave's key group: keys 64 kh / KS + [0, 64 / KS) of a tile
   // one block per (64-query tile, K/V head, batch row), query tiles fastest: the tiles of
   // a K/V head run on one XCD and read K/V from its L2
   const int nqt = (Lq + 64 * QS - 1) / (64 * QS);
@@ -94,7 +101,7 @@ __global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf
     qt = id % nqt;
     hk = (id / nqt) % Hkv;
     b = id / (nqt * Hkv);
-    h = hk * G + wave / 4;  // query heads hk G .. hk G + G - 1 read K/V head hk
+    h = hk * G + (KS > 1 ? 0 : wave / 4);  // query heads hk G .. hk G + G - 1 read K/V head hk
   } else {
     qt = id % nqt;
     h = (id / nqt) % H;
@@ -181,35 +188,39 @@ __global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf
     }
     // the buffer of tile t - 1, which every wave finished before the barrier above
     if (t + NS - 1 < nt) issue(t + NS - 1, (t + NS - 1) % NS);
-    f32x4 s[QS][4];
+    // a key group whose keys of this tile all lie past the end skips it (its scores
+    // would all be -inf)
+    if (KS > 1 && t * KT + kh * (KT / KS) >= Lk) continue;
+    f32x4 s[QS][KB];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < KB; ++ks) {
 #pragma unroll
       for (int u = 0; u < QS; ++u) s[u][ks] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kc = 0; kc < DH / 32; ++kc) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sk + (kc >> 1) * 8192 + ks * 2048 + kofs[kc & 1]);
+        const bf16x8 kf =
+            *reinterpret_cast<const bf16x8*>(sk + (kc >> 1) * 8192 + (kh * KB + ks) * 2048 + kofs[kc & 1]);
 #pragma unroll
         for (int u = 0; u < QS; ++u) s[u][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[u][kc], s[u][ks], 0, 0, 0);
       }
     }
-    bf16x8 pf[QS][2];
+    bf16x8 pf[QS][KB / 2];
 #pragma unroll
     for (int u = 0; u < QS; ++u) {
-      // s[u][ks][j] = score(query q[u], key t*64 + ks*16 + 4*grp + j), unscaled: the
+      // s[u][ks][j] = score(query q[u], key t*64 + (kh*KB + ks)*16 + 4*grp + j), unscaled: the
       // softmax runs in base 2 on s * scale_log2, the scale folded into one FMA per score
       float mt = -INFINITY;
       if ((t + 1) * KT <= Lk) {  // a whole tile: no key is masked
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
+        for (int ks = 0; ks < KB; ++ks)
 #pragma unroll
           for (int j = 0; j < 4; ++j) mt = fmaxf(mt, s[u][ks][j]);
       } else {
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
+        for (int ks = 0; ks < KB; ++ks)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const int key = t * KT + ks * 16 + 4 * grp + j;
+            const int key = t * KT + (kh * KB + ks) * 16 + 4 * grp + j;
             if (key >= Lk) s[u][ks][j] = -INFINITY;
             mt = fmaxf(mt, s[u][ks][j]);
           }
@@ -227,7 +238,7 @@ __global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf
       const float alpha = m_run[u] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[u] - m_new);
       float ps = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
+      for (int ks = 0; ks < KB; ++ks)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[u][ks][j], scale_log2, -m_new));
@@ -240,24 +251,59 @@ __global__ __launch_bounds__(256 * (G > 0 ? G : 1), G == 4 ? 1 : 2) void attn_bf
 #pragma unroll
         for (int d = 0; d < DH / 16; ++d) o[u][d] *= alpha;
 #pragma unroll
-      for (int kc2 = 0; kc2 < 2; ++kc2)
+      for (int c = 0; c < KB / 2; ++c)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          pf[u][kc2][j] = (bf16)s[u][2 * kc2][j];
-          pf[u][kc2][4 + j] = (bf16)s[u][2 * kc2 + 1][j];
+          pf[u][c][j] = (bf16)s[u][2 * c][j];
+          pf[u][c][4 + j] = (bf16)s[u][2 * c + 1][j];
         }
     }
 #pragma unroll
-    for (int kc2 = 0; kc2 < 2; ++kc2) {
+    for (int c = 0; c < KB / 2; ++c) {
+      const int kc2 = kh * (KB / 2) + c;  // 32-key half of the tile
 #pragma unroll
       for (int d = 0; d < DH / 16; ++d) {
         const bf16x4 v0 = *reinterpret_cast<const bf16x4*>(sk + d * 2048 + vofs[kc2][0]);
         const bf16x4 v1 = *reinterpret_cast<const bf16x4*>(sk + d * 2048 + vofs[kc2][1]);
         const bf16x8 vf = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
 #pragma unroll
-        for (int u = 0; u < QS; ++u) o[u][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[u][kc2], o[u][d], 0, 0, 0);
+        for (int u = 0; u < QS; ++u) o[u][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[u][c], o[u][d], 0, 0, 0);
       }
     }
+  }
+  if constexpr (KS > 1) {
+    // merge the second key group into the first, one query strip at a time: each group's
+    // output and sum are relative to its own reference m; both are rescaled to the larger
+    // one.  Per lane: m, l and the DH / 4 output values, in [wave - 4][value][lane] floats.
+    constexpr int NV = 2 + DH / 4;
+    static_assert(4 * NV * 64 * 4 <= NS * STAGE, "merge area larger than the K/V ring");
+    float* xs = reinterpret_cast<float*>(smem);
+#pragma unroll
+    for (int u = 0; u < QS; ++u) {
+      __syncthreads();  // every wave is done with the K/V ring (or the previous strip's merge)
+      if (kh == 1) {
+        float* w = xs + (size_t)(wave - 4) * NV * 64 + lane;
+        w[0] = m_run[u];
+        w[64] = l_run[u];
+#pragma unroll
+        for (int d = 0; d < DH / 16; ++d)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) w[(2 + 4 * d + j) * 64] = o[u][d][j];
+      }
+      __syncthreads();
+      if (kh == 0) {
+        const float* r = xs + (size_t)wave * NV * 64 + lane;
+        const float m1 = r[0], m0 = m_run[u], mm = fmaxf(m0, m1);
+        const float a0 = m0 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m0 - mm);
+        const float a1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - mm);
+        l_run[u] = l_run[u] * a0 + r[64] * a1;
+#pragma unroll
+        for (int d = 0; d < DH / 16; ++d)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o[u][d][j] = o[u][d][j] * a0 + r[(2 + 4 * d + j) * 64] * a1;
+      }
+    }
+    if (kh == 1) return;
   }
 #pragma unroll
   for (int u = 0; u < QS; ++u) {
@@ -334,9 +380,9 @@ hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, voi
   if (dt == BF16) {
     const float sl2 = 1.4426950408889634f / sqrtf((float)dh);
     const int nqt = (Lq + 63) / 64, G = H % Hkv == 0 ? H / Hkv : 0;
-    auto go = [&](auto kernel, int g, int qs) {
+    auto go = [&](auto kernel, int g, int qs, int ks) {
       const int tiles = (Lq + 64 * qs - 1) / (64 * qs);
-      const dim3 grid(tiles * (g > 0 ? Hkv : H) * B), block(256 * (g > 0 ? g : 1));
+      const dim3 grid(tiles * (g > 0 ? Hkv : H) * B), block(256 * (g > 0 ? g : 1) * ks);
       launch_timed(kernel, grid, block, 0, s, static_cast<const bf16*>(Q), static_cast<const bf16*>(K),
                    static_cast<const bf16*>(Vt), static_cast<bf16*>(O), H, Hkv, Lq, Lk, kv_cap, sl2);
       return hipGetLastError();
@@ -349,16 +395,25 @@ hipError_t attention(DType dt, const void* Q, const void* K, const void* Vt, voi
     const bool pack = (long)nqt * Hkv * B >= 512;
     // Two query strips per wave (128 queries per block) halve the LDS reads per product
     // (each K / V^T fragment feeds two MFMAs), when the grid keeps two blocks per CU.
-    const bool two = (long)((Lq + 127) / 128) * H * B >= 512;
-    if (dh == 64) {
-      if (G == 1) return two ? go(attn_bf16_kernel<64, 2, 1, 2>, 1, 2) : go(attn_bf16_kernel<64, 2, 1, 1>, 1, 1);
-      return two ? go(attn_bf16_kernel<64, 2, 0, 2>, 0, 2) : go(attn_bf16_kernel<64, 2, 0, 1>, 0, 1);
+    const long n128 = (long)((Lq + 127) / 128) * H * B;
+    const bool two = n128 >= 512;
+    // Otherwise the keys of each tile are split between two wave groups (KS = 2), which
+    // doubles the waves per block: with two strips per wave when the query tiles of 128
+    // still give every CU a block, else with one.
+    const bool two_split = !two && Lq >= 128 && n128 >= 256;
+    if (dh == 64) {  // the key split measured slower at this width (small workload 3.66 -> 4.01 ms)
+      if (G == 1) return two ? go(attn_bf16_kernel<64, 2, 1, 2, 1>, 1, 2, 1) : go(attn_bf16_kernel<64, 2, 1, 1, 1>, 1, 1, 1);
+      return two ? go(attn_bf16_kernel<64, 2, 0, 2, 1>, 0, 2, 1) : go(attn_bf16_kernel<64, 2, 0, 1, 1>, 0, 1, 1);
     }
     if (dh == 128) {
-      if (G == 1) return two ? go(attn_bf16_kernel<128, 2, 1, 2>, 1, 2) : go(attn_bf16_kernel<128, 2, 1, 1>, 1, 1);
-      if (pack && G == 2) return go(attn_bf16_kernel<128, 2, 2, 1>, 2, 1);
-      if (pack && G == 4) return go(attn_bf16_kernel<128, 2, 4, 1>, 4, 1);
-      return two ? go(attn_bf16_kernel<128, 2, 0, 2>, 0, 2) : go(attn_bf16_kernel<128, 2, 0, 1>, 0, 1);
+      if (G == 1) {
+        if (two) return go(attn_bf16_kernel<128, 2, 1, 2, 1>, 1, 2, 1);
+        return two_split ? go(attn_bf16_kernel<128, 2, 1, 2, 2>, 1, 2, 2) : go(attn_bf16_kernel<128, 2, 1, 1, 2>, 1, 1, 2);
+      }
+      if (pack && G == 2) return go(attn_bf16_kernel<128, 2, 2, 1, 1>, 2, 1, 1);
+      if (pack && G == 4) return go(attn_bf16_kernel<128, 2, 4, 1, 1>, 4, 1, 1);
+      if (two) return go(attn_bf16_kernel<128, 2, 0, 2, 1>, 0, 2, 1);
+      return two_split ? go(attn_bf16_kernel<128, 2, 0, 2, 2>, 0, 2, 2) : go(attn_bf16_kernel<128, 2, 0, 1, 2>, 0, 1, 2);
     }
     return hipErrorInvalidValue;
   }

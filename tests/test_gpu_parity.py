@@ -258,17 +258,22 @@ def test_gelu_bf16_step_parity():
     _teacher_step_parity(cfg, 2, BF16_TOL)
 
 
-@pytest.mark.parametrize("dh,H,Hkv,B", [(64, 12, 12, 2), (128, 16, 16, 2), (128, 16, 4, 2), (128, 16, 16, 16),
-                                         (64, 12, 12, 24)])
-def test_attention_dominated_layer(dh, H, Hkv, B):
+@pytest.mark.parametrize("dh,H,Hkv,B,gen", [(64, 12, 12, 2, 100), (128, 16, 16, 2, 100), (128, 16, 4, 2, 100),
+                                             (128, 16, 16, 16, 100), (64, 12, 12, 24, 100), (128, 16, 4, 2, 2),
+                                             (128, 16, 16, 2, 3), (128, 16, 16, 8, 100), (128, 16, 4, 8, 100)])
+def test_attention_dominated_layer(dh, H, Hkv, B, gen):
     """One anchor layer whose output is dominated by attention (feed-forward off,
     V and O projections scaled up twofold: the attention output, rms ~1, is ~50 times
     the embedding it is added to), so that an attention error cannot hide behind the
-    residual stream.  Covers both head widths and grouped KV heads; at B = 16 / 24 the
+    residual stream.  Covers both head widths and grouped KV heads.  At B = 16 / 24 the
     grid is large enough for two 16-query strips per wave (128-query blocks), and the
-    130 positions leave a ragged second block of 2 queries."""
+    130 positions leave a ragged second block of 2 queries.  At head width 128 and
+    B = 2 the keys of each 64-key tile are split between two wave groups of one strip
+    each, at B = 8 of two strips each; the 130 keys leave a last tile of 2 keys, which
+    the second group skips, 32 keys give that group no key at all, and 33 keys give it
+    one."""
     cfg = synth.get_config("1b", n_anchor=1, n_denoise=1, vocab=512, n_heads=H, n_kv_heads=Hkv,
-                           head_dim=dh, d_model=H * dh, prompt_len=30, gen_len=100)
+                           head_dim=dh, d_model=H * dh, prompt_len=30, gen_len=gen)
     tensors = synth.make_weights(cfg, perturb=True)
     names = [s[0] for s in synth.weight_specs(cfg)]
     for li in range(2):
