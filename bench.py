@@ -376,19 +376,24 @@ def cpu_baseline(cfg, K, budget_s=10.0):
     t_first = time.perf_counter() - t0
     value, rows, el = rate(K, budget_s) if 4 * t_first < budget_s else rate(K, budget_s, 1, t_first)
     per_k = one_thread = None
+    k_note = ""
     if el / rows * len(cfg["Ks"]) * 4 < budget_s:  # each interval's rate on its own share of the budget
         per_k = {f"K={Kx}": rate(Kx, budget_s / len(cfg["Ks"]))[0] for Kx in cfg["Ks"]}
         # short rows: also the rate on one thread (the oracle's results do not depend on it)
         from threadpoolctl import threadpool_limits
         with threadpool_limits(limits=1):
             one_thread = rate(K, budget_s / 4)[0]
+    elif el / rows <= 40.0:
+        # rows of up to ~40 s (the small workload): one complete row at each other interval
+        per_k = {f"K={Kx}": value if Kx == K else rate(Kx, 0.0)[0] for Kx in cfg["Ks"]}
+        k_note = "; k_sweep: one complete row at each other interval"
     threads = max([t.get("num_threads", 1) for t in threadpool_info()] + [1])
     return {"value": value, "unit": "tokens/s", "cores": threads, "kind": "oracle", "extrapolated": False,
             "cpu_model": cpu_model(), "host_cpus_available": len(os.sched_getaffinity(0)),
             "k_sweep": per_k, "one_thread": one_thread,
             "sample": f"{rows} rows (prompts of the workload's {B}, in turn), each a complete generation by the "
                       f"oracle's Algorithm 1 at K={K} ({G} positions, T={T}), {el:.1f} s in all; rate of those rows "
-                      f"(rows are independent)"}
+                      f"(rows are independent){k_note}"}
 
 
 STREAM_HEAD_ROWS = 16384  # vocabulary rows of the head in the streamed sample
