@@ -32,6 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector (the float32 models' products and attention run on the VALU)
 PEAK_HBM_GBS = 8000.0
 
 
@@ -162,7 +163,10 @@ def kernel_table(cfg, B, K, stages):
         if not n or not w:
             continue
         expect = sum(launches[x] for x in names)
-        peak, unit, scale = (PEAK_BF16_TFLOPS, "TFLOP/s", 1e12) if bound == "mfma" else (PEAK_HBM_GBS, "GB/s", 1e9)
+        if bound == "mfma" and cfg["dtype"] != "bf16":  # float32 kernels: VALU arithmetic
+            desc, bound = desc.replace("bf16 MFMA", "fp32 VALU"), "alu"
+        peak, unit, scale = ((PEAK_BF16_TFLOPS if bound == "mfma" else PEAK_FP32_TFLOPS), "TFLOP/s", 1e12) \
+            if bound != "hbm" else (PEAK_HBM_GBS, "GB/s", 1e9)
         achieved = w / (ms / 1e3) / scale
         out.append({"kernel": desc, "stages": list(names), "bound": bound, "ms_per_step": ms,
                     "launches": n, "launches_expected": expect, "achieved": achieved, "peak": peak,
