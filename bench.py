@@ -579,9 +579,15 @@ def main():
 
     K0 = args.K
     tokens = B * G
+    # passes other than the headline (the stage table, the other refresh intervals): half
+    # the headline's generations, at most 3 on the workloads whose generations take seconds
+    long_gen = T * (P + G) >= 2 ** 16
+    n_aux = max(1, args.steps // 2)
+    if long_gen:
+        n_aux = min(n_aux, 3)
     print(f"[bench] {workload_name(cfg)}", file=sys.stderr, flush=True)
     # 1. per-stage breakdown (HIP events around every stage, so a pass of its own)
-    _, _, stages = timed(K0, max(1, args.steps // 2), args.warmup, profile=-1)
+    _, _, stages = timed(K0, n_aux, min(args.warmup, 1) if long_gen else args.warmup, profile=-1)
     kernels = kernel_table(cfg, B, K0, stages)
     for k in kernels:
         print(f"[bench]   {k['ms_per_step']:8.3f} ms  {k['achieved']:8.1f} {k['unit']:7s} ({100 * k['frac']:.1f}% "
@@ -601,7 +607,7 @@ def main():
         for K in cfg["Ks"]:
             if K == K0:
                 continue
-            kms, _, _ = timed(K, max(1, args.steps // 2), 0 if T * (P + G) >= 2 ** 16 else 1)
+            kms, _, _ = timed(K, n_aux, 0 if long_gen else 1)
             sweep[f"K={K}"] = {"tokens_per_s": tokens / (kms / 1e3), "ms_per_step": kms}
             print(f"[bench] K={K}: {kms:.3f} ms -> {tokens / (kms / 1e3):.1f} tokens/s", file=sys.stderr,
                   flush=True)
