@@ -460,6 +460,55 @@ __global__ void resid_reduce_kernel(const float* part, int S, int M, int N, floa
   *r = x;
 }
 
+// resid[m, :] += sum_s part[s, m, :] as above, then y[m, :] = bf16(resid[m, :] * rsqrt(
+// mean(resid[m, :]^2) + eps) * g): the RMSNorm that follows a residual product, in the
+// same pass over the row.  One block of 256 threads per row, NV float4 per thread
+// (N <= 1024 NV): every slice load of the row is independent, so the row costs one
+// round trip; the row's sum of squares is a block reduction.
+template <int NV>
+__global__ __launch_bounds__(256) void resid_reduce_rms_kernel(const float* part, int S, int M, int N, float* resid,
+                                                               int ldr, const float* g, float eps, bf16* y) {
+  __shared__ float red[4];
+  const int m = blockIdx.x, t = threadIdx.x;
+  const size_t MN = (size_t)M * N;
+  float4 x[NV];
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = (t + 256 * i) * 4;
+    if (c < N) {
+      float4 acc = *reinterpret_cast<const float4*>(part + (size_t)m * N + c);
+      for (int k = 1; k < S; ++k) {
+        const float4 v = *reinterpret_cast<const float4*>(part + k * MN + (size_t)m * N + c);
+        acc.x += v.x;
+        acc.y += v.y;
+        acc.z += v.z;
+        acc.w += v.w;
+      }
+      float4* r = reinterpret_cast<float4*>(resid + (size_t)m * ldr + c);
+      float4 v = *r;
+      v.x += acc.x;
+      v.y += acc.y;
+      v.z += acc.z;
+      v.w += acc.w;
+      *r = v;
+      x[i] = v;
+      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+  }
+  ss = block_sum(ss, red);
+  const float rs = rsqrtf(ss / N + eps);
+  bf16* yr = y + (size_t)m * N;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = (t + 256 * i) * 4;
+    if (c < N) {
+      const float4 w = *reinterpret_cast<const float4*>(g + c);
+      store4(yr + c, x[i].x * rs * w.x, x[i].y * rs * w.y, x[i].z * rs * w.z, x[i].w * rs * w.w);
+    }
+  }
+}
+
 // K slices of a residual product on 256 x 256 tiles, one block per CU: the S in
 // [2, 16] (each slice >= 8 K tiles, slices as even as the tile count allows) that
 // minimises the modelled time, in K-step units: rounds of 256 blocks x (K tiles per
@@ -515,6 +564,7 @@ int gemm_resid_slices(int M, int N, int K) {
   const int S256 = resid_slices256(M, N, K);
   return S256 > 1 ? S256 : resid_slices(M, N, K);
 }
+bool gemm_resid_norms(int M, int N, int K) { return gemm_resid_slices(M, N, K) > 1 && N % 4 == 0 && N <= 8192; }
 
 hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e, hipStream_t s) {
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
@@ -535,6 +585,25 @@ hipError_t gemm(DType dt, const GemmProblem& p, EpiKind kind, const EpiParams& e
       hipError_t err = S256 > 1 ? launch_bf16<256, 256, 2, 2, 4, 1, EPI_STORE_F32>(q, f, s)
                                 : launch_bf16<128, 128, 2, 2, 2, 2, EPI_STORE_F32>(q, f, s);
       if (err != hipSuccess) return err;
+      if (e.norm_out) {  // the ordered sum and the RMSNorm of the updated rows in one pass
+        if (!gemm_resid_norms(p.M, p.N, p.K) || !e.norm_g) return hipErrorInvalidValue;
+        const float* part = static_cast<const float*>(e.part);
+        bf16* y = static_cast<bf16*>(e.norm_out);
+        const int nv = (p.N + 1023) / 1024;
+        if (nv <= 1)
+          hipLaunchKernelGGL(resid_reduce_rms_kernel<1>, dim3(p.M), dim3(256), 0, s, part, S, p.M, p.N, e.resid, e.ldr,
+                             e.norm_g, e.norm_eps, y);
+        else if (nv <= 2)
+          hipLaunchKernelGGL(resid_reduce_rms_kernel<2>, dim3(p.M), dim3(256), 0, s, part, S, p.M, p.N, e.resid, e.ldr,
+                             e.norm_g, e.norm_eps, y);
+        else if (nv <= 5)
+          hipLaunchKernelGGL(resid_reduce_rms_kernel<5>, dim3(p.M), dim3(256), 0, s, part, S, p.M, p.N, e.resid, e.ldr,
+                             e.norm_g, e.norm_eps, y);
+        else
+          hipLaunchKernelGGL(resid_reduce_rms_kernel<8>, dim3(p.M), dim3(256), 0, s, part, S, p.M, p.N, e.resid, e.ldr,
+                             e.norm_g, e.norm_eps, y);
+        return hipGetLastError();
+      }
       const long total = (long)p.M * (p.N / 4);
       hipLaunchKernelGGL(resid_reduce_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
                          static_cast<const float*>(e.part), S, p.M, p.N, e.resid, e.ldr);

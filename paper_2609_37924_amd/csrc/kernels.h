@@ -99,6 +99,12 @@ struct EpiParams {
   float inv_temp = 1.f;
   void* part = nullptr;
   size_t split_stride = 0;  // elements between the K slices' outputs (EPI_STORE_F32, ksplit > 1)
+  // EPI_RESID split over K with gemm_resid_norms(M, N, K): the ordered sum of the slices
+  // also writes the RMSNorm of each updated row, norm_out[m, :] (bf16) =
+  // resid[m, :] * rsqrt(mean(resid[m, :]^2) + norm_eps) * norm_g
+  const float* norm_g = nullptr;
+  float norm_eps = 0.f;
+  void* norm_out = nullptr;
 };
 
 // Sampling partial of one (row, 64-entry vocabulary group): the group maximum m_g of
@@ -124,6 +130,9 @@ int gemm_split_slices(int M, int N, int K);
 // K slices of a bf16 EPI_RESID product given a part buffer (1: no split; else
 // part holds slices * M * N floats): long K with few 128 x 128 tiles.
 int gemm_resid_slices(int M, int N, int K);
+// Whether a bf16 EPI_RESID product of this shape (split over K) can also write the RMSNorm
+// of its updated rows (EpiParams::norm_out); otherwise the caller normalises them.
+bool gemm_resid_norms(int M, int N, int K);
 
 // ---- norms / embedding / elementwise (norm.hip)
 // out[t, :] = embed[tok[t], :] as float32; `embed` has table_rows rows of length d

@@ -474,8 +474,12 @@ struct KVTarget {
 };
 
 // One pre-norm layer on x [N, d]; prenormed: ws.xn already holds the attention norm of x.
+// next_norm: the attention-norm gains of the layer that follows (nullptr if none); when
+// the FFN down product's slice sum can write that norm, it does, and *next_prenormed is
+// set.
 static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int pos0, KVTarget kv,
-                             bool prenormed = false) {
+                             bool prenormed = false, const float* next_norm = nullptr,
+                             bool* next_prenormed = nullptr) {
   const tadm_config& c = m->cfg;
   const LayerIdx& w = m->lay.layers[li];
   Workspace& s = m->ws;
@@ -488,6 +492,8 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
   if (capture)
     HIPCHK(hipMemcpyAsync(m->layer_cap + 2 * (size_t)li * slot, x, slot * 4, hipMemcpyDeviceToDevice, st));
   if (!prenormed) HIPCHK(rms_norm(m->dt, x, m->Wf(w.attn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
+  if (next_prenormed) *next_prenormed = false;
+  bool fused_norm = false;
   {
     // q/k/v projection with the rotary embedding and head split in the epilogue
     GemmProblem p{N, (H + 2 * Hk) * dh, d, s.xn, d, d, nullptr, 0, m->W(w.wqkv), d};
@@ -516,15 +522,21 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
     e.resid = x;
     e.ldr = d;
     const int S = m->dt == BF16 ? gemm_resid_slices(N, d, H * dh) : 1;
+    fused_norm = m->dt == BF16 && gemm_resid_norms(N, d, H * dh);
     if (S > 1) {
       TRY(ensure_kpart(m, (size_t)S * N * d));
       e.part = s.kpart;
+    }
+    if (fused_norm) {  // the slice sum writes the FFN norm of the updated rows
+      e.norm_g = m->Wf(w.ffn_norm);
+      e.norm_eps = c.rms_eps;
+      e.norm_out = s.xn;
     }
     TRY(prof_begin(m, TADM_STAGE_OPROJ, S > 1));
     HIPCHK(gemm(m->dt, p, EPI_RESID, e, st));
     TRY(prof_end(m, TADM_STAGE_OPROJ));
   }
-  HIPCHK(rms_norm(m->dt, x, m->Wf(w.ffn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
+  if (!fused_norm) HIPCHK(rms_norm(m->dt, x, m->Wf(w.ffn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
   TRY(prof_begin(m, TADM_STAGE_FFN_UP));
   if (c.ffn_kind == TADM_FFN_GELU) {
     GemmProblem p{N, F, d, s.xn, d, d, nullptr, 0, m->W(w.wup), d};
@@ -557,6 +569,12 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
       TRY(ensure_kpart(m, (size_t)S * N * d));
       e.part = s.kpart;
     }
+    if (next_norm && next_prenormed && m->dt == BF16 && gemm_resid_norms(N, d, F)) {
+      e.norm_g = next_norm;  // the slice sum writes the next layer's attention norm
+      e.norm_eps = c.rms_eps;
+      e.norm_out = s.xn;
+      *next_prenormed = true;
+    }
     TRY(prof_begin(m, TADM_STAGE_FFN_DOWN, S > 1));
     HIPCHK(gemm(m->dt, p, EPI_RESID, e, st));
     TRY(prof_end(m, TADM_STAGE_FFN_DOWN));
@@ -574,8 +592,13 @@ static KVTarget kv_target(tadm_model* m, const tadm_context* ctx, int li) {
 // prenormed: ws.xn already holds the first layer's attention norm of x
 static tadm_status run_part(tadm_model* m, int first, int count, float* x, int B, int L, int pos0,
                             const tadm_context* ctx, bool prenormed = false) {
-  for (int li = first; li < first + count; ++li)
-    TRY(run_layer(m, li, x, B, L, pos0, kv_target(m, ctx, li), prenormed && li == first));
+  bool pre = prenormed;
+  for (int li = first; li < first + count; ++li) {
+    const float* next_norm = li + 1 < first + count ? m->Wf(m->lay.layers[li + 1].attn_norm) : nullptr;
+    bool next_pre = false;
+    TRY(run_layer(m, li, x, B, L, pos0, kv_target(m, ctx, li), pre, next_norm, &next_pre));
+    pre = next_pre;
+  }
   return TADM_OK;
 }
 
