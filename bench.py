@@ -289,13 +289,13 @@ def render_counter_summary(fetch_dir, write_dir, mfma_dir=None, command=""):
         calls = len(fk)
         if "oproj" in names:
             # a residual product split over K is two kernels, the fp32 slices and their
-            # ordered reduction: its bytes are both kernels', and it is one launch of the
-            # stage (the reduction marks it)
-            red = [r for r in fetch if "resid_reduce_kernel" in r["Kernel_Name"]]
+            # ordered reduction (with or without the RMSNorm that follows): its bytes are
+            # both kernels', and it is one launch of the stage (the reduction marks it)
+            red = [r for r in fetch if "resid_reduce" in r["Kernel_Name"]]
             if red:
                 sx = re.compile(SLICE_PATTERN)
                 fk += red + [r for r in fetch if sx.search(r["Kernel_Name"])]
-                wk += [r for r in write if "resid_reduce_kernel" in r["Kernel_Name"] or sx.search(r["Kernel_Name"])]
+                wk += [r for r in write if "resid_reduce" in r["Kernel_Name"] or sx.search(r["Kernel_Name"])]
                 calls += len(red)
         if not fk or len(fk) != len(wk):
             continue

@@ -9,7 +9,8 @@
 // otherwise); q/k/v [M, d] x [(H + 2 Hkv) dh, d] with the rotary epilogue; attention over
 // the pass's queries and its keys (the prompt as context plus the block in block mode);
 // attention output [M, H dh] x [d, H dh] and FFN down [M, d_ffn] x [d, d_ffn] with the
-// residual epilogue (K-sliced as the library slices them); FFN up [M, d] x [2 d_ffn or
+// residual epilogue (K-sliced as the library slices them, the slice sum also writing the
+// following RMSNorm where the library's does); FFN up [M, d] x [2 d_ffn or
 // d_ffn, d] with its GLU / GELU epilogue.  Operands are seeded uniform bf16 values.
 // Prints each stage's mean time per launch from HIP events.
 #include <hip/hip_runtime.h>
@@ -161,6 +162,10 @@ int main(int argc, char** argv) {
   HIP_OK(hipMemcpy(rope, rope_h.data(), rope_h.size() * 4, hipMemcpyHostToDevice));
   const int S_o = gemm_resid_slices(M, d, H * dh), S_d = gemm_resid_slices(M, d, F);
   float* part = alloc<float>((size_t)(S_o > S_d ? S_o : S_d) * M * d);
+  // the RMSNorm that the residual products' slice sums write when they can (unit gains)
+  float* gain = alloc<float>((size_t)d);
+  hipLaunchKernelGGL(fill_f32, dim3(16), dim3(256), 0, 0, gain, (size_t)d, 1.0f);
+  uint16_t* xn2 = alloc<uint16_t>((size_t)M * d);
   const size_t copy_n = (size_t)M * d / 4;  // float4 granules of one [M, d] float32 row block
   float* copy_dst = alloc<float>((size_t)M * d);
   HIP_OK(hipDeviceSynchronize());
@@ -215,6 +220,11 @@ int main(int argc, char** argv) {
     e.resid = x;
     e.ldr = d;
     if (S_o > 1) e.part = part;
+    if (gemm_resid_norms(M, d, H * dh)) {
+      e.norm_g = gain;
+      e.norm_eps = 1e-6f;
+      e.norm_out = xn2;
+    }
     return gemm(BF16, p, EPI_RESID, e, st);
   });
   stage("ffn_up", 2.0 * M * d * Nup, [&]() {
@@ -230,11 +240,17 @@ int main(int argc, char** argv) {
     e.resid = x;
     e.ldr = d;
     if (S_d > 1) e.part = part;
+    if (gemm_resid_norms(M, d, F)) {
+      e.norm_g = gain;
+      e.norm_eps = 1e-6f;
+      e.norm_out = xn2;
+    }
     return gemm(BF16, p, EPI_RESID, e, st);
   });
   HIP_OK(hipStreamSynchronize(st));
   for (void* p : {(void*)xn, (void*)wqkv, (void*)wo, (void*)wup, (void*)wdown, (void*)ao, (void*)ffn, (void*)q,
-                  (void*)kc, (void*)vt, (void*)x, (void*)rope, (void*)part, (void*)copy_dst})
+                  (void*)kc, (void*)vt, (void*)x, (void*)rope, (void*)part, (void*)copy_dst, (void*)gain,
+                  (void*)xn2})
     HIP_OK(hipFree(p));
   HIP_OK(hipStreamDestroy(st));
   return 0;
