@@ -193,21 +193,42 @@ def traffic_path(config, K):
     return os.path.join(ROOT, "profiles", f"{config}_k{K}_hbm_traffic.md")
 
 
-TRAFFIC_LINE = re.compile(r"^traffic stage=(\S+) bytes_per_launch=(\S+) sources=(\S+)$")
+TRAFFIC_LINE = re.compile(r"^traffic stage=(\S+) bytes_per_launch=(\S+)(?: mfma_busy=(\S+))? sources=(\S+)$")
+
+
+def stored_counters(config, K, stage, source):
+    """(HBM bytes per launch, MFMA busy %) of a kernel group from the committed counter
+    summary of this workload; (None, None) when there is none or the kernel's sources
+    changed since (the busy share is None where the summary has none)."""
+    path = traffic_path(config, K)
+    if not os.path.exists(path):
+        return None, None
+    with open(path) as f:
+        for line in f:
+            mt = TRAFFIC_LINE.match(line.strip())
+            if mt and mt.group(1) == stage and mt.group(4) == source_digest(source):
+                return float(mt.group(2)), (float(mt.group(3)) if mt.group(3) else None)
+    return None, None
 
 
 def stored_traffic(config, K, stage, source):
     """HBM bytes per launch of a kernel from the committed counter summary of this
     workload, or None when there is none or the kernel's sources changed since."""
-    path = traffic_path(config, K)
-    if not os.path.exists(path):
-        return None
-    with open(path) as f:
-        for line in f:
-            mt = TRAFFIC_LINE.match(line.strip())
-            if mt and mt.group(1) == stage and mt.group(3) == source_digest(source):
-                return float(mt.group(2))
-    return None
+    return stored_counters(config, K, stage, source)[0]
+
+
+def attach_counters(config, K, kernels):
+    """Per kernel group, the achieved HBM bandwidth (counter bytes per launch x launches
+    / stage time) and the MFMA busy share, from the committed counter summary."""
+    for r in kernels:
+        source = next(k[4] for k in KERNELS if k[0] == r["kernel"])
+        b, busy = stored_counters(config, K, r["stages"][0], source)
+        if b is not None:
+            gbs = b * r["launches"] / (r["ms_per_step"] / 1e3) / 1e9
+            r["hbm_bytes_per_launch"], r["hbm_gbs"], r["hbm_frac"] = b, gbs, gbs / PEAK_HBM_GBS
+        if busy is not None:
+            r["mfma_busy_pct"] = busy
+    return kernels
 
 
 # ------------------------------------------------------------ profile render ---
@@ -301,7 +322,11 @@ def render_counter_summary(fetch_dir, write_dir, mfma_dir=None, command=""):
             continue
         b = (sum(float(r["Counter_Value"]) for r in fk) * sf + sum(float(r["Counter_Value"]) for r in wk) * sw) \
             * 1024.0 / calls
-        print(f"    traffic stage={names[0]} bytes_per_launch={b:.0f} sources={source_digest(source)}")
+        # MFMA busy share of the group's products (its dispatches other than a slice reduction)
+        busy = [u for n, us in util.items() if rx.search(n) or ("oproj" in names and re.search(SLICE_PATTERN, n))
+                for u in us]
+        mb = f" mfma_busy={sum(busy) / len(busy):.1f}" if busy else ""
+        print(f"    traffic stage={names[0]} bytes_per_launch={b:.0f}{mb} sources={source_digest(source)}")
         print(f"      ({desc}: {calls} launches, {len(fk)} dispatches, {b / 1e6:.3f} MB per launch)")
 
 
@@ -588,7 +613,7 @@ def main():
     print(f"[bench] {workload_name(cfg)}", file=sys.stderr, flush=True)
     # 1. per-stage breakdown (HIP events around every stage, so a pass of its own)
     _, _, stages = timed(K0, n_aux, min(args.warmup, 1) if long_gen else args.warmup, profile=-1)
-    kernels = kernel_table(cfg, B, K0, stages)
+    kernels = attach_counters(args.config, K0, kernel_table(cfg, B, K0, stages))
     for k in kernels:
         print(f"[bench]   {k['ms_per_step']:8.3f} ms  {k['achieved']:8.1f} {k['unit']:7s} ({100 * k['frac']:.1f}% "
               f"of peak)  {k['launches']} launches  {k['kernel']}", file=sys.stderr, flush=True)
