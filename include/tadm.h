@@ -331,11 +331,12 @@ enum { TADM_TAP_EMBED = 0, TADM_TAP_FUSED = 1, TADM_TAP_FINAL = 2, TADM_TAP_CHOI
 /* Keep a copy of h~ for TADM_TAP_FUSED (one extra [B, L, d] copy per step; off by default). */
 tadm_status tadm_debug_taps(tadm_model* m, int32_t enable);
 /* Per-layer capture for layer-by-layer checks: from now on every transformer layer li
- * that runs (in any call) copies the residual stream entering it to slot 2 li and the
- * stream leaving it to slot 2 li + 1 of dst_dev, each slot [B, L, d] float32 of that
- * call (caller-owned, bytes = capacity; a layer whose slots do not fit is skipped).
- * A slot holds the last call that ran the layer.  dst_dev = NULL turns capture off.
- * Costs two device copies per layer; for tests. */
+ * that runs (in any call) copies the residual stream entering it to slot 3 li, the
+ * stream after its attention half to slot 3 li + 1 and the stream leaving it to slot
+ * 3 li + 2 of dst_dev, each slot [B, L, d] float32 of that call (caller-owned, bytes =
+ * capacity; a layer whose slots do not fit is skipped).  A slot holds the last call
+ * that ran the layer.  dst_dev = NULL turns capture off.  Costs three device copies per
+ * layer; for tests. */
 tadm_status tadm_debug_layers(tadm_model* m, float* dst_dev, size_t bytes);
 /* Enqueues copies of one layer's context K [B, Hkv, cap, head_dim] (rotary embedding
  * applied) and V transposed [B, Hkv, head_dim, cap], in the model dtype; positions

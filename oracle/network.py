@@ -110,10 +110,11 @@ class Weights:
 
 
 # ------------------------------------------------------------- transformer layer
-def transformer_layer(W, li, x, pos, ctx_kv=None):
-    """One pre-norm layer on one row. x [L, d]; ctx_kv = (k, v) of earlier context.
+def attention_sublayer(W, li, x, pos, ctx_kv=None):
+    """The attention half of one pre-norm layer on one row: x + O Attn(RoPE(Q, K), V) of
+    the RMS-normed x.  x [L, d]; ctx_kv = (k, v) of earlier context.
 
-    Returns (x_out, (k, v)) where k already carries its rotary embedding.
+    Returns (x_mid, (k, v)) where k already carries its rotary embedding.
     """
     cfg = W.cfg
     H, Hkv, dh = cfg["n_heads"], cfg["n_kv_heads"], cfg["head_dim"]
@@ -132,8 +133,16 @@ def transformer_layer(W, li, x, pos, ctx_kv=None):
     else:
         k_all, v_all = k, v
     o = op(attention(q, k_all, v_all, op).reshape(L, H * dh))
-    x = x + o @ W[p + "wo"].T
-    xn = op(rms_norm(x, W[p + "ffn_norm"], eps))
+    return x + o @ W[p + "wo"].T, (k, v)
+
+
+def ffn_sublayer(W, li, x):
+    """The feed-forward half of one pre-norm layer on one row: x + FFN of the RMS-normed x
+    (GeLU, SwiGLU or GeGLU)."""
+    cfg = W.cfg
+    p = f"layer{li}."
+    op = lambda t: operand(cfg, t)  # noqa: E731
+    xn = op(rms_norm(x, W[p + "ffn_norm"], cfg["rms_eps"]))
     kind = cfg["ffn_kind"]
     if kind == "gelu":
         f = gelu(xn @ W[p + "w_up"].T)
@@ -143,7 +152,18 @@ def transformer_layer(W, li, x, pos, ctx_kv=None):
         f = gelu(xn @ W[p + "w_gate"].T) * (xn @ W[p + "w_up"].T)
     else:
         raise ValueError(kind)
-    return x + op(f) @ W[p + "w_down"].T, (k, v)
+    return x + op(f) @ W[p + "w_down"].T
+
+
+def transformer_layer(W, li, x, pos, ctx_kv=None):
+    """One pre-norm layer on one row (App. C.2: DiT block, no time conditioning): the
+    attention half, then the feed-forward half.  x [L, d]; ctx_kv = (k, v) of earlier
+    context.
+
+    Returns (x_out, (k, v)) where k already carries its rotary embedding.
+    """
+    x, kv = attention_sublayer(W, li, x, pos, ctx_kv)
+    return ffn_sublayer(W, li, x), kv
 
 
 def layer_ids(cfg, part):

@@ -288,7 +288,8 @@ struct tadm_model {
   void* embT = nullptr;            // embedding rows [0, V) transposed, [d, round64(V)] (lazy)
   bool embT_valid = false;
   int tap_B = 0, tap_L = 0, tap_Lc = 0;
-  // per-layer capture (tadm_debug_layers): residual stream entering and leaving each layer
+  // per-layer capture (tadm_debug_layers): residual stream entering each layer, after its
+  // attention half and leaving it
   float* layer_cap = nullptr;
   size_t layer_cap_bytes = 0;
   // profiling
@@ -486,11 +487,12 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
   const int N = B * L, d = c.d_model, H = c.n_heads, Hk = c.n_kv_heads, dh = c.head_dim,
             F = c.d_ffn;
   const hipStream_t st = m->stream;
-  // capture slots: 2 li (entering layer li) and 2 li + 1 (leaving it), [N, d] float32 each
+  // capture slots: 3 li (entering layer li), 3 li + 1 (after its attention half) and
+  // 3 li + 2 (leaving it), [N, d] float32 each
   const size_t slot = (size_t)N * d;
-  const bool capture = m->layer_cap && (2 * (size_t)li + 2) * slot * 4 <= m->layer_cap_bytes;
+  const bool capture = m->layer_cap && (3 * (size_t)li + 3) * slot * 4 <= m->layer_cap_bytes;
   if (capture)
-    HIPCHK(hipMemcpyAsync(m->layer_cap + 2 * (size_t)li * slot, x, slot * 4, hipMemcpyDeviceToDevice, st));
+    HIPCHK(hipMemcpyAsync(m->layer_cap + 3 * (size_t)li * slot, x, slot * 4, hipMemcpyDeviceToDevice, st));
   if (!prenormed) HIPCHK(rms_norm(m->dt, x, m->Wf(w.attn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
   if (next_prenormed) *next_prenormed = false;
   bool fused_norm = false;
@@ -536,6 +538,8 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
     HIPCHK(gemm(m->dt, p, EPI_RESID, e, st));
     TRY(prof_end(m, TADM_STAGE_OPROJ));
   }
+  if (capture)
+    HIPCHK(hipMemcpyAsync(m->layer_cap + (3 * (size_t)li + 1) * slot, x, slot * 4, hipMemcpyDeviceToDevice, st));
   if (!fused_norm) HIPCHK(rms_norm(m->dt, x, m->Wf(w.ffn_norm), c.rms_eps, N, d, N, 0, 0, s.xn, st));
   TRY(prof_begin(m, TADM_STAGE_FFN_UP));
   if (c.ffn_kind == TADM_FFN_GELU) {
@@ -580,7 +584,7 @@ static tadm_status run_layer(tadm_model* m, int li, float* x, int B, int L, int 
     TRY(prof_end(m, TADM_STAGE_FFN_DOWN));
   }
   if (capture)
-    HIPCHK(hipMemcpyAsync(m->layer_cap + (2 * (size_t)li + 1) * slot, x, slot * 4, hipMemcpyDeviceToDevice, st));
+    HIPCHK(hipMemcpyAsync(m->layer_cap + (3 * (size_t)li + 2) * slot, x, slot * 4, hipMemcpyDeviceToDevice, st));
   return TADM_OK;
 }
 
