@@ -221,7 +221,8 @@ def attach_counters(config, K, kernels):
     """Per kernel group, the achieved HBM bandwidth (counter bytes per launch x launches
     / stage time) and the MFMA busy share, from the committed counter summary."""
     for r in kernels:
-        source = next(k[4] for k in KERNELS if k[0] == r["kernel"])
+        # by stage: the float32 workloads' rows carry a renamed description
+        source = next(k[4] for k in KERNELS if k[1][0] == r["stages"][0])
         b, busy = stored_counters(config, K, r["stages"][0], source)
         if b is not None:
             gbs = b * r["launches"] / (r["ms_per_step"] / 1e3) / 1e9
@@ -742,7 +743,7 @@ def main():
         dom = None
     if dom:
         live = next(r for r in kernel_table(cfg, B, K0, dom_stages) if r["kernel"] == dom["kernel"])
-        source = next(k[4] for k in KERNELS if k[0] == dom["kernel"])
+        source = next(k[4] for k in KERNELS if k[1][0] == dom["stages"][0])
         traffic = stored_traffic(args.config, K0, dom["stages"][0], source)
         avg_ms = live["ms_per_step"] / live["launches"]
         roof = {"kernel": live["kernel"], "bound": live["bound"], "achieved": live["achieved"],

@@ -63,8 +63,25 @@ typedef const __attribute__((address_space(1))) void* gbl_ptr;
 // an XCD holds at once (gm * gn of them) cover a gm x gn patch of tiles, which keeps the
 // A and W rows that the XCD streams in at each K step (gm*BM + gn*BN) low; without a
 // patch (gm = 0) the region is walked m first.
-__device__ __forceinline__ void tile_of(const GemmProblem& p, int tiles_m, int& tm, int& tn) {
+// A grid with no even split into 8 regions is walked in bands of `band` tile rows, each
+// band column by column, and XCD x takes the x-th eighth of that walk: the blocks it
+// holds at once cover about band x (R / band) tiles.  The grid is then padded to a
+// multiple of 8 blocks; a padded block gets tm = tiles_m and does nothing.
+__device__ __forceinline__ void tile_of(const GemmProblem& p, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int b = blockIdx.x;
+  if (p.band > 0) {
+    const int tiles = tiles_m * tiles_n, chunk = (tiles + 7) / 8, o = (b % 8) * chunk + b / 8;
+    if (o >= tiles) {
+      tm = tiles_m;
+      tn = 0;
+      return;
+    }
+    const int per = p.band * tiles_n, g = o / per, first = g * p.band, j = o - g * per;
+    const int h = min(p.band, tiles_m - first);
+    tm = first + j % h;
+    tn = j / h;
+    return;
+  }
   if (p.rm > 0) {
     const int x = b % 8, i = b / 8, regions_m = tiles_m / p.rm;
     int lm, ln;
@@ -119,7 +136,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, MINB) void gemm_bf16_kernel(GemmPro
   const int wm = wave % WGM, wn = wave / WGM;
   const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
   int tmi, tni;
-  tile_of(p, tiles_m, tmi, tni);
+  tile_of(p, tiles_m, tiles_n, tmi, tni);
+  if (tmi >= tiles_m) return;  // padding of a banded grid
   const int m0 = tmi * BM, n0 = tni * BN;
   if (p.M_dev) {  // rows present this call; the grid was sized for p.M
     p.M = min(*p.M_dev, p.M);
@@ -349,6 +367,22 @@ inline void xcd_patch(int rm, int rn, int BM, int BN, int R, int& gm, int& gn) {
   }
 }
 
+// Band height h <= tiles_m of the banded walk that streams the fewest rows per K step
+// for R blocks held at once (h * BM + ceil(R / h) * BN).  1B-class head, 16 512 x 50 304 x
+// 2 048 on 128 x 128 tiles (129 x 393, no even split): h = 8.
+inline int xcd_band(int tiles_m, int BM, int BN, int R) {
+  int best_h = 1;
+  long best = -1;
+  for (int h = 1; h <= tiles_m && h <= R; ++h) {
+    const long cost = (long)h * BM + (long)((R + h - 1) / h) * BN;
+    if (best < 0 || cost < best) {
+      best = cost;
+      best_h = h;
+    }
+  }
+  return best_h;
+}
+
 template <int BM, int BN, int ST, int WGM, int WGN, int MINB, EpiKind K>
 hipError_t launch_bf16(const GemmProblem& p0, const EpiParams& e, hipStream_t s) {
   GemmProblem p = p0;
@@ -356,9 +390,11 @@ hipError_t launch_bf16(const GemmProblem& p0, const EpiParams& e, hipStream_t s)
   xcd_regions(tiles_m, tiles_n, BM, BN, p.rm, p.rn);
   // one block per CU for the 8-wave tiles, MINB per CU otherwise (LDS bounds both)
   if (MINB <= 2) xcd_patch(p.rm, p.rn, BM, BN, 32 * MINB, p.gm, p.gn);
+  p.band = p.rm > 0 ? 0 : xcd_band(tiles_m, BM, BN, 32 * MINB);
+  const int blocks = p.band > 0 ? (tiles_m * tiles_n + 7) / 8 * 8 : tiles_m * tiles_n;
   p.w_first = p.N > p.M;
-  launch_timed(gemm_bf16_kernel<BM, BN, ST, WGM, WGN, MINB, K>, dim3(tiles_m * tiles_n, p.ksplit),
-               dim3(64 * WGM * WGN), 0, s, p, e);
+  launch_timed(gemm_bf16_kernel<BM, BN, ST, WGM, WGN, MINB, K>, dim3(blocks, p.ksplit), dim3(64 * WGM * WGN), 0, s, p,
+               e);
   return hipGetLastError();
 }
 

@@ -11,10 +11,13 @@
 // attention output [M, H dh] x [d, H dh] and FFN down [M, d_ffn] x [d, d_ffn] with the
 // residual epilogue (K-sliced as the library slices them, the slice sum also writing the
 // following RMSNorm where the library's does); FFN up [M, d] x [2 d_ffn or
-// d_ffn, d] with its GLU / GELU epilogue.  Operands are seeded uniform bf16 values.
+// d_ffn, d] with its GLU / GELU epilogue; the vocabulary projection [Mh, d] x [V, d]
+// with the sampling epilogue, Mh the masked rows a reverse step sees on average under
+// the linear schedule.  Operands are seeded uniform bf16 values.
 // Prints each stage's mean time per launch from HIP events.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -54,6 +57,10 @@ __global__ void fill_bf16(uint16_t* out, size_t n, float scale, uint64_t seed) {
     memcpy(&b, &v, 4);
     out[i] = (uint16_t)(b >> 16);
   }
+}
+
+__global__ void fill_iota(int32_t* out, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) out[i] = i;
 }
 
 __global__ void fill_f32(float* out, size_t n, float v) {
@@ -118,6 +125,7 @@ int main(int argc, char** argv) {
   const int d = (int)num(kv, "d_model", 0, true), H = (int)num(kv, "n_heads", 0, true);
   const int Hkv = (int)num(kv, "n_kv_heads", H), dh = (int)num(kv, "head_dim", 0, true);
   const int F = (int)num(kv, "d_ffn", 0, true), ffn_kind = (int)num(kv, "ffn_kind", 1);
+  const int V = (int)num(kv, "vocab", 0, true), T = (int)num(kv, "T", 0, true);
   const int reps = (int)num(kv, "reps", 5);
   const double theta = num(kv, "rope_theta", 10000.0);
   if ((int)num(kv, "dtype", 1) != 1) {
@@ -125,7 +133,7 @@ int main(int argc, char** argv) {
     return 1;
   }
   if (B <= 0 || G <= 0 || BL <= 0 || P < 0 || d <= 0 || H <= 0 || Hkv <= 0 || H % Hkv || dh <= 0 || F <= 0 ||
-      reps <= 0 || d % 64 || F % 64 || (H * dh) % 64 || (dh != 64 && dh != 128)) {
+      reps <= 0 || d % 64 || F % 64 || (H * dh) % 64 || (dh != 64 && dh != 128) || V <= 0 || T <= 0) {
     fprintf(stderr, "kernel_bench: unsupported shape\n");
     return 1;
   }
@@ -134,6 +142,11 @@ int main(int argc, char** argv) {
   const int ctx = block_mode ? P : 0;           // context keys ahead of them
   const int Lk = ctx + L, cap = Lk + 64;       // keys; K/V capacity (whole key tiles)
   const int M = B * L, Nqkv = (H + 2 * Hkv) * dh, Nup = ffn_kind == 0 ? F : 2 * F;
+  // head rows: the positions still masked before a reverse step, floor(BL i / T) of each
+  // row's BL at step i, averaged over the T steps of a block
+  long long head_sum = 0;
+  for (int i = 1; i <= T; ++i) head_sum += (long long)B * (((long long)BL * i) / T);
+  const int Mh = std::max(1, (int)((head_sum + T / 2) / T)), ng = (V + 63) / 64;
   HIP_OK(hipSetDevice(0));
   hipStream_t st;
   HIP_OK(hipStreamCreate(&st));
@@ -166,12 +179,17 @@ int main(int argc, char** argv) {
   float* gain = alloc<float>((size_t)d);
   hipLaunchKernelGGL(fill_f32, dim3(16), dim3(256), 0, 0, gain, (size_t)d, 1.0f);
   uint16_t* xn2 = alloc<uint16_t>((size_t)M * d);
+  uint16_t* wout = random_bf16((size_t)V * d, 1.0f / sqrtf((float)d), 10);
+  int32_t* hidx = alloc<int32_t>((size_t)Mh);
+  hipLaunchKernelGGL(fill_iota, dim3(64), dim3(256), 0, 0, hidx, Mh);
+  SamplePart* hpart = alloc<SamplePart>((size_t)Mh * ng);
   const size_t copy_n = (size_t)M * d / 4;  // float4 granules of one [M, d] float32 row block
   float* copy_dst = alloc<float>((size_t)M * d);
   HIP_OK(hipDeviceSynchronize());
 
-  printf("kernel_bench: M = %d x %d = %d rows, d %d, heads %d/%d x %d, ffn %d (%s), keys %d; K slices %d / %d\n", B, L,
-         M, d, H, Hkv, dh, F, ffn_kind == 0 ? "gelu" : ffn_kind == 1 ? "swiglu" : "geglu", Lk, S_o, S_d);
+  printf("kernel_bench: M = %d x %d = %d rows, d %d, heads %d/%d x %d, ffn %d (%s), keys %d; K slices %d / %d; "
+         "head %d rows x V %d\n", B, L, M, d, H, Hkv, dh, F, ffn_kind == 0 ? "gelu" : ffn_kind == 1 ? "swiglu" : "geglu",
+         Lk, S_o, S_d, Mh, V);
   fflush(stdout);
   hipEvent_t e0, e1;
   HIP_OK(hipEventCreate(&e0));
@@ -247,10 +265,23 @@ int main(int argc, char** argv) {
     }
     return gemm(BF16, p, EPI_RESID, e, st);
   });
+  stage("head", 2.0 * Mh * d * V, [&]() {
+    GemmProblem p{Mh, V, d, xn, d, d, nullptr, 0, wout, d};
+    EpiParams e;
+    e.rows_idx = hidx;
+    e.Lc = L;
+    e.pos_base = ctx;
+    e.n_groups = ng;
+    e.step_id = 1;
+    e.k0 = 0x2545F491u;
+    e.k1 = 0x4F6CDD1Du;
+    e.part = hpart;
+    return head_sample(p, e, st);
+  });
   HIP_OK(hipStreamSynchronize(st));
   for (void* p : {(void*)xn, (void*)wqkv, (void*)wo, (void*)wup, (void*)wdown, (void*)ao, (void*)ffn, (void*)q,
                   (void*)kc, (void*)vt, (void*)x, (void*)rope, (void*)part, (void*)copy_dst, (void*)gain,
-                  (void*)xn2})
+                  (void*)xn2, (void*)wout, (void*)hidx, (void*)hpart})
     HIP_OK(hipFree(p));
   HIP_OK(hipStreamDestroy(st));
   return 0;

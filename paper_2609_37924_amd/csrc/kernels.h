@@ -38,6 +38,7 @@ struct GemmProblem {
   const int* M_dev = nullptr;  // if set: rows actually present (<= M; M sizes the grid)
   int rm = 0, rn = 0;          // per-XCD tile region (set by the launcher)
   int gm = 0, gn = 0;          // blocks an XCD runs at once, as gm x gn tiles of its region (0: m first)
+  int band = 0;                // no even region split: band height of the banded walk (set by the launcher)
   int ksplit = 1;              // K slices (grid.y); slice s writes out + s * split_stride
   int w_first = 0;             // more weight rows than activation rows (N > M; set by the launcher)
 };

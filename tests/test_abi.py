@@ -145,9 +145,13 @@ def test_kernel_bench_rejects_bad_arguments_before_device_work():
         pytest.skip("kernel_bench not built")
     for argv, msg in (([], "missing batch"), (["foo"], "bad argument"),
                       (["batch=1", "prompt_len=0", "gen_len=8", "d_model=64", "n_heads=1", "head_dim=32",
-                        "d_ffn=64"], "unsupported shape"),
+                        "d_ffn=64", "vocab=64", "T=4"], "unsupported shape"),
+                      (["batch=1", "prompt_len=0", "gen_len=8", "d_model=64", "n_heads=1", "head_dim=64",
+                        "d_ffn=64", "vocab=0", "T=4"], "unsupported shape"),
                       (["batch=2", "prompt_len=0", "gen_len=8", "d_model=64", "n_heads=1", "head_dim=64",
-                        "d_ffn=64", "dtype=0"], "bf16 workloads only")):
+                        "d_ffn=64"], "missing vocab"),
+                      (["batch=2", "prompt_len=0", "gen_len=8", "d_model=64", "n_heads=1", "head_dim=64",
+                        "d_ffn=64", "vocab=64", "T=4", "dtype=0"], "bf16 workloads only")):
         r = subprocess.run([kb] + argv, capture_output=True, text=True, timeout=60)
         assert r.returncode == 1, (argv, r.returncode, r.stderr)
         assert msg in r.stderr, (argv, r.stderr)

@@ -99,3 +99,23 @@ def test_bench_prints_native_driver_arguments(root):
     cfg = synth.get_config("block")
     assert int(kv["batch"]) == cfg["batch"] and int(kv["block_len"]) == cfg["block_len"]
     assert int(kv["n_kv_heads"]) == cfg["n_kv_heads"] and int(kv["vocab"]) == cfg["vocab"]
+
+
+@pytest.mark.parametrize("name", ["tiny"] + CONFIGS)
+def test_kernel_table_takes_counters_for_every_workload(name):
+    """The per-kernel table and its counter fields build for every workload, the float32
+    one included (its rows are described as VALU kernels, so counters are looked up by
+    stage); a stored figure is attached only where the committed summary matches."""
+    cfg = synth.get_config(name)
+    K = cfg["Ks"][0]
+    _, launches = bench.schedule_work(cfg, cfg["batch"], K)
+    stages = {s: {"ms_per_step": 1.0 + i, "launches": n} for i, (s, n) in enumerate(sorted(launches.items())) if n}
+    rows = bench.attach_counters(name, K, bench.kernel_table(cfg, cfg["batch"], K, stages))
+    assert rows
+    for r in rows:
+        src = next(k[4] for k in bench.KERNELS if k[1][0] == r["stages"][0])
+        b, busy = bench.stored_counters(name, K, r["stages"][0], src)
+        assert r.get("hbm_bytes_per_launch") == b
+        assert r.get("mfma_busy_pct") == busy
+        if b is not None:
+            assert r["hbm_gbs"] == pytest.approx(b * r["launches"] / (r["ms_per_step"] / 1e3) / 1e9)
