@@ -645,6 +645,8 @@ def test_masked_only_head_equals_full_head():
     (1000, 256, (37, 1)),      # 128 x 128 head tiles; last normaliser group has 40 entries
     (32768, 768, (50, 9)),     # the small workload's head
     (262144, 256, (20, 3)),    # largest vocabulary: 256 x 256 head tiles, 4096 groups
+    (50304, 256, (41, 7)),     # 393 (fused) and 197 (logits) tile columns: no even split
+                               # into 8 XCD regions, so both products take the banded walk
 ])
 def test_fused_head_sampler_matches_unfused(vocab, d, masked):
     """The masked-only bf16 head samples in its epilogue.  Token and confidence of every
