@@ -13,7 +13,9 @@
 // following RMSNorm where the library's does); FFN up [M, d] x [2 d_ffn or
 // d_ffn, d] with its GLU / GELU epilogue; the vocabulary projection [Mh, d] x [V, d]
 // with the sampling epilogue, Mh the masked rows a reverse step sees on average under
-// the linear schedule.  Operands are seeded uniform bf16 values.
+// the linear schedule, and the merge of its partials into tokens; with the gated-MLP
+// fusion, its two products ([M, 2d] x [5d, 2d] with the GELU / sigmoid split and
+// [M, 4d] x [d, 4d] with the gated residual).  Operands are seeded uniform bf16 values.
 // Prints each stage's mean time per launch from HIP events.
 #include <hip/hip_runtime.h>
 
@@ -61,6 +63,15 @@ __global__ void fill_bf16(uint16_t* out, size_t n, float scale, uint64_t seed) {
 
 __global__ void fill_iota(int32_t* out, int n) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) out[i] = i;
+}
+
+// row_map of the finalize merge: the first `rows` canvas entries have partial rows
+__global__ void fill_row_map(int32_t* out, int n, int rows) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) out[i] = i < rows ? i : -1;
+}
+
+__global__ void fill_i32(int32_t* out, int n, int32_t v) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) out[i] = v;
 }
 
 __global__ void fill_f32(float* out, size_t n, float v) {
@@ -126,7 +137,7 @@ int main(int argc, char** argv) {
   const int Hkv = (int)num(kv, "n_kv_heads", H), dh = (int)num(kv, "head_dim", 0, true);
   const int F = (int)num(kv, "d_ffn", 0, true), ffn_kind = (int)num(kv, "ffn_kind", 1);
   const int V = (int)num(kv, "vocab", 0, true), T = (int)num(kv, "T", 0, true);
-  const int reps = (int)num(kv, "reps", 5);
+  const int reps = (int)num(kv, "reps", 5), fusion_kind = (int)num(kv, "fusion_kind", 0);
   const double theta = num(kv, "rope_theta", 10000.0);
   if ((int)num(kv, "dtype", 1) != 1) {
     fprintf(stderr, "kernel_bench: bf16 workloads only\n");
@@ -183,6 +194,26 @@ int main(int argc, char** argv) {
   int32_t* hidx = alloc<int32_t>((size_t)Mh);
   hipLaunchKernelGGL(fill_iota, dim3(64), dim3(256), 0, 0, hidx, Mh);
   SamplePart* hpart = alloc<SamplePart>((size_t)Mh * ng);
+  int32_t* row_map = alloc<int32_t>((size_t)M);
+  int32_t* canvas = alloc<int32_t>((size_t)M);
+  int32_t* choice = alloc<int32_t>((size_t)M);
+  float* conf = alloc<float>((size_t)M);
+  hipLaunchKernelGGL(fill_row_map, dim3(64), dim3(256), 0, 0, row_map, M, Mh);
+  hipLaunchKernelGGL(fill_i32, dim3(64), dim3(256), 0, 0, canvas, M, V);  // every position masked
+  // gated-MLP fusion: [LN(c); anchor] [M, 2d] x [5d, 2d] -> GELU hidden [M, 4d] and gate [M, d];
+  // hidden x [d, 4d] -> x = h + gate * (. + b2)
+  const bool gated = fusion_kind == 0;
+  uint16_t* fa = gated ? random_bf16((size_t)M * d, 1.0f, 11) : nullptr;
+  uint16_t* w1g = gated ? random_bf16((size_t)5 * d * 2 * d, 1.0f / sqrtf(2.0f * d), 12) : nullptr;
+  uint16_t* w2 = gated ? random_bf16((size_t)d * 4 * d, 1.0f / sqrtf(4.0f * d), 13) : nullptr;
+  uint16_t* fus_h = gated ? alloc<uint16_t>((size_t)M * 4 * d) : nullptr;
+  float* fus_g = gated ? alloc<float>((size_t)M * d) : nullptr;
+  float* fbias = gated ? alloc<float>((size_t)5 * d) : nullptr;
+  float* fh = gated ? alloc<float>((size_t)M * d) : nullptr;
+  if (gated) {
+    hipLaunchKernelGGL(fill_f32, dim3(64), dim3(256), 0, 0, fbias, (size_t)5 * d, 0.01f);
+    hipLaunchKernelGGL(fill_f32, dim3(1024), dim3(256), 0, 0, fh, (size_t)M * d, 0.5f);
+  }
   const size_t copy_n = (size_t)M * d / 4;  // float4 granules of one [M, d] float32 row block
   float* copy_dst = alloc<float>((size_t)M * d);
   HIP_OK(hipDeviceSynchronize());
@@ -278,7 +309,36 @@ int main(int argc, char** argv) {
     e.part = hpart;
     return head_sample(p, e, st);
   });
+  stage("sample", 0.0, [&]() { return sample_finalize(hpart, ng, V, row_map, canvas, B, L, 0, V, choice, conf, st); });
+  if (gated) {
+    stage("fusion1", 2.0 * M * 5.0 * d * 2 * d, [&]() {
+      GemmProblem p{M, 5 * d, 2 * d, xn, d, d, fa, d, w1g, 2 * d};
+      EpiParams e;
+      e.out = fus_h;
+      e.ldo = 4 * d;
+      e.bias = fbias;
+      e.out2 = fus_g;
+      e.ldo2 = d;
+      e.split = 4 * d;
+      return gemm(BF16, p, EPI_FUSION1, e, st);
+    });
+    stage("fusion2", 2.0 * M * d * 4.0 * d, [&]() {
+      GemmProblem p{M, d, 4 * d, fus_h, 4 * d, 4 * d, nullptr, 0, w2, 4 * d};
+      EpiParams e;
+      e.resid = x;
+      e.ldr = d;
+      e.bias = fbias;
+      e.aux = fh;
+      e.ld_aux = d;
+      e.gate = fus_g;
+      e.ldg = d;
+      return gemm(BF16, p, EPI_FUSION2, e, st);
+    });
+  }
   HIP_OK(hipStreamSynchronize(st));
+  for (void* p : {(void*)row_map, (void*)canvas, (void*)choice, (void*)conf, (void*)fa, (void*)w1g, (void*)w2,
+                  (void*)fus_h, (void*)fus_g, (void*)fbias, (void*)fh})
+    if (p) HIP_OK(hipFree(p));
   for (void* p : {(void*)xn, (void*)wqkv, (void*)wo, (void*)wup, (void*)wdown, (void*)ao, (void*)ffn, (void*)q,
                   (void*)kc, (void*)vt, (void*)x, (void*)rope, (void*)part, (void*)copy_dst, (void*)gain,
                   (void*)xn2, (void*)wout, (void*)hidx, (void*)hpart})
