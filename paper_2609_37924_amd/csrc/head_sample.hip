@@ -145,7 +145,12 @@ struct Epi<EPI_SAMPLE, T> {
   }
 };
 
-// grid (Lc, B), 256 threads: one workgroup per canvas position.
+// groups a finalize thread merges at most (n_groups <= SAMPLE_MAX_VOCAB / 64, 256 threads)
+constexpr int FIN_GROUPS = SAMPLE_MAX_VOCAB / 64 / 256;
+
+// grid (Lc, B), 256 threads: one workgroup per canvas position.  A thread reads each of
+// its groups' partials once and keeps m_g and S_g in registers for the normaliser pass
+// (reading them again missed the L2 for wide rows: 2x the partial bytes fetched).
 __global__ __launch_bounds__(256) void finalize_kernel(const SamplePart* part, int n_groups, int V,
                                                        const int32_t* row_map, const int32_t* canvas, int L,
                                                        int off, int Lc, int mask_id, int32_t* choice,
@@ -165,11 +170,19 @@ __global__ __launch_bounds__(256) void finalize_kernel(const SamplePart* part, i
   }
   const SamplePart* P = part + (size_t)row_map[row] * n_groups;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  float mx = -INFINITY;
+  float mx = -INFINITY, gm[FIN_GROUPS];
+  long long gS[FIN_GROUPS];
   Cand best{-INFINITY, 0x7FFFFFFF, 0.f};
-  for (int g = tid; g < n_groups; g += 256) {
-    mx = fmaxf(mx, P[g].m);
-    best = better_cand(best, Cand{P[g].score, P[g].v, P[g].lp});
+#pragma unroll
+  for (int i = 0; i < FIN_GROUPS; ++i) {
+    const int g = tid + 256 * i;
+    if (g < n_groups) {
+      const SamplePart q = P[g];
+      gm[i] = q.m;
+      gS[i] = q.S;
+      mx = fmaxf(mx, q.m);
+      best = better_cand(best, Cand{q.score, q.v, q.lp});
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -183,7 +196,9 @@ __global__ __launch_bounds__(256) void finalize_kernel(const SamplePart* part, i
   __syncthreads();
   mx = fmaxf(fmaxf(s_m[0], s_m[1]), fmaxf(s_m[2], s_m[3]));
   long long S = 0;
-  for (int g = tid; g < n_groups; g += 256) S += (long long)rintf((float)P[g].S * own_exp(P[g].m - mx));
+#pragma unroll
+  for (int i = 0; i < FIN_GROUPS; ++i)
+    if (tid + 256 * i < n_groups) S += (long long)rintf((float)gS[i] * own_exp(gm[i] - mx));
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) S += __shfl_xor(S, o, 64);
   if (lane == 0) s_S[wave] = S;
@@ -217,6 +232,7 @@ hipError_t sample_finalize(const SamplePart* part, int n_groups, int V, const in
                            float* conf, hipStream_t s) {
   const int Lc = L - canvas_off;
   if (B * Lc == 0) return hipSuccess;
+  if (n_groups > FIN_GROUPS * 256) return hipErrorInvalidValue;
   launch_timed(finalize_kernel, dim3(Lc, B), dim3(256), 0, s, part, n_groups, V, row_map, canvas, L, canvas_off, Lc,
                mask_id, choice, conf);
   return hipGetLastError();
